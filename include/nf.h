@@ -1,0 +1,160 @@
+/*
+ * nf.h - C ABI of the MI355X (gfx950) library for mini-batch training of
+ * fully connected feed-forward networks, after Curcic, "A parallel Fortran
+ * framework for neural networks and deep learning" (arXiv:1902.06714).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All real data is IEEE fp32 (the paper's default real32 kind, section 3.1).
+ * - Batches are row-major: a batch of B samples of width d is B rows of d
+ *   contiguous floats, sample after sample.  This is byte-identical to the
+ *   paper's column-major x(d, B) (section 3.4, batch training).
+ * - Canonical parameter order: for l = 1..L (L = n_dims - 1 layers after the
+ *   input), the weights W_l as a row-major [d_l][d_{l-1}] array (row j holds
+ *   the weights from every unit of layer l-1 into unit j of layer l), then the
+ *   biases b_l[d_l].  The paper stores w(this, next) column-major on the
+ *   source layer (section 3.1, layer definition), which has the same bytes.
+ *   The paper's unused input-layer biases and last-layer weights are not
+ *   stored.  The device layout is private; get/set convert.
+ * - Pointers named d_* are device pointers on the net's device; pointers named
+ *   host_* are host memory.  The caller owns all of them; the library never
+ *   frees or retains them past the call.
+ * - `stream` is a hipStream_t passed as void* (NULL means the default stream).
+ *   Compute calls only enqueue work on that stream and return; the caller
+ *   keeps the inputs alive and unmodified until the stream reaches that work.
+ * - Every call returns an nf_status.  On error nothing has been enqueued, the
+ *   net is unchanged, and nf_last_error() gives a message for this thread.
+ *   No C++ exception crosses the ABI.
+ * - A net is not thread-safe: calls on one net must not overlap.
+ */
+#ifndef NF_H
+#define NF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Opaque network: owned by the library, created by nf_net_create. */
+typedef struct nf_net nf_net;
+
+/* The activation functions of section 2 (Gaussian, RELU, sigmoid, step,
+ * tangent hyperbolic).  f and its derivative f' (taken at the stored
+ * pre-activation z, section 3.3):
+ *   NF_GAUSSIAN  exp(-z^2)            -2 z exp(-z^2)
+ *   NF_RELU      max(0, z)            1 if z > 0 else 0
+ *   NF_SIGMOID   1 / (1 + exp(-z))    sigma(z) sigma(-z)   (section 3.1)
+ *   NF_STEP      1 if z > 0 else 0    0
+ *   NF_TANH      tanh(z)              1 - tanh(z)^2                         */
+typedef enum {
+  NF_GAUSSIAN = 0,
+  NF_RELU = 1,
+  NF_SIGMOID = 2,
+  NF_STEP = 3,
+  NF_TANH = 4
+} nf_act;
+
+typedef enum {
+  NF_OK = 0,
+  NF_EINVAL = -1,  /* bad argument: NULL pointer, bad enum, count <= 0 ...   */
+  NF_ESHAPE = -2,  /* sizes that do not fit the net or each other           */
+  NF_ENOMEM = -3,  /* device or host allocation failed                      */
+  NF_EDEVICE = -4  /* a HIP runtime call failed (includes "no GPU")         */
+} nf_status;
+
+/* Create a network (the network constructor of section 3.1).
+ * dims[0..n_dims-1]: units per layer including input and output layers,
+ *   n_dims >= 2, every entry in 1 .. 65536.
+ * acts[0..n_acts-1]: nf_act values.  n_acts = 0: sigmoid on every layer (the
+ *   paper's default); n_acts = 1: that activation on every layer (the paper's
+ *   case); n_acts = n_dims - 1: one per layer after the input.
+ * The net lives on the HIP device current at the call.  Its parameters start
+ * at zero: load them with nf_set_params (the single-GPU stand-in for the
+ * broadcast of initial parameters, section 3.5).
+ * *out receives the handle; it is set only on success. */
+nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts,
+                        int32_t n_acts, nf_net** out);
+
+/* Destroy a network; waits for its outstanding work.  NULL is a no-op. */
+nf_status nf_net_destroy(nf_net* net);
+
+/* Number of floats in the canonical parameter vector:
+ * sum over l of d_l * d_{l-1} + d_l.  Returns -1 for NULL. */
+int64_t nf_param_count(const nf_net* net);
+
+/* Copy n = nf_param_count(net) floats in canonical order from host memory
+ * into the net.  Waits for the net's outstanding work first; returns after
+ * the copy is complete. */
+nf_status nf_set_params(nf_net* net, const float* host_src, int64_t n);
+
+/* Copy the current parameters, canonical order, into host memory (n floats).
+ * Waits for the net's outstanding work. */
+nf_status nf_get_params(nf_net* net, float* host_dst, int64_t n);
+
+/* Copy the tendencies of the most recent nf_train_batch step (the weight and
+ * bias gradients of the quadratic cost summed over the whole mini-batch,
+ * before scaling by eta/B; section 3.3-3.5) into host memory, canonical order,
+ * n floats.  Zero before the first step.  Waits for outstanding work. */
+nf_status nf_get_grads(nf_net* net, float* host_dst, int64_t n);
+
+/* Batched inference: the network output for every sample, storing nothing in
+ * the net (the output function of section 3.2).
+ * d_x: [batch][d_0] input, d_out: [batch][d_L] output; batch >= 1. */
+nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out,
+                     void* stream);
+
+/* One SGD step on one mini-batch (sections 3.2-3.5):
+ * forward propagation of every sample, the output delta
+ * (a_L - y) f'(z_L), the hidden deltas (W_{l+1}^T delta_{l+1}) f'(z_l) with
+ * the weights from before this step, the weight and bias tendencies summed
+ * over the batch, and W_l -= (eta / batch) * sum, b_l -= (eta / batch) * sum.
+ * n_shards >= 1 splits the batch into that many equal contiguous pieces
+ * whose tendencies are formed separately and added in piece order (the
+ * collective sum of section 3.5, on one GPU); batch % n_shards must be 0.
+ * d_x: [batch][d_0] inputs, d_y: [batch][d_L] targets (one-hot for
+ * classification). */
+nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_t batch,
+                         float eta, int32_t n_shards, void* stream);
+
+/* Consecutive mini-batches: samples [t*batch, (t+1)*batch) for
+ * t = 0 .. n_samples/batch - 1, one nf_train_batch step each, in order
+ * (the epoch loop of section 4 without the random window).  n_samples must be
+ * a positive multiple of batch. */
+nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
+                         int64_t batch, float eta, int32_t n_shards, void* stream);
+
+/* Per-kernel timing, for measuring the method's computational performance the
+ * way section 5 reports it (elapsed time), one kernel at a time.  While
+ * recording is on, every kernel the net launches is bracketed by a pair of HIP
+ * events on its stream, and the library notes the algorithmic bytes the
+ * kernel must move (inputs read once, outputs written once) and the flops of
+ * its contraction (2 per multiply-add, no padding).  Recording costs a little
+ * time per launch; leave it off for throughput runs. */
+typedef struct {
+  char name[64];      /* kernel family, e.g. "gemm_fwd_stash_128x128" */
+  int64_t launches;   /* launches recorded since the last read             */
+  double total_ms;    /* sum of the event-measured durations (ms)          */
+  double bytes;       /* algorithmic bytes, summed over the launches       */
+  double flops;       /* algorithmic flops, summed over the launches       */
+} nf_kernel_stat;
+
+/* Turn recording on (enable != 0) or off.  Turning it on discards anything
+ * recorded and not yet read. */
+nf_status nf_profile(nf_net* net, int32_t enable);
+
+/* Wait for the recorded work, then write one entry per kernel name (at most
+ * cap entries, ordered by total time, largest first) to out[] and their number
+ * to *count; the records are then cleared. */
+nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t* count);
+
+/* Message for the last failed call on this thread ("" if none).  The pointer
+ * stays valid until the next nf_* call on the same thread. */
+const char* nf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NF_H */

@@ -234,26 +234,39 @@ def cost(theta, dims, acts, X, Y) -> float:
     return 0.5 * float(np.sum(d * d))
 
 
-def piece_gradient(theta, dims, acts, X, Y) -> np.ndarray:
+def _kink_side(name: str, Z: np.ndarray, fp: np.ndarray, kink_tol: float) -> np.ndarray:
+    """The other admissible derivative for relu units whose pre-activation lies
+    within kink_tol * rms(z of the layer) of the kink at zero: a computation
+    that rounds z may land on either side, and both results are correct."""
+    if kink_tol <= 0.0 or name != "relu":
+        return fp
+    near = np.abs(Z) <= kink_tol * np.sqrt(np.mean(Z * Z))
+    return np.where(near, 1.0 - fp, fp)
+
+
+def piece_gradient(theta, dims, acts, X, Y, kink_tol: float = 0.0) -> np.ndarray:
     """Tendencies summed over the samples of one piece of a batch: for each
     layer, sum over samples s of delta_s (outer) a_s, and sum of delta_s.
-    The delta recurrences are the single-sample ones, applied to each row."""
+    The delta recurrences are the single-sample ones, applied to each row.
+    kink_tol > 0 takes the other side of the relu kink for units within that
+    relative distance of it (used to measure how much a result depends on
+    those undetermined decisions; 0 is the method itself)."""
     acts = _check_acts(acts, dims)
     layers = unpack(theta, dims)
     L = len(layers)
     Z, A = forward(theta, dims, acts, X)
     Yd = np.asarray(Y, dtype=np.float64)
     parts: List[Tuple[np.ndarray, np.ndarray]] = [None] * L
-    D = (A[L] - Yd) * act_prime(acts[L - 1], Z[L])          # [B][d_L]
+    D = (A[L] - Yd) * _kink_side(acts[L - 1], Z[L], act_prime(acts[L - 1], Z[L]), kink_tol)
     for l in range(L - 1, -1, -1):
         parts[l] = (D.T @ A[l], D.sum(axis=0))              # sum_s delta_s a_s^T, sum_s delta_s
         if l > 0:
             W = layers[l][0]
-            D = (D @ W) * act_prime(acts[l - 1], Z[l])      # row s: W^T delta_s times f'(z_s)
+            D = (D @ W) * _kink_side(acts[l - 1], Z[l], act_prime(acts[l - 1], Z[l]), kink_tol)
     return pack(parts)
 
 
-def batch_gradient(theta, dims, acts, X, Y, shards: int = 1) -> np.ndarray:
+def batch_gradient(theta, dims, acts, X, Y, shards: int = 1, kink_tol: float = 0.0) -> np.ndarray:
     """Tendencies summed over the whole mini-batch.  The batch is split into
     `shards` equal contiguous pieces whose sums are added in piece order, the
     single-process picture of the collective sum of section 3.5."""
@@ -264,16 +277,18 @@ def batch_gradient(theta, dims, acts, X, Y, shards: int = 1) -> np.ndarray:
     per = B // shards
     total = None
     for k in range(shards):
-        gk = piece_gradient(theta, dims, acts, X[k * per:(k + 1) * per], Y[k * per:(k + 1) * per])
+        gk = piece_gradient(theta, dims, acts, X[k * per:(k + 1) * per], Y[k * per:(k + 1) * per],
+                            kink_tol)
         total = gk if total is None else total + gk
     return total
 
 
-def train_batch(theta, dims, acts, X, Y, eta, shards: int = 1, precision="f32"):
+def train_batch(theta, dims, acts, X, Y, eta, shards: int = 1, precision="f32",
+                kink_tol: float = 0.0):
     """One SGD step on a mini-batch: theta - (eta / B) * (summed tendencies).
     Returns (new theta, summed tendencies in fp64)."""
     B = np.asarray(X).shape[0]
-    g = batch_gradient(theta, dims, acts, X, Y, shards)
+    g = batch_gradient(theta, dims, acts, X, Y, shards, kink_tol)
     new = np.asarray(theta, dtype=np.float64) - (eta / B) * g
     return _round(new, precision), g
 

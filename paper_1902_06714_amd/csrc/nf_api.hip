@@ -1,0 +1,657 @@
+// Host runtime behind include/nf.h: argument validation, the device layout of
+// a network, its workspace, and the launch sequence of one training step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "nf.h"
+#include "nf_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+nf_status fail(nf_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+nf_status hip_fail(hipError_t e, const char* what) {
+  return fail(NF_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr int64_t kAlign = 64;  // floats (256 bytes) between tensors
+
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+struct LayerLayout {
+  int in = 0, out = 0, act = 0;
+  int64_t ldw = 0;    // row pitch of W_l (floats), multiple of 4; padding is zero
+  int64_t w_off = 0;  // offsets in floats inside the parameter / tendency buffers
+  int64_t b_off = 0;
+  int64_t lda = 0;    // row pitch of the per-sample buffers of this layer
+};
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    ok = (prev == dev) || hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+struct nf_net {
+  int device = 0;
+  std::vector<int> dims;
+  std::vector<LayerLayout> layers;
+  int64_t n_params = 0;       // canonical floats
+  int64_t dev_floats = 0;     // device layout floats
+  float* params = nullptr;    // device layout
+  float* grads = nullptr;     // device layout, tendencies of the last step
+  // workspace for up to ws_batch samples
+  int64_t ws_batch = 0;
+  float* ws = nullptr;
+  std::vector<float*> actv;   // actv[l]: f(z_l) [B][lda_l], l = 1..L-1
+  std::vector<float*> fbuf;   // fbuf[l]: f'(z_l), overwritten by delta_l, l = 1..L
+  // per-piece tendencies
+  float* partial = nullptr;
+  int64_t partial_floats = 0;
+  hipStream_t last = nullptr;
+  bool used = false;
+  // per-kernel timing (nf_profile)
+  struct Rec {
+    const char* name;
+    hipEvent_t a, b;
+    double bytes, flops;
+  };
+  bool prof = false;
+  std::vector<Rec> recs;
+};
+
+namespace {
+
+int num_layers(const nf_net* n) { return (int)n->dims.size() - 1; }
+
+nf_status sync_net(nf_net* n) {
+  if (!n->used) return NF_OK;
+  hipError_t e = hipStreamSynchronize(n->last);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  return NF_OK;
+}
+
+void free_ws(nf_net* n) {
+  if (n->ws) (void)hipFree(n->ws);
+  n->ws = nullptr;
+  n->ws_batch = 0;
+  n->actv.assign(n->dims.size(), nullptr);
+  n->fbuf.assign(n->dims.size(), nullptr);
+}
+
+// Make room for `batch` samples.  Growing waits for the net's earlier work,
+// which may still read the old buffers.
+nf_status ensure_ws(nf_net* n, int64_t batch) {
+  if (batch <= n->ws_batch) return NF_OK;
+  nf_status st = sync_net(n);
+  if (st != NF_OK) return st;
+  const int L = num_layers(n);
+  int64_t total = 0;
+  std::vector<int64_t> aoff(L + 1, -1), foff(L + 1, -1);
+  for (int l = 1; l <= L; ++l) {
+    const int64_t sz = round_up(batch * n->layers[l].lda, kAlign);
+    if (l < L) {
+      aoff[l] = total;
+      total += sz;
+    }
+    foff[l] = total;
+    total += sz;
+  }
+  float* buf = nullptr;
+  hipError_t e = hipMalloc(&buf, (size_t)total * sizeof(float));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(NF_ENOMEM, "hipMalloc of the workspace failed: " + std::string(hipGetErrorString(e)));
+  }
+  e = hipMemset(buf, 0, (size_t)total * sizeof(float));  // pitch padding must read as zero
+  if (e != hipSuccess) {
+    (void)hipFree(buf);
+    return hip_fail(e, "hipMemset");
+  }
+  free_ws(n);
+  n->ws = buf;
+  n->ws_batch = batch;
+  for (int l = 1; l <= L; ++l) {
+    n->actv[l] = aoff[l] >= 0 ? buf + aoff[l] : nullptr;
+    n->fbuf[l] = buf + foff[l];
+  }
+  return NF_OK;
+}
+
+nf_status ensure_partial(nf_net* n, int64_t floats) {
+  if (floats <= n->partial_floats) return NF_OK;
+  nf_status st = sync_net(n);
+  if (st != NF_OK) return st;
+  float* buf = nullptr;
+  hipError_t e = hipMalloc(&buf, (size_t)floats * sizeof(float));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(NF_ENOMEM, "hipMalloc of the piece buffer failed");
+  }
+  if (n->partial) (void)hipFree(n->partial);
+  n->partial = buf;
+  n->partial_floats = floats;
+  return NF_OK;
+}
+
+bool vec_ok(const float* p, int64_t ld) {
+  return ld % 4 == 0 && (reinterpret_cast<uintptr_t>(p) & 15) == 0;
+}
+
+int pick_tile(int64_t M, int64_t N, int64_t splits) {
+  const int64_t big = ((M + 127) / 128) * ((N + 127) / 128) * splits;
+  return big >= 256 ? nf::TILE_128x128 : nf::TILE_64x64;
+}
+
+void clear_recs(nf_net* n) {
+  for (auto& r : n->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  n->recs.clear();
+}
+
+// Runs `enqueue` on stream s; with recording on, brackets it with events.
+template <class F>
+nf_status timed(nf_net* n, const char* name, double bytes, double flops, hipStream_t s,
+                F&& enqueue) {
+  nf_net::Rec r{name, nullptr, nullptr, bytes, flops};
+  if (n->prof) {
+    hipError_t e = hipEventCreate(&r.a);
+    if (e == hipSuccess) e = hipEventCreate(&r.b);
+    if (e == hipSuccess) e = hipEventRecord(r.a, s);
+    if (e != hipSuccess) return hip_fail(e, "profiling event");
+  }
+  hipError_t e = enqueue();
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  if (n->prof) {
+    e = hipEventRecord(r.b, s);
+    if (e != hipSuccess) return hip_fail(e, "profiling event");
+    n->recs.push_back(r);
+  }
+  return NF_OK;
+}
+
+// Algorithmic bytes of one contraction launch: each operand read once, each
+// result written once (4 bytes per float).
+double gemm_bytes(int epi, const nf::GemmParams& p, int nsplit) {
+  const double M = p.M, N = p.N, K = p.K;
+  switch (epi) {
+    case nf::EPI_FWD_STASH: return 4.0 * (M * K + N * K + N + 2 * M * N);
+    case nf::EPI_FWD_DELTA: return 4.0 * (M * K + N * K + N + 2 * M * N);
+    case nf::EPI_FWD_OUT: return 4.0 * (M * K + N * K + N + M * N);
+    case nf::EPI_BWD: return 4.0 * (M * K + K * N + 2 * M * N);
+    case nf::EPI_DW_SGD: return 4.0 * (K * M + K * N + 3 * M * N + 3 * M);
+    default: return 4.0 * (K * M + K * N + nsplit * (M * N + M));
+  }
+}
+
+nf_status launch(nf_net* n, int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
+                 const nf::GemmParams& p, hipStream_t s) {
+  const int tile = pick_tile(p.M, p.N, nsplit);
+  return timed(n, nf::gemm_name(epi, tile), gemm_bytes(epi, p, nsplit),
+               2.0 * p.M * (double)p.N * p.K, s,
+               [&] { return nf::launch_gemm(epi, tile, akc, bkc, av, bv, nsplit, p, s); });
+}
+
+// Forward propagation of `batch` samples through every layer (section 3.2).
+// train: keep f(z_l) and f'(z_l) for back-propagation and finish with the
+// output delta; otherwise write f(z_L) to `out`.
+nf_status run_forward(nf_net* n, const float* x, const float* y, int64_t batch, float* out,
+                      bool train, hipStream_t s) {
+  const int L = num_layers(n);
+  for (int l = 1; l <= L; ++l) {
+    const LayerLayout& ly = n->layers[l];
+    nf::GemmParams p{};
+    p.A = l == 1 ? x : n->actv[l - 1];
+    p.lda = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
+    p.B = n->params + ly.w_off;
+    p.ldb = ly.ldw;
+    p.M = (int)batch;
+    p.N = ly.out;
+    p.K = ly.in;
+    p.nsub = 1;
+    p.bias = n->params + ly.b_off;
+    p.act = ly.act;
+    const bool av = l == 1 ? vec_ok(x, n->dims[0]) : true;
+    int epi;
+    if (train) {
+      if (l < L) {
+        epi = nf::EPI_FWD_STASH;
+        p.out0 = n->actv[l];
+        p.ld0 = ly.lda;
+        p.out1 = n->fbuf[l];
+        p.ld1 = ly.lda;
+      } else {
+        epi = nf::EPI_FWD_DELTA;
+        p.aux = y;
+        p.ldaux = ly.out;
+        p.out0 = n->fbuf[l];
+        p.ld0 = ly.lda;
+      }
+    } else {
+      epi = nf::EPI_FWD_OUT;
+      if (l < L) {
+        p.out0 = n->actv[l];
+        p.ld0 = ly.lda;
+      } else {
+        p.out0 = out;
+        p.ld0 = ly.out;
+      }
+    }
+    nf_status st = launch(n, epi, true, true, av, true, 1, p, s);
+    if (st != NF_OK) return st;
+  }
+  return NF_OK;
+}
+
+// Back-propagation and the SGD step (sections 3.3-3.5).  Layer l's weights are
+// updated only after delta_{l-1}, which reads them, has been formed.
+nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float eta, int shards,
+                              hipStream_t s) {
+  const int L = num_layers(n);
+  const float scale = (float)((double)eta / (double)batch);
+  const int64_t shard_len = batch / shards;
+  for (int l = L; l >= 1; --l) {
+    const LayerLayout& ly = n->layers[l];
+    if (l > 1) {
+      // delta_{l-1} = (delta_l W_l) * f'(z_{l-1}), in place over f'(z_{l-1})
+      const LayerLayout& lp = n->layers[l - 1];
+      nf::GemmParams p{};
+      p.A = n->fbuf[l];
+      p.lda = ly.lda;
+      p.B = n->params + ly.w_off;
+      p.ldb = ly.ldw;
+      p.M = (int)batch;
+      p.N = lp.out;
+      p.K = ly.out;
+      p.nsub = 1;
+      p.aux = n->fbuf[l - 1];
+      p.ldaux = lp.lda;
+      p.out0 = n->fbuf[l - 1];
+      p.ld0 = lp.lda;
+      nf_status st = launch(n, nf::EPI_BWD, true, false, true, true, 1, p, s);
+      if (st != NF_OK) return st;
+    }
+    // tendencies of layer l: G = delta_l^T A_{l-1}, g = sum of delta_l rows
+    const float* aprev = l == 1 ? x : n->actv[l - 1];
+    const int64_t ldprev = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
+    const bool bv = l == 1 ? vec_ok(x, n->dims[0]) : true;
+    const int64_t M = ly.out, N = ly.in;
+    // pieces: every shard is cut into nsub sub-pieces when the tile grid alone
+    // would leave most compute units idle
+    int nsub = 1;
+    {
+      const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+      const int64_t want = 256;
+      while (tiles * shards * nsub < want && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
+             (int64_t)shards * nsub * 2 <= 65535)
+        nsub *= 2;
+    }
+    const int64_t sub_len = (shard_len + nsub - 1) / nsub;
+    const int nsplit = shards * nsub;
+    nf::GemmParams p{};
+    p.A = n->fbuf[l];
+    p.lda = ly.lda;
+    p.B = aprev;
+    p.ldb = ldprev;
+    p.M = (int)M;
+    p.N = (int)N;
+    p.K = (int)batch;
+    p.nsub = nsub;
+    p.shard_len = (int)shard_len;
+    p.sub_len = (int)sub_len;
+    p.scale = scale;
+    if (nsplit == 1) {
+      p.out0 = n->grads + ly.w_off;
+      p.ld0 = ly.ldw;
+      p.W = n->params + ly.w_off;
+      p.ldw = ly.ldw;
+      p.bvec = n->params + ly.b_off;
+      p.gbias = n->grads + ly.b_off;
+      nf_status st = launch(n, nf::EPI_DW_SGD, false, false, true, bv, 1, p, s);
+      if (st != NF_OK) return st;
+    } else {
+      const int64_t pstride = round_up(M * ly.ldw, kAlign);
+      nf_status st = ensure_partial(n, (int64_t)nsplit * (pstride + round_up(M, kAlign)));
+      if (st != NF_OK) return st;
+      p.partial = n->partial;
+      p.pstride = pstride;
+      p.ld0 = ly.ldw;
+      p.pbias = n->partial + (int64_t)nsplit * pstride;
+      st = launch(n, nf::EPI_DW_PARTIAL, false, false, true, bv, nsplit, p, s);
+      if (st != NF_OK) return st;
+      const double elems = (double)M * N + M;
+      st = timed(n, "fold_sgd", 4.0 * elems * (nsplit + 3), elems * (nsplit + 1), s, [&] {
+        return nf::launch_fold_sgd(p.partial, pstride, p.pbias, shards, nsub, (int)M, (int)N,
+                                   ly.ldw, n->grads + ly.w_off, n->grads + ly.b_off,
+                                   n->params + ly.w_off, n->params + ly.b_off, scale, s);
+      });
+      if (st != NF_OK) return st;
+    }
+  }
+  return NF_OK;
+}
+
+nf_status check_net(const nf_net* n) {
+  if (!n) return fail(NF_EINVAL, "net is NULL");
+  return NF_OK;
+}
+
+nf_status train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
+                     int shards, hipStream_t s) {
+  nf_status st = run_forward(n, x, y, batch, nullptr, true, s);
+  if (st != NF_OK) return st;
+  return run_backward_update(n, x, batch, eta, shards, s);
+}
+
+nf_status check_train_args(const nf_net* n, const float* x, const float* y, int64_t batch,
+                           float eta, int32_t shards) {
+  if (!x || !y) return fail(NF_EINVAL, "x or y is NULL");
+  if (batch <= 0) return fail(NF_EINVAL, "batch must be positive");
+  if (batch > (int64_t)1 << 30) return fail(NF_ESHAPE, "batch is too large");
+  if (shards < 1) return fail(NF_EINVAL, "n_shards must be at least 1");
+  if (shards > 65535) return fail(NF_ESHAPE, "n_shards must be at most 65535");
+  if (batch % shards != 0) return fail(NF_ESHAPE, "batch must split evenly into n_shards pieces");
+  if (!(eta == eta) || eta == __builtin_inff() || eta == -__builtin_inff())
+    return fail(NF_EINVAL, "eta must be finite");
+  (void)n;
+  return NF_OK;
+}
+
+template <class F>
+nf_status guarded(F&& f) {
+  try {
+    g_err.clear();
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(NF_ENOMEM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(NF_EINVAL, std::string("internal error: ") + e.what());
+  } catch (...) {
+    return fail(NF_EINVAL, "internal error");
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32_t n_acts,
+                        nf_net** out) {
+  return guarded([&]() -> nf_status {
+    if (!out) return fail(NF_EINVAL, "out is NULL");
+    if (!dims) return fail(NF_EINVAL, "dims is NULL");
+    if (n_dims < 2) return fail(NF_ESHAPE, "need at least an input and an output layer");
+    if (n_dims > 1024) return fail(NF_ESHAPE, "too many layers");
+    for (int i = 0; i < n_dims; ++i)
+      if (dims[i] < 1 || dims[i] > 65536) return fail(NF_ESHAPE, "layer sizes must be in 1..65536");
+    if (n_acts != 0 && n_acts != 1 && n_acts != n_dims - 1)
+      return fail(NF_ESHAPE, "n_acts must be 0, 1 or n_dims - 1");
+    if (n_acts > 0 && !acts) return fail(NF_EINVAL, "acts is NULL");
+    for (int i = 0; i < n_acts; ++i)
+      if (acts[i] < NF_GAUSSIAN || acts[i] > NF_TANH) return fail(NF_EINVAL, "unknown activation");
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return hip_fail(e, "no usable HIP device");
+    }
+    nf_net* n = new nf_net();
+    n->device = dev;
+    n->dims.assign(dims, dims + n_dims);
+    n->layers.resize(n_dims);
+    int64_t off = 0, canon = 0;
+    for (int l = 1; l < n_dims; ++l) {
+      LayerLayout& ly = n->layers[l];
+      ly.in = dims[l - 1];
+      ly.out = dims[l];
+      ly.act = n_acts == 0 ? NF_SIGMOID : (n_acts == 1 ? acts[0] : acts[l - 1]);
+      ly.ldw = round_up(ly.in, 4);
+      ly.w_off = off;
+      off = round_up(off + (int64_t)ly.out * ly.ldw, kAlign);
+      ly.b_off = off;
+      off = round_up(off + ly.out, kAlign);
+      ly.lda = round_up(ly.out, 4);
+      canon += (int64_t)ly.out * ly.in + ly.out;
+    }
+    n->n_params = canon;
+    n->dev_floats = off;
+    n->actv.assign(n_dims, nullptr);
+    n->fbuf.assign(n_dims, nullptr);
+    e = hipMalloc(&n->params, (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&n->grads, (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(n->params, 0, (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(n->grads, 0, (size_t)off * sizeof(float));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      if (n->params) (void)hipFree(n->params);
+      if (n->grads) (void)hipFree(n->grads);
+      delete n;
+      return fail(e == hipErrorOutOfMemory ? NF_ENOMEM : NF_EDEVICE,
+                  std::string("device allocation failed: ") + hipGetErrorString(e));
+    }
+    *out = n;
+    return NF_OK;
+  });
+}
+
+nf_status nf_net_destroy(nf_net* net) {
+  return guarded([&]() -> nf_status {
+    if (!net) return NF_OK;
+    DeviceGuard g(net->device);
+    nf_status st = sync_net(net);
+    clear_recs(net);
+    free_ws(net);
+    if (net->partial) (void)hipFree(net->partial);
+    if (net->params) (void)hipFree(net->params);
+    if (net->grads) (void)hipFree(net->grads);
+    delete net;
+    return st;
+  });
+}
+
+int64_t nf_param_count(const nf_net* net) { return net ? net->n_params : -1; }
+
+static nf_status copy_params(nf_net* n, float* dev, const float* host_src, float* host_dst,
+                             int64_t count) {
+  if (count != n->n_params) return fail(NF_ESHAPE, "parameter count does not match the net");
+  DeviceGuard g(n->device);
+  if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+  nf_status st = sync_net(n);
+  if (st != NF_OK) return st;
+  int64_t canon = 0;
+  for (size_t l = 1; l < n->layers.size(); ++l) {
+    const LayerLayout& ly = n->layers[l];
+    const size_t wbytes = (size_t)ly.in * sizeof(float);
+    hipError_t e;
+    if (host_src) {
+      e = hipMemcpy2D(dev + ly.w_off, ly.ldw * sizeof(float), host_src + canon, wbytes, wbytes,
+                      ly.out, hipMemcpyHostToDevice);
+      if (e == hipSuccess)
+        e = hipMemcpy(dev + ly.b_off, host_src + canon + (int64_t)ly.out * ly.in,
+                      (size_t)ly.out * sizeof(float), hipMemcpyHostToDevice);
+    } else {
+      e = hipMemcpy2D(host_dst + canon, wbytes, dev + ly.w_off, ly.ldw * sizeof(float), wbytes,
+                      ly.out, hipMemcpyDeviceToHost);
+      if (e == hipSuccess)
+        e = hipMemcpy(host_dst + canon + (int64_t)ly.out * ly.in, dev + ly.b_off,
+                      (size_t)ly.out * sizeof(float), hipMemcpyDeviceToHost);
+    }
+    if (e != hipSuccess) return hip_fail(e, "parameter copy");
+    canon += (int64_t)ly.out * ly.in + ly.out;
+  }
+  return NF_OK;
+}
+
+nf_status nf_set_params(nf_net* net, const float* host_src, int64_t n) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!host_src) return fail(NF_EINVAL, "host_src is NULL");
+    return copy_params(net, net->params, host_src, nullptr, n);
+  });
+}
+
+nf_status nf_get_params(nf_net* net, float* host_dst, int64_t n) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
+    return copy_params(net, net->params, nullptr, host_dst, n);
+  });
+}
+
+nf_status nf_get_grads(nf_net* net, float* host_dst, int64_t n) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
+    return copy_params(net, net->grads, nullptr, host_dst, n);
+  });
+}
+
+nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!d_x || !d_out) return fail(NF_EINVAL, "x or out is NULL");
+    if (batch <= 0) return fail(NF_EINVAL, "batch must be positive");
+    if (batch > (int64_t)1 << 30) return fail(NF_ESHAPE, "batch is too large");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    st = run_forward(net, d_x, nullptr, batch, d_out, false, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_t batch, float eta,
+                         int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    st = train_step(net, d_x, d_y, batch, eta, n_shards, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
+                         int64_t batch, float eta, int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    if (n_samples <= 0 || n_samples % batch != 0)
+      return fail(NF_ESHAPE, "n_samples must be a positive multiple of batch");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    for (int64_t t = 0; t < n_samples / batch; ++t) {
+      st = train_step(net, d_x + t * batch * d0, d_y + t * batch * dl, batch, eta, n_shards, s);
+      if (st != NF_OK) break;
+    }
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+nf_status nf_profile(nf_net* net, int32_t enable) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    DeviceGuard g(net->device);
+    if (enable) {
+      st = sync_net(net);
+      if (st != NF_OK) return st;
+      clear_recs(net);
+    }
+    net->prof = enable != 0;
+    return NF_OK;
+  });
+}
+
+nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t* count) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!count || (cap > 0 && !out)) return fail(NF_EINVAL, "out or count is NULL");
+    if (cap < 0) return fail(NF_EINVAL, "cap must not be negative");
+    DeviceGuard g(net->device);
+    st = sync_net(net);
+    if (st != NF_OK) return st;
+    std::vector<nf_kernel_stat> agg;
+    for (const auto& r : net->recs) {
+      float ms = 0.0f;
+      hipError_t e = hipEventElapsedTime(&ms, r.a, r.b);
+      if (e != hipSuccess) {
+        clear_recs(net);
+        return hip_fail(e, "hipEventElapsedTime");
+      }
+      nf_kernel_stat* k = nullptr;
+      for (auto& a : agg)
+        if (std::strncmp(a.name, r.name, sizeof(a.name)) == 0) k = &a;
+      if (!k) {
+        agg.push_back(nf_kernel_stat{});
+        k = &agg.back();
+        std::snprintf(k->name, sizeof(k->name), "%s", r.name);
+      }
+      k->launches += 1;
+      k->total_ms += ms;
+      k->bytes += r.bytes;
+      k->flops += r.flops;
+    }
+    clear_recs(net);
+    std::sort(agg.begin(), agg.end(),
+              [](const nf_kernel_stat& a, const nf_kernel_stat& b) { return a.total_ms > b.total_ms; });
+    const int32_t n = (int32_t)std::min<size_t>(agg.size(), (size_t)cap);
+    for (int32_t i = 0; i < n; ++i) out[i] = agg[i];
+    *count = n;
+    return NF_OK;
+  });
+}
+
+const char* nf_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

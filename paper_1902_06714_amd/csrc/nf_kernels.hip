@@ -1,0 +1,384 @@
+// fp32 kernels for mini-batch MLP training on gfx950 (CDNA4).
+//
+// Every layer step of the method is one tiled contraction on the fp32 matrix
+// cores (v_mfma_f32_32x32x2_f32) with the rest of the step fused into its
+// epilogue:
+//   forward     Z = A_{l-1} W_l^T, + b_l, activation and its derivative
+//               (section 3.2, Eq. 2; f' is kept for back-propagation)
+//   output      delta_L = (f(z_L) - y) f'(z_L)   (section 3.3)
+//   backward    delta_l = (delta_{l+1} W_{l+1}) * f'(z_l)   (section 3.3)
+//   tendencies  G_l = delta_l^T A_{l-1} and g_l = column sums of delta_l,
+//               summed over the batch in a fixed order, with the SGD step
+//               W_l -= (eta/B) G_l fused in when the batch is one piece
+//               (sections 3.3-3.5)
+// Reductions run in a fixed order (each accumulator walks k upwards; pieces
+// of a split batch are added in piece order), so results are bitwise
+// reproducible from run to run.  No float atomics are used.
+#include "nf_internal.h"
+
+namespace nf {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+enum { ACT_GAUSSIAN = 0, ACT_RELU = 1, ACT_SIGMOID = 2, ACT_STEP = 3, ACT_TANH = 4 };
+
+// f(z) and f'(z) of the five activations (section 2; sigmoid from section 3.1).
+// The sigmoid and tanh derivatives are formed from exp(-|z|) so that they keep
+// their relative accuracy when the unit saturates.
+__device__ __forceinline__ void act_eval(int act, float z, float& f, float& fp) {
+  switch (act) {
+    case ACT_SIGMOID: {
+      const float e = expf(-fabsf(z));
+      const float r = 1.0f / (1.0f + e);
+      f = z >= 0.0f ? r : e * r;
+      fp = e * r * r;  // sigma(z) sigma(-z)
+      break;
+    }
+    case ACT_TANH: {
+      f = tanhf(z);
+      const float e = expf(-2.0f * fabsf(z));
+      const float r = 1.0f / (1.0f + e);
+      fp = 4.0f * e * r * r;  // 1 - tanh^2 = 4 e^{-2|z|} / (1 + e^{-2|z|})^2
+      break;
+    }
+    case ACT_RELU:
+      f = z > 0.0f ? z : 0.0f;
+      fp = z > 0.0f ? 1.0f : 0.0f;
+      break;
+    case ACT_GAUSSIAN: {
+      const float g = expf(-z * z);
+      f = g;
+      fp = -2.0f * z * g;
+      break;
+    }
+    default:  // ACT_STEP
+      f = z > 0.0f ? 1.0f : 0.0f;
+      fp = 0.0f;
+      break;
+  }
+}
+
+// Global -> register -> LDS staging of one R x BK operand tile X(r, k),
+// r in [r0, r0 + R), k in [k0, k0 + BK).  In LDS the tile is k-major,
+// lds[k * (R + 4) + r], which is the order the MFMA operand reads want.
+// KC: k is the contiguous index in memory (X[r*ld + k]), else X[k*ld + r].
+// VEC: rows are 16-byte aligned with a pitch that is a multiple of 4 and the
+// pitch padding is zero, so aligned float4 loads are safe.
+template <int R, int BK, int NT, bool KC, bool VEC>
+struct TileLoader {
+  static constexpr int SR = R + 4;
+  static constexpr int NV = VEC ? (R * BK / 4) / NT : (R * BK) / NT;
+  static_assert(VEC ? (R * BK / 4) % NT == 0 : (R * BK) % NT == 0, "tile not divisible");
+  float4 v[VEC ? NV : 1];
+  float s[VEC ? 1 : NV];
+
+  __device__ __forceinline__ void load(const float* __restrict__ X, int64_t ld, int rmax,
+                                       int kend, int r0, int k0, int tid) {
+    if constexpr (VEC) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int q = tid + i * NT;
+        int r, k;
+        if constexpr (KC) {
+          r = q / (BK / 4);
+          k = (q % (BK / 4)) * 4;
+        } else {
+          k = q / (R / 4);
+          r = (q % (R / 4)) * 4;
+        }
+        const int gr = r0 + r, gk = k0 + k;
+        if (gr < rmax && gk < kend) {
+          const float* ptr = KC ? X + (int64_t)gr * ld + gk : X + (int64_t)gk * ld + gr;
+          v[i] = *reinterpret_cast<const float4*>(ptr);
+        } else {
+          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e = tid + i * NT;
+        int r, k;
+        if constexpr (KC) {
+          r = e / BK;
+          k = e % BK;
+        } else {
+          k = e / R;
+          r = e % R;
+        }
+        const int gr = r0 + r, gk = k0 + k;
+        s[i] = (gr < rmax && gk < kend) ? (KC ? X[(int64_t)gr * ld + gk] : X[(int64_t)gk * ld + gr])
+                                        : 0.0f;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+    if constexpr (VEC) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int q = tid + i * NT;
+        if constexpr (KC) {
+          const int r = q / (BK / 4), k = (q % (BK / 4)) * 4;
+          lds[(k + 0) * SR + r] = v[i].x;
+          lds[(k + 1) * SR + r] = v[i].y;
+          lds[(k + 2) * SR + r] = v[i].z;
+          lds[(k + 3) * SR + r] = v[i].w;
+        } else {
+          const int k = q / (R / 4), r = (q % (R / 4)) * 4;
+          *reinterpret_cast<float4*>(lds + k * SR + r) = v[i];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int e = tid + i * NT;
+        int r, k;
+        if constexpr (KC) {
+          r = e / BK;
+          k = e % BK;
+        } else {
+          k = e / R;
+          r = e % R;
+        }
+        lds[k * SR + r] = s[i];
+      }
+    }
+  }
+};
+
+// C[BM x BN] tile per workgroup; (BM/WM) x (BN/WN) waves, each owning a
+// WM x WN sub-tile made of 32 x 32 MFMA blocks.  grid = (M tiles, N tiles,
+// pieces of the k range).
+template <int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV, int EPI>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_kernel(const GemmParams p) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int SA = BM + 4, SB = BN + 4;
+  __shared__ __attribute__((aligned(16))) float As[2][BK * SA];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK * SB];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = (wave % (BM / WM)) * WM;
+  const int wn = (wave / (BM / WM)) * WN;
+  const int m0 = blockIdx.x * BM;
+  const int n0 = blockIdx.y * BN;
+
+  // k range of this piece
+  int kbeg = 0, kend = p.K;
+  if constexpr (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) {
+    const int z = blockIdx.z;
+    const int shard = z / p.nsub, sub = z % p.nsub;
+    const int sb = shard * p.shard_len;
+    kbeg = sb + sub * p.sub_len;
+    kend = min(kbeg + p.sub_len, sb + p.shard_len);
+  }
+  const bool do_bias = (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) && blockIdx.y == 0;
+
+  TileLoader<BM, BK, NT, AKC, AV> la;
+  TileLoader<BN, BK, NT, BKC, BV> lb;
+
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+  float bsum = 0.0f;
+
+  const int ntiles = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (ntiles > 0) {
+    la.load(p.A, p.lda, p.M, kend, m0, kbeg, tid);
+    lb.load(p.B, p.ldb, p.N, kend, n0, kbeg, tid);
+    la.store(As[0], tid);
+    lb.store(Bs[0], tid);
+  }
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    const bool more = t + 1 < ntiles;
+    if (more) {
+      const int kn = kbeg + (t + 1) * BK;
+      la.load(p.A, p.lda, p.M, kend, m0, kn, tid);
+      lb.load(p.B, p.ldb, p.N, kend, n0, kn, tid);
+    }
+    const float* a_s = As[buf];
+    const float* b_s = Bs[buf];
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 2) {
+      float av[TM], bv[TN];
+      const int krow = kk + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) av[i] = a_s[krow * SA + wm + i * 32 + (lane & 31)];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bv[j] = b_s[krow * SB + wn + j * 32 + (lane & 31)];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (do_bias && tid < BM) {
+      // column sums of delta (the bias tendency), k in increasing order
+#pragma unroll
+      for (int kk = 0; kk < BK; ++kk) bsum += a_s[kk * SA + tid];
+    }
+    if (more) {
+      la.store(As[buf ^ 1], tid);
+      lb.store(Bs[buf ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue.  Accumulator register v of lane l in a 32x32 block holds row
+  // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of the block.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn + j * 32 + (lane & 31);
+      if (n >= p.N) continue;
+      float bn = 0.0f;
+      if constexpr (EPI == EPI_FWD_STASH || EPI == EPI_FWD_DELTA || EPI == EPI_FWD_OUT) bn = p.bias[n];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        if (m >= p.M) continue;
+        const float c = acc[i][j][v];
+        if constexpr (EPI == EPI_FWD_STASH) {
+          float f, fp;
+          act_eval(p.act, c + bn, f, fp);
+          p.out0[(int64_t)m * p.ld0 + n] = f;
+          p.out1[(int64_t)m * p.ld1 + n] = fp;
+        } else if constexpr (EPI == EPI_FWD_DELTA) {
+          float f, fp;
+          act_eval(p.act, c + bn, f, fp);
+          p.out0[(int64_t)m * p.ld0 + n] = (f - p.aux[(int64_t)m * p.ldaux + n]) * fp;
+        } else if constexpr (EPI == EPI_FWD_OUT) {
+          float f, fp;
+          act_eval(p.act, c + bn, f, fp);
+          p.out0[(int64_t)m * p.ld0 + n] = f;
+        } else if constexpr (EPI == EPI_BWD) {
+          p.out0[(int64_t)m * p.ld0 + n] = c * p.aux[(int64_t)m * p.ldaux + n];
+        } else if constexpr (EPI == EPI_DW_SGD) {
+          const int64_t o = (int64_t)m * p.ldw + n;
+          p.out0[o] = c;
+          p.W[o] = fmaf(-p.scale, c, p.W[o]);
+        } else {  // EPI_DW_PARTIAL
+          p.partial[(int64_t)blockIdx.z * p.pstride + (int64_t)m * p.ld0 + n] = c;
+        }
+      }
+    }
+  }
+  if (do_bias && tid < BM) {
+    const int m = m0 + tid;
+    if (m < p.M) {
+      if constexpr (EPI == EPI_DW_SGD) {
+        p.gbias[m] = bsum;
+        p.bvec[m] = fmaf(-p.scale, bsum, p.bvec[m]);
+      } else if constexpr (EPI == EPI_DW_PARTIAL) {
+        p.pbias[(int64_t)blockIdx.z * p.M + m] = bsum;
+      }
+    }
+  }
+}
+
+// Sum of the per-piece tendencies in piece order, then the SGD step.
+__global__ void fold_sgd_kernel(const float* __restrict__ partial, int64_t pstride,
+                                const float* __restrict__ pbias, int nshards, int nsub, int M,
+                                int N, int64_t ldw, float* __restrict__ G,
+                                float* __restrict__ gbias, float* __restrict__ W,
+                                float* __restrict__ b, float scale) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nw = (int64_t)M * N;
+  if (idx < nw) {
+    const int m = (int)(idx / N), n = (int)(idx % N);
+    const int64_t o = (int64_t)m * ldw + n;
+    float tot = 0.0f;
+    for (int s = 0; s < nshards; ++s) {
+      float piece = partial[(int64_t)(s * nsub) * pstride + o];
+      for (int q = 1; q < nsub; ++q) piece += partial[(int64_t)(s * nsub + q) * pstride + o];
+      tot = s == 0 ? piece : tot + piece;
+    }
+    G[o] = tot;
+    W[o] = fmaf(-scale, tot, W[o]);
+  } else if (idx < nw + M) {
+    const int m = (int)(idx - nw);
+    float tot = 0.0f;
+    for (int s = 0; s < nshards; ++s) {
+      float piece = pbias[(int64_t)(s * nsub) * M + m];
+      for (int q = 1; q < nsub; ++q) piece += pbias[(int64_t)(s * nsub + q) * M + m];
+      tot = s == 0 ? piece : tot + piece;
+    }
+    gbias[m] = tot;
+    b[m] = fmaf(-scale, tot, b[m]);
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV, int EPI>
+static hipError_t launch_one(int nsplit, const GemmParams& p, hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, nsplit);
+  gemm_kernel<BM, BN, BK, WM, WN, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int WM, int WN>
+static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
+                                const GemmParams& p, hipStream_t s) {
+#define NF_CASE(AKC, BKC, AV, BV, E)                                     \
+  if (akc == AKC && bkc == BKC && av == AV && bv == BV && epi == E)      \
+    return launch_one<BM, BN, BK, WM, WN, AKC, BKC, AV, BV, E>(nsplit, p, s);
+  // forward: A = activations [m][k], B(k, n) = W[n][k]
+  NF_CASE(true, true, true, true, EPI_FWD_STASH)
+  NF_CASE(true, true, false, true, EPI_FWD_STASH)
+  NF_CASE(true, true, true, true, EPI_FWD_DELTA)
+  NF_CASE(true, true, false, true, EPI_FWD_DELTA)
+  NF_CASE(true, true, true, true, EPI_FWD_OUT)
+  NF_CASE(true, true, false, true, EPI_FWD_OUT)
+  // backward: A = delta [m][k], B(k, n) = W[k][n]
+  NF_CASE(true, false, true, true, EPI_BWD)
+  // tendencies: A(m, k) = delta[k][m], B(k, n) = activations[k][n]
+  NF_CASE(false, false, true, true, EPI_DW_SGD)
+  NF_CASE(false, false, true, false, EPI_DW_SGD)
+  NF_CASE(false, false, true, true, EPI_DW_PARTIAL)
+  NF_CASE(false, false, true, false, EPI_DW_PARTIAL)
+#undef NF_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec, bool b_vec,
+                       int nsplit, const GemmParams& p, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
+  if (tile == TILE_128x128)
+    return dispatch_tile<128, 128, 16, 64, 64>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
+  return dispatch_tile<64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
+}
+
+const char* gemm_name(int epi, int tile) {
+  static const char* names[2][6] = {
+      {"gemm_fwd_stash_128x128", "gemm_fwd_delta_128x128", "gemm_fwd_out_128x128",
+       "gemm_bwd_128x128", "gemm_dw_sgd_128x128", "gemm_dw_partial_128x128"},
+      {"gemm_fwd_stash_64x64", "gemm_fwd_delta_64x64", "gemm_fwd_out_64x64", "gemm_bwd_64x64",
+       "gemm_dw_sgd_64x64", "gemm_dw_partial_64x64"}};
+  if (epi < 0 || epi > 5 || tile < 0 || tile > 1) return "gemm";
+  return names[tile][epi];
+}
+
+hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* pbias, int nshards,
+                           int nsub, int M, int N, int64_t ldw, float* G, float* gbias, float* W,
+                           float* b, float scale, hipStream_t s) {
+  const int64_t total = (int64_t)M * N + M;
+  const int threads = 256;
+  const int64_t blocks = (total + threads - 1) / threads;
+  fold_sgd_kernel<<<dim3((unsigned)blocks), threads, 0, s>>>(partial, pstride, pbias, nshards, nsub,
+                                                           M, N, ldw, G, gbias, W, b, scale);
+  return hipGetLastError();
+}
+
+}  // namespace nf

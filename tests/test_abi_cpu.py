@@ -1,0 +1,99 @@
+"""The C ABI library on a machine without a GPU: it loads, exports every
+function include/nf.h declares, rejects bad arguments before touching the
+device, and reports a missing device as an error instead of falling back."""
+
+import ctypes
+
+import pytest
+
+from paper_1902_06714_amd import nf
+
+
+def _gpu_present() -> bool:
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+def test_every_declared_function_is_exported():
+    names = nf.declared_functions()
+    assert {"nf_net_create", "nf_net_destroy", "nf_param_count", "nf_set_params",
+            "nf_get_params", "nf_get_grads", "nf_forward", "nf_train_batch",
+            "nf_train_epoch", "nf_profile", "nf_profile_read", "nf_last_error"} <= set(names)
+    lib = nf.raw()
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in nf.h but not exported"
+
+
+def test_header_is_plain_c():
+    import subprocess
+    res = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c",
+                          nf.HEADER], capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+
+
+def _create(dims, acts):
+    d = (ctypes.c_int32 * max(1, len(dims)))(*dims)
+    a = (ctypes.c_int32 * max(1, len(acts)))(*acts)
+    out = ctypes.c_void_p(12345)
+    st = nf.raw().nf_net_create(d if dims else None, len(dims), a if acts else None, len(acts),
+                                ctypes.byref(out))
+    return st, out.value
+
+
+@pytest.mark.parametrize("dims,acts,expect", [
+    ([784], [], nf.NF_ESHAPE),                       # no output layer
+    ([], [], nf.NF_EINVAL),                          # NULL dims
+    ([4, 0, 2], [], nf.NF_ESHAPE),                   # empty layer
+    ([4, -3, 2], [], nf.NF_ESHAPE),
+    ([4, 70000, 2], [], nf.NF_ESHAPE),               # layer too wide
+    ([4, 3, 2], [2, 2, 2], nf.NF_ESHAPE),            # n_acts neither 0, 1 nor n_dims - 1
+    ([4, 3, 2], [7], nf.NF_EINVAL),                  # unknown activation
+    ([4, 3, 2], [-1, 2], nf.NF_EINVAL),
+])
+def test_create_rejects_bad_arguments(dims, acts, expect):
+    st, handle = _create(dims, acts)
+    assert st == expect, nf.nf_last_error()
+    assert handle == 12345, "out must not be written on error"
+    assert nf.nf_last_error() != ""
+
+
+def test_create_null_out():
+    d = (ctypes.c_int32 * 2)(3, 2)
+    assert nf.raw().nf_net_create(d, 2, None, 0, None) == nf.NF_EINVAL
+
+
+def test_null_net_calls():
+    lib = nf.raw()
+    assert lib.nf_param_count(None) == -1
+    assert lib.nf_net_destroy(None) == nf.NF_OK
+    buf = (ctypes.c_float * 4)()
+    assert lib.nf_set_params(None, buf, 4) == nf.NF_EINVAL
+    assert lib.nf_get_params(None, buf, 4) == nf.NF_EINVAL
+    assert lib.nf_get_grads(None, buf, 4) == nf.NF_EINVAL
+    assert lib.nf_forward(None, buf, 1, buf, None) == nf.NF_EINVAL
+    assert lib.nf_train_batch(None, buf, buf, 1, 1.0, 1, None) == nf.NF_EINVAL
+    assert lib.nf_train_epoch(None, buf, buf, 1, 1, 1.0, 1, None) == nf.NF_EINVAL
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the behaviour without a GPU")
+def test_no_device_is_an_error_not_a_fallback():
+    st, _ = _create([784, 30, 10], [])
+    assert st == nf.NF_EDEVICE
+    assert "device" in nf.nf_last_error().lower()
+
+
+def test_one_hip_runtime_per_process():
+    """The binding loads the library after torch, so both share one HIP runtime
+    (two runtimes in one process collide on the device)."""
+    import subprocess
+    import sys
+    code = ("import paper_1902_06714_amd.nf, torch\n"
+            "maps = open('/proc/self/maps').read().split('\\n')\n"
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n")
+    res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=__import__("os").path.dirname(nf.LIB_PATH) + "/..")
+    assert res.returncode == 0, res.stderr
+    assert res.stdout.strip() == "1"
