@@ -70,6 +70,8 @@ struct nf_net {
   // per-piece tendencies
   float* partial = nullptr;
   int64_t partial_floats = 0;
+  // every layer after the input has at most NARROW_WIDTH units
+  bool narrow = false;
   hipStream_t last = nullptr;
   bool used = false;
   // per-kernel timing (nf_profile)
@@ -355,6 +357,94 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
   return NF_OK;
 }
 
+bool narrow_ok(const nf_net* n, const float* x, int shards) {
+  return n->narrow && shards == 1 && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0]);
+}
+
+nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const float* y,
+                                      int64_t batch, float* out) {
+  nf::NarrowFwdParams p{};
+  const int L = num_layers(n);
+  p.X = x;
+  p.Y = y;
+  p.B = (int)batch;
+  p.d0 = n->dims[0];
+  p.L = L;
+  p.dims[0] = n->dims[0];
+  for (int l = 1; l <= L; ++l) {
+    const LayerLayout& ly = n->layers[l];
+    p.dims[l] = ly.out;
+    p.acts[l - 1] = ly.act;
+    p.W[l - 1] = n->params + ly.w_off;
+    p.ldw[l - 1] = ly.ldw;
+    p.bias[l - 1] = n->params + ly.b_off;
+    p.A[l - 1] = n->actv[l];
+    p.D[l - 1] = n->fbuf[l];
+  }
+  p.out = out;
+  return p;
+}
+
+// Algorithmic work of the per-sample pass: inputs, targets and weights read,
+// per-sample activations and deltas written; forward and delta flops.
+void narrow_fwd_work(const nf_net* n, int64_t B, bool train, double* bytes, double* flops) {
+  const int L = num_layers(n);
+  double by = (double)B * n->dims[0], fl = 0.0;
+  for (int l = 1; l <= L; ++l) {
+    const double dl = n->dims[l], dp = n->dims[l - 1];
+    by += dl * dp + dl;
+    fl += 2.0 * B * dl * dp;
+    if (train && l >= 2) fl += 2.0 * B * dl * dp;
+  }
+  if (train) {
+    by += (double)B * n->dims[L];                       // targets
+    for (int l = 1; l <= L; ++l) by += (double)B * n->dims[l] * (l < L ? 2 : 1);
+  } else {
+    by += (double)B * n->dims[L];                       // outputs
+  }
+  *bytes = 4.0 * by;
+  *flops = fl;
+}
+
+nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
+                            hipStream_t s) {
+  const int L = num_layers(n);
+  double by, fl;
+  narrow_fwd_work(n, batch, true, &by, &fl);
+  const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, y, batch, nullptr);
+  nf_status st =
+      timed(n, "narrow_fwd_train", by, fl, s, [&] { return nf::launch_narrow_fwd(true, fp, s); });
+  if (st != NF_OK) return st;
+
+  nf::NarrowDwParams dp{};
+  dp.B = (int)batch;
+  dp.L = L;
+  dp.X = x;
+  dp.scale = (float)((double)eta / (double)batch);
+  dp.dims[0] = n->dims[0];
+  int base = 0;
+  double dby = 0.0, dfl = 0.0;
+  for (int l = 1; l <= L; ++l) {
+    const LayerLayout& ly = n->layers[l];
+    dp.dims[l] = ly.out;
+    dp.A[l - 1] = l < L ? n->actv[l] : nullptr;
+    dp.D[l - 1] = n->fbuf[l];
+    dp.W[l - 1] = n->params + ly.w_off;
+    dp.ldw[l - 1] = ly.ldw;
+    dp.bias[l - 1] = n->params + ly.b_off;
+    dp.G[l - 1] = n->grads + ly.w_off;
+    dp.gb[l - 1] = n->grads + ly.b_off;
+    dp.tile_base[l - 1] = base;
+    base += (ly.in + 15) / 16;
+    // deltas and previous activations read, tendencies written, parameters updated
+    const double M = ly.out, N = ly.in;
+    dby += 4.0 * ((double)batch * (M + N) + 3 * M * N + 3 * M);
+    dfl += 2.0 * batch * M * N;
+  }
+  dp.tile_base[L] = base;
+  return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
+}
+
 nf_status check_net(const nf_net* n) {
   if (!n) return fail(NF_EINVAL, "net is NULL");
   return NF_OK;
@@ -362,6 +452,7 @@ nf_status check_net(const nf_net* n) {
 
 nf_status train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
                      int shards, hipStream_t s) {
+  if (narrow_ok(n, x, shards)) return narrow_train_step(n, x, y, batch, eta, s);
   nf_status st = run_forward(n, x, y, batch, nullptr, true, s);
   if (st != NF_OK) return st;
   return run_backward_update(n, x, batch, eta, shards, s);
@@ -438,6 +529,10 @@ nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts
       ly.lda = round_up(ly.out, 4);
       canon += (int64_t)ly.out * ly.in + ly.out;
     }
+    n->narrow = n_dims - 1 <= nf::NARROW_MAX_LAYERS;
+    for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
+    if (n->narrow)
+      for (int l = 1; l < n_dims; ++l) n->layers[l].lda = nf::NARROW_WIDTH;
     n->n_params = canon;
     n->dev_floats = off;
     n->actv.assign(n_dims, nullptr);
@@ -546,7 +641,15 @@ nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out,
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = ensure_ws(net, batch);
     if (st != NF_OK) return st;
-    st = run_forward(net, d_x, nullptr, batch, d_out, false, s);
+    if (net->narrow && net->dims[0] % 4 == 0 && vec_ok(d_x, net->dims[0])) {
+      double by, fl;
+      narrow_fwd_work(net, batch, false, &by, &fl);
+      const nf::NarrowFwdParams fp = narrow_fwd_params(net, d_x, nullptr, batch, d_out);
+      st = timed(net, "narrow_fwd_infer", by, fl, s,
+                 [&] { return nf::launch_narrow_fwd(false, fp, s); });
+    } else {
+      st = run_forward(net, d_x, nullptr, batch, d_out, false, s);
+    }
     net->last = s;
     net->used = true;
     return st;

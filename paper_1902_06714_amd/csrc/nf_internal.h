@@ -61,4 +61,47 @@ hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* p
                            int nshards, int nsub, int M, int N, int64_t ldw, float* G,
                            float* gbias, float* W, float* b, float scale, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// Narrow networks: every layer after the input has at most NARROW_WIDTH units
+// (the paper's 784-30-10 MNIST network is one).  A training step is two
+// kernels: a per-sample pass (forward, output delta, hidden deltas) and the
+// batch tendencies with the SGD step.  Per-sample buffers have pitch
+// NARROW_WIDTH and zero padding.
+// ---------------------------------------------------------------------------
+constexpr int NARROW_MAX_LAYERS = 4;
+constexpr int NARROW_WIDTH = 32;
+constexpr int NARROW_TILE = 16;       // samples per workgroup of the per-sample pass
+
+struct NarrowFwdParams {
+  const float* X;                          // [B][d0], d0 % 4 == 0, 16-byte aligned
+  const float* Y;                          // [B][d_L] targets (training)
+  int B, d0, L;
+  int dims[NARROW_MAX_LAYERS + 1];
+  int acts[NARROW_MAX_LAYERS];
+  const float* W[NARROW_MAX_LAYERS];       // W_l [d_l][ldw_l] (index l-1)
+  int64_t ldw[NARROW_MAX_LAYERS];
+  const float* bias[NARROW_MAX_LAYERS];
+  float* A[NARROW_MAX_LAYERS];             // f(z_l) [B][32], l = 1..L-1
+  float* D[NARROW_MAX_LAYERS];             // delta_l [B][32], l = 1..L
+  float* out;                              // inference: f(z_L) [B][d_L]
+};
+
+struct NarrowDwParams {
+  int B, L;                                // batch, layers
+  int dims[NARROW_MAX_LAYERS + 1];
+  const float* X;                          // layer-1 inputs [B][d0]
+  const float* A[NARROW_MAX_LAYERS];       // f(z_l) [B][32], l = 1..L-1
+  const float* D[NARROW_MAX_LAYERS];       // delta_l [B][32]
+  float* W[NARROW_MAX_LAYERS];
+  int64_t ldw[NARROW_MAX_LAYERS];
+  float* bias[NARROW_MAX_LAYERS];
+  float* G[NARROW_MAX_LAYERS];             // tendencies, same layout as W / bias
+  float* gb[NARROW_MAX_LAYERS];
+  int tile_base[NARROW_MAX_LAYERS + 1];    // first workgroup (16-column tile) of each layer
+  float scale;
+};
+
+hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s);
+hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
+
 }  // namespace nf

@@ -1,0 +1,296 @@
+// Training step for narrow networks (every layer after the input has at most
+// 32 units, like the paper's 784-30-10 MNIST network, section 4).
+//
+// Kernel 1, per 16-sample tile (one workgroup of 8 waves):
+//   layer 1   z_1 = W_1 x + b_1 on the fp32 matrix cores (16x16x4), the input
+//             width split across the 8 waves and summed in wave order;
+//   layers 2+ one thread per (sample, unit) with the previous layer in LDS;
+//   deltas    output delta (a_L - y) f'(z_L) and hidden deltas
+//             (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3), with f'(z_l) kept
+//             in registers from the forward pass.
+// Kernel 2, tendencies of every layer (sections 3.3-3.5): workgroup
+//   (layer, 16-column tile) forms the batch sum of delta (outer) activation
+//   for its columns on the matrix cores (16x16x4), its 8 waves splitting the
+//   batch and their sums added in wave order; it then stores the tendency and
+//   applies W -= (eta/B) G itself, so no workgroup waits on another.  The
+//   order of every sum is fixed, so results are reproducible bit for bit.
+#include "nf_act.h"
+#include "nf_internal.h"
+
+namespace nf {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int N1_WAVES = 8;
+constexpr int N1_UNROLL = 8;  // 16-wide input groups loaded per wave before use
+
+template <bool TRAIN>
+__global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowFwdParams p) {
+  constexpr int T = NARROW_TILE;
+  constexpr int NW = NARROW_WIDTH;
+  __shared__ float zp[N1_WAVES][T][NW + 1];
+  __shared__ float hs[2][T][NW + 1];                         // activations, then deltas
+  __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];    // W_2 .. W_L
+  __shared__ float bs[NARROW_MAX_LAYERS][NW];                // b_1 .. b_L
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int s0 = blockIdx.x * T;
+
+  // stage the small layers' weights and every bias in LDS (read again and
+  // again by the per-sample threads below); the loads are issued together
+  // and land while layer 1 runs
+  constexpr int NSTAGE = (NARROW_MAX_LAYERS - 1) * NW * NW / (N1_WAVES * 64);
+  static_assert((NARROW_MAX_LAYERS - 1) * NW * NW % (N1_WAVES * 64) == 0, "staging split");
+  float wst[NSTAGE];
+#pragma unroll
+  for (int u = 0; u < NSTAGE; ++u) {
+    const int e = tid + u * N1_WAVES * 64;
+    const int l = e / (NW * NW) + 2, rem = e % (NW * NW), row = rem / NW, colw = rem % NW;
+    const bool ok = l <= p.L && row < p.dims[l] && colw < p.dims[l - 1];
+    // out-of-range entries read W_1[0][0] (always present) and are zeroed
+    const float* src = ok ? p.W[l - 1] + (int64_t)row * p.ldw[l - 1] + colw : p.W[0];
+    const float v = *src;
+    wst[u] = ok ? v : 0.0f;
+  }
+  float bst = 0.0f;
+  if (tid < NARROW_MAX_LAYERS * NW) {
+    const int l = tid / NW + 1, u = tid % NW;
+    if (l <= p.L && u < p.dims[l]) bst = p.bias[l - 1][u];
+  }
+  // this thread's target (sample tid / 32, output unit tid % 32)
+  float ytg = 0.0f;
+  if (TRAIN) {
+    const int ys = s0 + (tid >> 5), yu = tid & 31;
+    if (ys < p.B && yu < p.dims[p.L]) ytg = p.Y[(int64_t)ys * p.dims[p.L] + yu];
+  }
+
+  // ---- layer 1 on the matrix cores: lane (r, g) = (lane % 16, lane / 16)
+  // feeds sample r and units r, 16 + r with the inputs [16 k + 4 g, 16 k + 4 g + 4)
+  // of every 16-wide group k it handles; the four MFMAs of a group take one
+  // of those four inputs each, so every product of the dot product is formed.
+  // Out-of-range rows and inputs are loaded from a valid address and zeroed.
+  {
+    const int r = lane & 15, g = lane >> 4;
+    const int d1 = p.dims[1];
+    const bool x_ok = s0 + r < p.B;
+    const bool w0_ok = r < d1, w1_ok = 16 + r < d1;
+    const float* xrow = p.X + (int64_t)(x_ok ? s0 + r : p.B - 1) * p.d0;
+    const float* w0 = p.W[0] + (int64_t)(w0_ok ? r : 0) * p.ldw[0];
+    const float* w1 = p.W[0] + (int64_t)(w1_ok ? 16 + r : 0) * p.ldw[0];
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    const int ngroups = (p.d0 + 15) / 16;
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int gb = wave; gb < ngroups; gb += N1_WAVES * N1_UNROLL) {
+      float4 xv[N1_UNROLL], wa[N1_UNROLL], wb[N1_UNROLL];
+#pragma unroll
+      for (int u = 0; u < N1_UNROLL; ++u) {
+        const int k = (gb + u * N1_WAVES) * 16 + g * 4;
+        const int kc = k < p.d0 ? k : 0;
+        xv[u] = *reinterpret_cast<const float4*>(xrow + kc);
+        wa[u] = *reinterpret_cast<const float4*>(w0 + kc);
+        wb[u] = *reinterpret_cast<const float4*>(w1 + kc);
+      }
+#pragma unroll
+      for (int u = 0; u < N1_UNROLL; ++u) {
+        const bool k_ok = (gb + u * N1_WAVES) * 16 + g * 4 < p.d0;
+        const float4 x = (k_ok && x_ok) ? xv[u] : zero;
+        const float4 a = (k_ok && w0_ok) ? wa[u] : zero;
+        const float4 b = (k_ok && w1_ok) ? wb[u] : zero;
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, a.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, b.x, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, a.y, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, b.y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.z, a.z, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.z, b.z, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, a.w, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, b.w, acc1, 0, 0, 0);
+      }
+    }
+    // accumulator register v of lane (r, g): sample 4 g + v, unit r (+16)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      zp[wave][4 * g + v][r] = acc0[v];
+      zp[wave][4 * g + v][16 + r] = acc1[v];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < NSTAGE; ++u) {
+    const int e = tid + u * N1_WAVES * 64;
+    const int l = e / (NW * NW) + 2, rem = e % (NW * NW);
+    ws[l - 2][rem / NW][rem % NW] = wst[u];
+  }
+  if (tid < NARROW_MAX_LAYERS * NW) bs[tid / NW][tid % NW] = bst;
+  __syncthreads();
+
+  // ---- thread (s, j): sample s of the tile, unit j of the current layer
+  const int s = tid >> 5, j = tid & 31;
+  const int gs = s0 + s;
+  const bool s_ok = gs < p.B;
+  float fp[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0f;
+  int cur = 0;
+  {
+    float z = zp[0][s][j];
+#pragma unroll
+    for (int w = 1; w < N1_WAVES; ++w) z += zp[w][s][j];
+    float a = 0.0f, f = 0.0f;
+    if (j < p.dims[1]) act_eval(p.acts[0], z + bs[0][j], a, f);
+    fp[0] = f;
+    if (p.L == 1) {
+      if (TRAIN) {
+        const float d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0f;
+        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < p.dims[1]) {
+        p.out[(int64_t)gs * p.dims[1] + j] = a;
+      }
+    } else {
+      hs[0][s][j] = a;
+      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
+    }
+  }
+  __syncthreads();
+
+  // ---- layers 2..L (padded units carry zeros, so every sum runs over 32)
+#pragma unroll
+  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
+    if (l > p.L) break;
+    const int dl = p.dims[l];
+    float z = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) z = fmaf(ws[l - 2][j][i], hs[cur][s][i], z);
+    float a = 0.0f, f = 0.0f;
+    if (j < dl) act_eval(p.acts[l - 1], z + bs[l - 1][j], a, f);
+    fp[l - 1] = f;
+    if (l == p.L) {
+      if (TRAIN) {
+        const float d = (j < dl && s_ok) ? (a - ytg) * f : 0.0f;
+        hs[cur ^ 1][s][j] = d;
+        if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < dl) {
+        p.out[(int64_t)gs * dl + j] = a;
+      }
+    } else {
+      hs[cur ^ 1][s][j] = a;
+      if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (!TRAIN) return;
+
+  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+#pragma unroll
+  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
+    if (l >= p.L) continue;
+    float t = 0.0f;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) t = fmaf(ws[l - 1][k][j], hs[cur][s][k], t);
+    const float d = j < p.dims[l] ? t * fp[l - 1] : 0.0f;
+    hs[cur ^ 1][s][j] = d;
+    if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+    cur ^= 1;
+    __syncthreads();
+  }
+}
+
+// Workgroup = 8 waves, one (layer, 16-column tile) over the whole batch:
+// G[u][c0 + r] = sum over samples of delta[s][u] a_prev[s][c0 + r] on the
+// 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
+// waves' sums are added in wave order, then the tile applies the SGD step.
+constexpr int N2_WAVES = 8;
+constexpr int N2_UNROLL = 8;   // groups of 4 samples loaded before use
+
+__global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDwParams p) {
+  __shared__ float red[N2_WAVES][NARROW_WIDTH][17];
+  __shared__ float bred[N2_WAVES][4][NARROW_WIDTH];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int l = 0;
+  while (l + 1 < p.L && (int)blockIdx.x >= p.tile_base[l + 1]) ++l;
+  const int c = (int)blockIdx.x - p.tile_base[l];
+  const int M = p.dims[l + 1], N = p.dims[l];
+  const int c0 = c * 16;
+  const float* xop = l == 0 ? p.X : p.A[l - 1];
+  const int64_t ldx = l == 0 ? p.dims[0] : NARROW_WIDTH;
+  const float* dl = p.D[l];
+
+  const int r = lane & 15, g = lane >> 4;
+  const bool col_ok = c0 + r < N;
+  const float* xcol = xop + (col_ok ? c0 + r : 0);
+  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  float bs0 = 0.0f, bs1 = 0.0f;
+  const int ngroups = (p.B + 3) / 4;
+  for (int gb = wave; gb < ngroups; gb += N2_WAVES * N2_UNROLL) {
+    float d0v[N2_UNROLL], d1v[N2_UNROLL], xv[N2_UNROLL];
+#pragma unroll
+    for (int u = 0; u < N2_UNROLL; ++u) {
+      const int smp = (gb + u * N2_WAVES) * 4 + g;
+      const int sc = smp < p.B ? smp : p.B - 1;
+      d0v[u] = dl[(int64_t)sc * NARROW_WIDTH + r];
+      d1v[u] = dl[(int64_t)sc * NARROW_WIDTH + 16 + r];
+      xv[u] = xcol[(int64_t)sc * ldx];
+    }
+#pragma unroll
+    for (int u = 0; u < N2_UNROLL; ++u) {
+      const bool ok = (gb + u * N2_WAVES) * 4 + g < p.B;
+      const float a0 = ok ? d0v[u] : 0.0f, a1 = ok ? d1v[u] : 0.0f;
+      const float b = (ok && col_ok) ? xv[u] : 0.0f;
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b, acc1, 0, 0, 0);
+      bs0 += a0;
+      bs1 += a1;
+    }
+  }
+  // accumulator register v of lane (r, g): unit 4 g + v (+16), column c0 + r
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    red[wave][4 * g + v][r] = acc0[v];
+    red[wave][16 + 4 * g + v][r] = acc1[v];
+  }
+  if (c == 0) {
+    bred[wave][g][r] = bs0;
+    bred[wave][g][16 + r] = bs1;
+  }
+  __syncthreads();
+
+  {
+    const int i = tid >> 4, jj = tid & 15;   // unit, column within the tile
+    float gsum = red[0][i][jj];
+#pragma unroll
+    for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][i][jj];
+    if (i < M && c0 + jj < N) {
+      const int64_t o = (int64_t)i * p.ldw[l] + c0 + jj;
+      p.G[l][o] = gsum;
+      p.W[l][o] = fmaf(-p.scale, gsum, p.W[l][o]);
+    }
+  }
+  if (c == 0 && tid < M) {
+    float gsum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < N2_WAVES; ++w)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
+    p.gb[l][tid] = gsum;
+    p.bias[l][tid] = fmaf(-p.scale, gsum, p.bias[l][tid]);
+  }
+}
+
+hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s) {
+  const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
+  if (train)
+    narrow_fwd_kernel<true><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  else
+    narrow_fwd_kernel<false><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s) {
+  narrow_dw_kernel<<<dim3(p.tile_base[p.L]), N2_WAVES * 64, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace nf

@@ -56,6 +56,14 @@ SMALL = [
     ((6, 9, 4), ("gaussian", "sigmoid"), 16, 16, 0.5),   # one sample per shard
     ((129, 1, 1), ("sigmoid",), 65, 5, 2.0),             # one-unit layers
     ((200, 130, 70, 3), ("sigmoid",), 4000, 4, 3.0),
+    # narrow networks (every layer after the input <= 32 units, input width % 4 == 0)
+    ((40, 17, 9, 5), ("tanh", "sigmoid", "gaussian"), 300, 1, 0.5),
+    ((64, 32, 32, 32, 2), ("sigmoid",), 1000, 1, 1.0),
+    ((784, 30, 10), ("sigmoid",), 1, 1, 3.0),
+    ((784, 30, 10), ("sigmoid",), 129, 1, 3.0),
+    ((8, 3), ("sigmoid",), 77, 1, 1.0),
+    ((20, 32), ("tanh",), 129, 1, 0.5),
+    ((1024, 32, 16, 10), ("tanh", "gaussian", "sigmoid"), 2048, 1, 0.5),
 ]
 
 
@@ -94,6 +102,21 @@ def test_small_relu_elementwise(dims, acts, batch, shards, eta):
         if not e <= parity.GRAD_TOL:
             fails.append(f"grads {name}: {e:.3e}")
     assert not fails, "\n".join(fails)
+
+
+def test_narrow_and_general_paths_agree():
+    """A narrow network trained with one shard (its own two-kernel path) and
+    with two shards (the general contraction path) differs only by rounding."""
+    dims = (784, 30, 10)
+    theta, X, Y = _problem(dims, 21, 1000)
+    res = []
+    for shards in (1, 2):
+        note(f"narrow vs general shards={shards}")
+        with GpuNet(dims, ("sigmoid",), theta) as net:
+            net.train_batch(to_dev(X), to_dev(Y), 3.0, shards)
+            res.append((net.params(), net.grads()))
+    assert not parity.check_params(res[0][0], res[1][0], dims, tol=1e-6)
+    assert not parity.check_params(res[0][1], res[1][1], dims, tol=1e-5, what="grads")
 
 
 def test_hand_worked_networks_on_gpu():
