@@ -80,7 +80,10 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
     const float* xrow = p.X + (int64_t)(x_ok ? s0 + r : p.B - 1) * p.d0;
     const float* w0 = p.W[0] + (int64_t)(w0_ok ? r : 0) * p.ldw[0];
     const float* w1 = p.W[0] + (int64_t)(w1_ok ? 16 + r : 0) * p.ldw[0];
+    // two accumulator chains per unit block (inputs 4g, 4g+2 and 4g+1, 4g+3
+    // of each group) keep more MFMAs in flight; they are added at the end
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    floatx4 acc2 = {0.f, 0.f, 0.f, 0.f}, acc3 = {0.f, 0.f, 0.f, 0.f};
     const int ngroups = (p.d0 + 15) / 16;
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int gb = wave; gb < ngroups; gb += N1_WAVES * N1_UNROLL) {
@@ -101,14 +104,16 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
         const float4 b = (k_ok && w1_ok) ? wb[u] : zero;
         acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, a.x, acc0, 0, 0, 0);
         acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, b.x, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, a.y, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, b.y, acc1, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, a.y, acc2, 0, 0, 0);
+        acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, b.y, acc3, 0, 0, 0);
         acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.z, a.z, acc0, 0, 0, 0);
         acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.z, b.z, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, a.w, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, b.w, acc1, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, a.w, acc2, 0, 0, 0);
+        acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, b.w, acc3, 0, 0, 0);
       }
     }
+    acc0 += acc2;
+    acc1 += acc3;
     // accumulator register v of lane (r, g): sample 4 g + v, unit r (+16)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
@@ -202,16 +207,24 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
 // 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
 // waves' sums are added in wave order, then the tile applies the SGD step.
 constexpr int N2_WAVES = 8;
-constexpr int N2_UNROLL = 8;   // groups of 4 samples loaded before use
+constexpr int N2_UNROLL = 32;  // groups of 4 samples loaded before use
 
 __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDwParams p) {
   __shared__ float red[N2_WAVES][NARROW_WIDTH][17];
   __shared__ float bred[N2_WAVES][4][NARROW_WIDTH];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // consecutive workgroups land on different XCDs (round robin over 8); give
+  // each XCD a contiguous run of tiles so that neighbouring 16-column tiles,
+  // which share 128-byte lines of the input rows, share one L2
+  const int nwg = p.tile_base[p.L];
+  const int per = (nwg + 7) / 8;
+  const int full = nwg - 8 * (per - 1);       // XCDs that get `per` tiles
+  const int xcd = (int)blockIdx.x & 7, slot = (int)blockIdx.x >> 3;
+  const int tile = xcd < full ? xcd * per + slot : full * per + (xcd - full) * (per - 1) + slot;
   int l = 0;
-  while (l + 1 < p.L && (int)blockIdx.x >= p.tile_base[l + 1]) ++l;
-  const int c = (int)blockIdx.x - p.tile_base[l];
+  while (l + 1 < p.L && tile >= p.tile_base[l + 1]) ++l;
+  const int c = tile - p.tile_base[l];
   const int M = p.dims[l + 1], N = p.dims[l];
   const int c0 = c * 16;
   const float* xop = l == 0 ? p.X : p.A[l - 1];
