@@ -30,6 +30,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 RIDGE = FP32_MFMA_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)   # flop per byte
+PROFILE_REPEATS = 20
 
 METRIC = "training samples/sec (fwd+bwd+SGD) at 784-30-10 and wide MLP; % HBM/MFMA roofline"
 
@@ -185,12 +186,13 @@ def main(argv=None) -> int:
         print(f"[bench] timed {args.steps} steps: {ms:.3f} ms (events), {wall * 1e3:.3f} ms (wall)",
               file=sys.stderr, flush=True)
 
-        # per-kernel durations, same workload and launch configuration
-        nf.nf_profile(net, True)
-        for _ in range(max(1, min(args.steps, 5))):
-            step()
+        # per-kernel durations, same workload and launch configuration: every
+        # launch runs PROFILE_REPEATS times back to back between two events on
+        # the stream it is launched on (kernels never write what they read)
+        nf.nf_profile(net, PROFILE_REPEATS)
+        step()
         stats = nf.nf_profile_read(net)
-        nf.nf_profile(net, False)
+        nf.nf_profile(net, 0)
         finite = bool(np.all(np.isfinite(nf.nf_get_params(net))))
     finally:
         nf.nf_net_destroy(net)

@@ -130,19 +130,24 @@ nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_
  * recording is on, every kernel the net launches is bracketed by a pair of HIP
  * events on its stream, and the library notes the algorithmic bytes the
  * kernel must move (inputs read once, outputs written once) and the flops of
- * its contraction (2 per multiply-add, no padding).  Recording costs a little
- * time per launch; leave it off for throughput runs. */
+ * its contraction (2 per multiply-add, no padding).  Recording costs time;
+ * leave it off for throughput runs. */
 typedef struct {
   char name[64];      /* kernel family, e.g. "gemm_fwd_stash_128x128" */
   int64_t launches;   /* launches recorded since the last read             */
-  double total_ms;    /* sum of the event-measured durations (ms)          */
+  double total_ms;    /* sum of the measured durations (ms)                */
   double bytes;       /* algorithmic bytes, summed over the launches       */
   double flops;       /* algorithmic flops, summed over the launches       */
 } nf_kernel_stat;
 
-/* Turn recording on (enable != 0) or off.  Turning it on discards anything
- * recorded and not yet read. */
-nf_status nf_profile(nf_net* net, int32_t enable);
+/* repeats = 0 turns recording off.  repeats = R >= 1 turns it on (discarding
+ * anything recorded and not yet read): each launch is then run R times in a
+ * row between its two events and charged the average of the R runs, which
+ * keeps the fixed cost of the event pair out of short kernels.  Repeating is
+ * harmless because no kernel writes a buffer it reads: a training step reads
+ * the parameters from one buffer and writes the updated ones to another.
+ * repeats must be in 0 .. 1000. */
+nf_status nf_profile(nf_net* net, int32_t repeats);
 
 /* Wait for the recorded work, then write one entry per kernel name (at most
  * cap entries, ordered by total time, largest first) to out[] and their number

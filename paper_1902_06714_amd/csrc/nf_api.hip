@@ -60,13 +60,17 @@ struct nf_net {
   std::vector<LayerLayout> layers;
   int64_t n_params = 0;       // canonical floats
   int64_t dev_floats = 0;     // device layout floats
-  float* params = nullptr;    // device layout
+  // parameters, double-buffered: a step reads pbuf[cur] and writes the
+  // updated parameters to pbuf[cur ^ 1], then cur flips
+  float* pbuf[2] = {nullptr, nullptr};
+  int cur = 0;
   float* grads = nullptr;     // device layout, tendencies of the last step
   // workspace for up to ws_batch samples
   int64_t ws_batch = 0;
   float* ws = nullptr;
   std::vector<float*> actv;   // actv[l]: f(z_l) [B][lda_l], l = 1..L-1
-  std::vector<float*> fbuf;   // fbuf[l]: f'(z_l), overwritten by delta_l, l = 1..L
+  std::vector<float*> fbuf;   // fbuf[l]: f'(z_l) [B][lda_l], l = 1..L-1
+  std::vector<float*> dbuf;   // dbuf[l]: delta_l [B][lda_l], l = 1..L
   // per-piece tendencies
   float* partial = nullptr;
   int64_t partial_floats = 0;
@@ -79,14 +83,19 @@ struct nf_net {
     const char* name;
     hipEvent_t a, b;
     double bytes, flops;
+    int repeats;
   };
-  bool prof = false;
+  int prof = 0;                // 0: off; R >= 1: each kernel runs R times between its events
   std::vector<Rec> recs;
 };
 
 namespace {
 
 int num_layers(const nf_net* n) { return (int)n->dims.size() - 1; }
+
+// parameters read by this step, and the buffer its update is written to
+float* cur_params(const nf_net* n) { return n->pbuf[n->cur]; }
+float* next_params(const nf_net* n) { return n->pbuf[n->cur ^ 1]; }
 
 nf_status sync_net(nf_net* n) {
   if (!n->used) return NF_OK;
@@ -101,6 +110,7 @@ void free_ws(nf_net* n) {
   n->ws_batch = 0;
   n->actv.assign(n->dims.size(), nullptr);
   n->fbuf.assign(n->dims.size(), nullptr);
+  n->dbuf.assign(n->dims.size(), nullptr);
 }
 
 // Make room for `batch` samples.  Growing waits for the net's earlier work,
@@ -111,14 +121,16 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
   if (st != NF_OK) return st;
   const int L = num_layers(n);
   int64_t total = 0;
-  std::vector<int64_t> aoff(L + 1, -1), foff(L + 1, -1);
+  std::vector<int64_t> aoff(L + 1, -1), foff(L + 1, -1), doff(L + 1, -1);
   for (int l = 1; l <= L; ++l) {
     const int64_t sz = round_up(batch * n->layers[l].lda, kAlign);
     if (l < L) {
       aoff[l] = total;
       total += sz;
+      foff[l] = total;
+      total += sz;
     }
-    foff[l] = total;
+    doff[l] = total;
     total += sz;
   }
   float* buf = nullptr;
@@ -137,7 +149,8 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
   n->ws_batch = batch;
   for (int l = 1; l <= L; ++l) {
     n->actv[l] = aoff[l] >= 0 ? buf + aoff[l] : nullptr;
-    n->fbuf[l] = buf + foff[l];
+    n->fbuf[l] = foff[l] >= 0 ? buf + foff[l] : nullptr;
+    n->dbuf[l] = buf + doff[l];
   }
   return NF_OK;
 }
@@ -175,22 +188,40 @@ void clear_recs(nf_net* n) {
   n->recs.clear();
 }
 
-// Runs `enqueue` on stream s; with recording on, brackets it with events.
+// Runs `enqueue` on stream s.  With recording on, the launch is bracketed by a
+// pair of events and, for R > 1, repeated R times in a row between them (every
+// kernel reads only buffers it does not write, so a repeat recomputes the same
+// values); the record is charged the average of the R runs.
 template <class F>
 nf_status timed(nf_net* n, const char* name, double bytes, double flops, hipStream_t s,
                 F&& enqueue) {
-  nf_net::Rec r{name, nullptr, nullptr, bytes, flops};
+  nf_net::Rec r{name, nullptr, nullptr, bytes, flops, n->prof};
   if (n->prof) {
     hipError_t e = hipEventCreate(&r.a);
     if (e == hipSuccess) e = hipEventCreate(&r.b);
     if (e == hipSuccess) e = hipEventRecord(r.a, s);
-    if (e != hipSuccess) return hip_fail(e, "profiling event");
+    if (e != hipSuccess) {
+      if (r.a) (void)hipEventDestroy(r.a);
+      if (r.b) (void)hipEventDestroy(r.b);
+      return hip_fail(e, "profiling event");
+    }
   }
-  hipError_t e = enqueue();
-  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  const int reps = n->prof > 1 ? n->prof : 1;
+  for (int i = 0; i < reps; ++i) {
+    hipError_t e = enqueue();
+    if (e != hipSuccess) {
+      if (r.a) (void)hipEventDestroy(r.a);
+      if (r.b) (void)hipEventDestroy(r.b);
+      return hip_fail(e, "kernel launch");
+    }
+  }
   if (n->prof) {
-    e = hipEventRecord(r.b, s);
-    if (e != hipSuccess) return hip_fail(e, "profiling event");
+    hipError_t e = hipEventRecord(r.b, s);
+    if (e != hipSuccess) {
+      (void)hipEventDestroy(r.a);
+      (void)hipEventDestroy(r.b);
+      return hip_fail(e, "profiling event");
+    }
     n->recs.push_back(r);
   }
   return NF_OK;
@@ -229,13 +260,13 @@ nf_status run_forward(nf_net* n, const float* x, const float* y, int64_t batch, 
     nf::GemmParams p{};
     p.A = l == 1 ? x : n->actv[l - 1];
     p.lda = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
-    p.B = n->params + ly.w_off;
+    p.B = cur_params(n) + ly.w_off;
     p.ldb = ly.ldw;
     p.M = (int)batch;
     p.N = ly.out;
     p.K = ly.in;
     p.nsub = 1;
-    p.bias = n->params + ly.b_off;
+    p.bias = cur_params(n) + ly.b_off;
     p.act = ly.act;
     const bool av = l == 1 ? vec_ok(x, n->dims[0]) : true;
     int epi;
@@ -250,7 +281,7 @@ nf_status run_forward(nf_net* n, const float* x, const float* y, int64_t batch, 
         epi = nf::EPI_FWD_DELTA;
         p.aux = y;
         p.ldaux = ly.out;
-        p.out0 = n->fbuf[l];
+        p.out0 = n->dbuf[l];
         p.ld0 = ly.lda;
       }
     } else {
@@ -279,12 +310,12 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
   for (int l = L; l >= 1; --l) {
     const LayerLayout& ly = n->layers[l];
     if (l > 1) {
-      // delta_{l-1} = (delta_l W_l) * f'(z_{l-1}), in place over f'(z_{l-1})
+      // delta_{l-1} = (delta_l W_l) * f'(z_{l-1}), with this step's W_l
       const LayerLayout& lp = n->layers[l - 1];
       nf::GemmParams p{};
-      p.A = n->fbuf[l];
+      p.A = n->dbuf[l];
       p.lda = ly.lda;
-      p.B = n->params + ly.w_off;
+      p.B = cur_params(n) + ly.w_off;
       p.ldb = ly.ldw;
       p.M = (int)batch;
       p.N = lp.out;
@@ -292,7 +323,7 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
       p.nsub = 1;
       p.aux = n->fbuf[l - 1];
       p.ldaux = lp.lda;
-      p.out0 = n->fbuf[l - 1];
+      p.out0 = n->dbuf[l - 1];
       p.ld0 = lp.lda;
       nf_status st = launch(n, nf::EPI_BWD, true, false, true, true, 1, p, s);
       if (st != NF_OK) return st;
@@ -315,7 +346,7 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
     const int64_t sub_len = (shard_len + nsub - 1) / nsub;
     const int nsplit = shards * nsub;
     nf::GemmParams p{};
-    p.A = n->fbuf[l];
+    p.A = n->dbuf[l];
     p.lda = ly.lda;
     p.B = aprev;
     p.ldb = ldprev;
@@ -329,9 +360,11 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
     if (nsplit == 1) {
       p.out0 = n->grads + ly.w_off;
       p.ld0 = ly.ldw;
-      p.W = n->params + ly.w_off;
+      p.W = next_params(n) + ly.w_off;
+      p.Win = cur_params(n) + ly.w_off;
       p.ldw = ly.ldw;
-      p.bvec = n->params + ly.b_off;
+      p.bvec = next_params(n) + ly.b_off;
+      p.bin = cur_params(n) + ly.b_off;
       p.gbias = n->grads + ly.b_off;
       nf_status st = launch(n, nf::EPI_DW_SGD, false, false, true, bv, 1, p, s);
       if (st != NF_OK) return st;
@@ -349,7 +382,9 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
       st = timed(n, "fold_sgd", 4.0 * elems * (nsplit + 3), elems * (nsplit + 1), s, [&] {
         return nf::launch_fold_sgd(p.partial, pstride, p.pbias, shards, nsub, (int)M, (int)N,
                                    ly.ldw, n->grads + ly.w_off, n->grads + ly.b_off,
-                                   n->params + ly.w_off, n->params + ly.b_off, scale, s);
+                                   cur_params(n) + ly.w_off, cur_params(n) + ly.b_off,
+                                   next_params(n) + ly.w_off, next_params(n) + ly.b_off, scale,
+                                   s);
       });
       if (st != NF_OK) return st;
     }
@@ -375,11 +410,11 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
     const LayerLayout& ly = n->layers[l];
     p.dims[l] = ly.out;
     p.acts[l - 1] = ly.act;
-    p.W[l - 1] = n->params + ly.w_off;
+    p.W[l - 1] = cur_params(n) + ly.w_off;
     p.ldw[l - 1] = ly.ldw;
-    p.bias[l - 1] = n->params + ly.b_off;
+    p.bias[l - 1] = cur_params(n) + ly.b_off;
     p.A[l - 1] = n->actv[l];
-    p.D[l - 1] = n->fbuf[l];
+    p.D[l - 1] = n->dbuf[l];
   }
   p.out = out;
   return p;
@@ -428,10 +463,12 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
     const LayerLayout& ly = n->layers[l];
     dp.dims[l] = ly.out;
     dp.A[l - 1] = l < L ? n->actv[l] : nullptr;
-    dp.D[l - 1] = n->fbuf[l];
-    dp.W[l - 1] = n->params + ly.w_off;
+    dp.D[l - 1] = n->dbuf[l];
+    dp.Win[l - 1] = cur_params(n) + ly.w_off;
+    dp.bin[l - 1] = cur_params(n) + ly.b_off;
+    dp.W[l - 1] = next_params(n) + ly.w_off;
     dp.ldw[l - 1] = ly.ldw;
-    dp.bias[l - 1] = n->params + ly.b_off;
+    dp.bias[l - 1] = next_params(n) + ly.b_off;
     dp.G[l - 1] = n->grads + ly.w_off;
     dp.gb[l - 1] = n->grads + ly.b_off;
     dp.tile_base[l - 1] = base;
@@ -452,10 +489,17 @@ nf_status check_net(const nf_net* n) {
 
 nf_status train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
                      int shards, hipStream_t s) {
-  if (narrow_ok(n, x, shards)) return narrow_train_step(n, x, y, batch, eta, s);
-  nf_status st = run_forward(n, x, y, batch, nullptr, true, s);
-  if (st != NF_OK) return st;
-  return run_backward_update(n, x, batch, eta, shards, s);
+  nf_status st;
+  if (narrow_ok(n, x, shards)) {
+    st = narrow_train_step(n, x, y, batch, eta, s);
+  } else {
+    st = run_forward(n, x, y, batch, nullptr, true, s);
+    if (st == NF_OK) st = run_backward_update(n, x, batch, eta, shards, s);
+  }
+  // the updated parameters are in the other buffer from here on (a failed
+  // launch leaves the net in an undefined state, reported as NF_EDEVICE)
+  if (st == NF_OK) n->cur ^= 1;
+  return st;
 }
 
 nf_status check_train_args(const nf_net* n, const float* x, const float* y, int64_t batch,
@@ -537,13 +581,18 @@ nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts
     n->dev_floats = off;
     n->actv.assign(n_dims, nullptr);
     n->fbuf.assign(n_dims, nullptr);
-    e = hipMalloc(&n->params, (size_t)off * sizeof(float));
+    n->dbuf.assign(n_dims, nullptr);
+    // both parameter buffers and the tendencies start at zero, padding included
+    e = hipMalloc(&n->pbuf[0], (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&n->pbuf[1], (size_t)off * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&n->grads, (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(n->params, 0, (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(n->pbuf[0], 0, (size_t)off * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(n->pbuf[1], 0, (size_t)off * sizeof(float));
     if (e == hipSuccess) e = hipMemset(n->grads, 0, (size_t)off * sizeof(float));
     if (e != hipSuccess) {
       (void)hipGetLastError();
-      if (n->params) (void)hipFree(n->params);
+      if (n->pbuf[0]) (void)hipFree(n->pbuf[0]);
+      if (n->pbuf[1]) (void)hipFree(n->pbuf[1]);
       if (n->grads) (void)hipFree(n->grads);
       delete n;
       return fail(e == hipErrorOutOfMemory ? NF_ENOMEM : NF_EDEVICE,
@@ -562,7 +611,8 @@ nf_status nf_net_destroy(nf_net* net) {
     clear_recs(net);
     free_ws(net);
     if (net->partial) (void)hipFree(net->partial);
-    if (net->params) (void)hipFree(net->params);
+    if (net->pbuf[0]) (void)hipFree(net->pbuf[0]);
+    if (net->pbuf[1]) (void)hipFree(net->pbuf[1]);
     if (net->grads) (void)hipFree(net->grads);
     delete net;
     return st;
@@ -607,7 +657,7 @@ nf_status nf_set_params(nf_net* net, const float* host_src, int64_t n) {
     nf_status st = check_net(net);
     if (st != NF_OK) return st;
     if (!host_src) return fail(NF_EINVAL, "host_src is NULL");
-    return copy_params(net, net->params, host_src, nullptr, n);
+    return copy_params(net, cur_params(net), host_src, nullptr, n);
   });
 }
 
@@ -616,7 +666,7 @@ nf_status nf_get_params(nf_net* net, float* host_dst, int64_t n) {
     nf_status st = check_net(net);
     if (st != NF_OK) return st;
     if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
-    return copy_params(net, net->params, nullptr, host_dst, n);
+    return copy_params(net, cur_params(net), nullptr, host_dst, n);
   });
 }
 
@@ -700,17 +750,18 @@ nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_
   });
 }
 
-nf_status nf_profile(nf_net* net, int32_t enable) {
+nf_status nf_profile(nf_net* net, int32_t repeats) {
   return guarded([&]() -> nf_status {
     nf_status st = check_net(net);
     if (st != NF_OK) return st;
     DeviceGuard g(net->device);
-    if (enable) {
+    if (repeats < 0 || repeats > 1000) return fail(NF_EINVAL, "repeats must be in 0..1000");
+    if (repeats) {
       st = sync_net(net);
       if (st != NF_OK) return st;
       clear_recs(net);
     }
-    net->prof = enable != 0;
+    net->prof = repeats;
     return NF_OK;
   });
 }
@@ -741,7 +792,7 @@ nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t
         std::snprintf(k->name, sizeof(k->name), "%s", r.name);
       }
       k->launches += 1;
-      k->total_ms += ms;
+      k->total_ms += ms / (r.repeats > 1 ? r.repeats : 1);
       k->bytes += r.bytes;
       k->flops += r.flops;
     }

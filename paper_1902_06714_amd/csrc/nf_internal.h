@@ -35,9 +35,11 @@ struct GemmParams {
   int64_t ld0;
   float* out1;         // [M][ld1]
   int64_t ld1;
-  float* W;            // EPI_DW_SGD: weights [M][ldw] updated in place
+  float* W;            // EPI_DW_SGD: updated weights [M][ldw] (W = Win - scale * G)
+  const float* Win;    // EPI_DW_SGD: weights before the step, same layout
   int64_t ldw;
-  float* bvec;         // EPI_DW_SGD: biases [M] updated in place
+  float* bvec;         // EPI_DW_SGD: updated biases [M]
+  const float* bin;    // EPI_DW_SGD: biases before the step
   float* gbias;        // EPI_DW_SGD: bias tendency [M]
   float* partial;      // EPI_DW_PARTIAL: [nsplit][M][ld0]
   int64_t pstride;
@@ -56,10 +58,12 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
 const char* gemm_name(int epi, int tile);
 
 // Fold the per-piece tendencies of one layer in piece order, store the sum as
-// the tendency, and apply the SGD step to W [M][ldw] and b [M].
+// the tendency, and write the SGD step W = Win - scale * G, b = bin - scale * g
+// (W [M][ldw], b [M]).
 hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* pbias,
                            int nshards, int nsub, int M, int N, int64_t ldw, float* G,
-                           float* gbias, float* W, float* b, float scale, hipStream_t s);
+                           float* gbias, const float* Win, const float* bin, float* W, float* b,
+                           float scale, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Narrow networks: every layer after the input has at most NARROW_WIDTH units
@@ -92,7 +96,9 @@ struct NarrowDwParams {
   const float* X;                          // layer-1 inputs [B][d0]
   const float* A[NARROW_MAX_LAYERS];       // f(z_l) [B][32], l = 1..L-1
   const float* D[NARROW_MAX_LAYERS];       // delta_l [B][32]
-  float* W[NARROW_MAX_LAYERS];
+  const float* Win[NARROW_MAX_LAYERS];     // parameters before the step
+  const float* bin[NARROW_MAX_LAYERS];
+  float* W[NARROW_MAX_LAYERS];             // parameters after the step
   int64_t ldw[NARROW_MAX_LAYERS];
   float* bias[NARROW_MAX_LAYERS];
   float* G[NARROW_MAX_LAYERS];             // tendencies, same layout as W / bias

@@ -9,8 +9,9 @@
 //   backward    delta_l = (delta_{l+1} W_{l+1}) * f'(z_l)   (section 3.3)
 //   tendencies  G_l = delta_l^T A_{l-1} and g_l = column sums of delta_l,
 //               summed over the batch in a fixed order, with the SGD step
-//               W_l -= (eta/B) G_l fused in when the batch is one piece
-//               (sections 3.3-3.5)
+//               W_l' = W_l - (eta/B) G_l fused in when the batch is one piece
+//               (sections 3.3-3.5); the updated parameters go to a second
+//               buffer, so every kernel leaves its inputs untouched
 // Reductions run in a fixed order (each accumulator walks k upwards; pieces
 // of a split batch are added in piece order), so results are bitwise
 // reproducible from run to run.  No float atomics are used.
@@ -231,7 +232,7 @@ gemm_kernel(const GemmParams p) {
         } else if constexpr (EPI == EPI_DW_SGD) {
           const int64_t o = (int64_t)m * p.ldw + n;
           p.out0[o] = c;
-          p.W[o] = fmaf(-p.scale, c, p.W[o]);
+          p.W[o] = fmaf(-p.scale, c, p.Win[o]);
         } else {  // EPI_DW_PARTIAL
           p.partial[(int64_t)blockIdx.z * p.pstride + (int64_t)m * p.ld0 + n] = c;
         }
@@ -243,7 +244,7 @@ gemm_kernel(const GemmParams p) {
     if (m < p.M) {
       if constexpr (EPI == EPI_DW_SGD) {
         p.gbias[m] = bsum;
-        p.bvec[m] = fmaf(-p.scale, bsum, p.bvec[m]);
+        p.bvec[m] = fmaf(-p.scale, bsum, p.bin[m]);
       } else if constexpr (EPI == EPI_DW_PARTIAL) {
         p.pbias[(int64_t)blockIdx.z * p.M + m] = bsum;
       }
@@ -251,11 +252,13 @@ gemm_kernel(const GemmParams p) {
   }
 }
 
-// Sum of the per-piece tendencies in piece order, then the SGD step.
+// Sum of the per-piece tendencies in piece order, then the SGD step (from the
+// parameters before the step into the other parameter buffer).
 __global__ void fold_sgd_kernel(const float* __restrict__ partial, int64_t pstride,
                                 const float* __restrict__ pbias, int nshards, int nsub, int M,
                                 int N, int64_t ldw, float* __restrict__ G,
-                                float* __restrict__ gbias, float* __restrict__ W,
+                                float* __restrict__ gbias, const float* __restrict__ Win,
+                                const float* __restrict__ bin, float* __restrict__ W,
                                 float* __restrict__ b, float scale) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nw = (int64_t)M * N;
@@ -269,7 +272,7 @@ __global__ void fold_sgd_kernel(const float* __restrict__ partial, int64_t pstri
       tot = s == 0 ? piece : tot + piece;
     }
     G[o] = tot;
-    W[o] = fmaf(-scale, tot, W[o]);
+    W[o] = fmaf(-scale, tot, Win[o]);
   } else if (idx < nw + M) {
     const int m = (int)(idx - nw);
     float tot = 0.0f;
@@ -279,7 +282,7 @@ __global__ void fold_sgd_kernel(const float* __restrict__ partial, int64_t pstri
       tot = s == 0 ? piece : tot + piece;
     }
     gbias[m] = tot;
-    b[m] = fmaf(-scale, tot, b[m]);
+    b[m] = fmaf(-scale, tot, bin[m]);
   }
 }
 
@@ -334,13 +337,15 @@ const char* gemm_name(int epi, int tile) {
 }
 
 hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* pbias, int nshards,
-                           int nsub, int M, int N, int64_t ldw, float* G, float* gbias, float* W,
-                           float* b, float scale, hipStream_t s) {
+                           int nsub, int M, int N, int64_t ldw, float* G, float* gbias,
+                           const float* Win, const float* bin, float* W, float* b, float scale,
+                           hipStream_t s) {
   const int64_t total = (int64_t)M * N + M;
   const int threads = 256;
   const int64_t blocks = (total + threads - 1) / threads;
   fold_sgd_kernel<<<dim3((unsigned)blocks), threads, 0, s>>>(partial, pstride, pbias, nshards, nsub,
-                                                           M, N, ldw, G, gbias, W, b, scale);
+                                                           M, N, ldw, G, gbias, Win, bin, W, b,
+                                                           scale);
   return hipGetLastError();
 }
 

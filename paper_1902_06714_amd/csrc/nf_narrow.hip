@@ -12,8 +12,9 @@
 //   (layer, 16-column tile) forms the batch sum of delta (outer) activation
 //   for its columns on the matrix cores (16x16x4), its 8 waves splitting the
 //   batch and their sums added in wave order; it then stores the tendency and
-//   applies W -= (eta/B) G itself, so no workgroup waits on another.  The
-//   order of every sum is fixed, so results are reproducible bit for bit.
+//   writes W' = W - (eta/B) G itself (into the other parameter buffer), so no
+//   workgroup waits on another.  The order of every sum is fixed, so results
+//   are reproducible bit for bit.
 #include "nf_act.h"
 #include "nf_internal.h"
 
@@ -278,7 +279,7 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
     if (i < M && c0 + jj < N) {
       const int64_t o = (int64_t)i * p.ldw[l] + c0 + jj;
       p.G[l][o] = gsum;
-      p.W[l][o] = fmaf(-p.scale, gsum, p.W[l][o]);
+      p.W[l][o] = fmaf(-p.scale, gsum, p.Win[l][o]);
     }
   }
   if (c == 0 && tid < M) {
@@ -288,7 +289,7 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
 #pragma unroll
       for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
     p.gb[l][tid] = gsum;
-    p.bias[l][tid] = fmaf(-p.scale, gsum, p.bias[l][tid]);
+    p.bias[l][tid] = fmaf(-p.scale, gsum, p.bin[l][tid]);
   }
 }
 

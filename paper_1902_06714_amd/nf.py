@@ -173,8 +173,9 @@ def nf_train_epoch(net, x, y, batch: int, eta: float, n_shards: int = 1, stream=
                                float(eta), int(n_shards), _stream(stream)), "nf_train_epoch")
 
 
-def nf_profile(net, enable: bool) -> None:
-    _check(_lib.nf_profile(net, 1 if enable else 0), "nf_profile")
+def nf_profile(net, repeats: int) -> None:
+    """0: off; R >= 1: record, running every launch R times between its events."""
+    _check(_lib.nf_profile(net, int(repeats)), "nf_profile")
 
 
 def nf_profile_read(net, cap: int = 64) -> list:

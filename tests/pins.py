@@ -275,8 +275,39 @@ def check_uniform_acts(m) -> List[str]:
     return [] if np.array_equal(a, b) else ["a single activation is not applied to all layers"]
 
 
+def check_accuracy(m) -> List[str]:
+    """Accuracy counts samples whose largest output (first index among equal
+    ones) is the label: a one-layer identity-like network worked by hand."""
+    # dims [3, 3], relu, W = I, b = 0: the output equals the (non-negative) input
+    theta = np.concatenate([np.eye(3).ravel(), np.zeros(3)])
+    X = np.array([[0.9, 0.1, 0.2],     # argmax 0
+                  [0.5, 0.5, 0.1],     # tie: first index, 0
+                  [0.0, 0.3, 0.7],     # argmax 2
+                  [0.2, 0.8, 0.8]])    # tie: 1
+    labels = np.array([0, 1, 2, 1])
+    got = m.accuracy(theta, (3, 3), ["relu"], X, labels)
+    return [] if got == 0.75 else [f"accuracy {got}, expected 3/4"]
+
+
+def check_kink_side(m) -> List[str]:
+    """The other side of the relu kink, worked by hand: x = 1, W1 = 1, b1 = -1
+    puts z1 exactly at the kink; W2 = 2, b2 = 1, y = 0 (relu output, z2 = 1).
+    The method: relu'(0) = 0, so the tendencies are dW1 = db1 = dW2 = 0 and
+    db2 = 1.  Taking the other side: delta1 = 2, so dW1 = db1 = 2."""
+    theta = np.array([1.0, -1.0, 2.0, 1.0])
+    X, Y = np.array([[1.0]]), np.array([[0.0]])
+    fails = []
+    g0 = m.batch_gradient(theta, (1, 1, 1), ["relu"], X, Y)
+    g1 = m.batch_gradient(theta, (1, 1, 1), ["relu"], X, Y, kink_tol=1e-5)
+    if not np.array_equal(g0, [0.0, 0.0, 0.0, 1.0]):
+        fails.append(f"tendencies at the kink {g0}")
+    if not np.array_equal(g1, [2.0, 2.0, 0.0, 1.0]):
+        fails.append(f"tendencies on the other side of the kink {g1}")
+    return fails
+
+
 ALL_CHECKS: List[Callable] = [
     check_hand_worked, check_activation_values, check_activation_fd, check_gradient_fd,
     check_gradient_autograd, check_sum_of_samples, check_partition, check_replicated_sample,
-    check_uniform_acts,
+    check_uniform_acts, check_accuracy, check_kink_side,
 ]
