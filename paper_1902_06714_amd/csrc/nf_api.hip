@@ -472,7 +472,7 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
     dp.G[l - 1] = n->grads + ly.w_off;
     dp.gb[l - 1] = n->grads + ly.b_off;
     dp.tile_base[l - 1] = base;
-    base += (ly.in + 15) / 16;
+    base += (ly.in + 15) / 16 * ((ly.out + 15) / 16);
     // deltas and previous activations read, tendencies written, parameters updated
     const double M = ly.out, N = ly.in;
     dby += 4.0 * ((double)batch * (M + N) + 3 * M * N + 3 * M);

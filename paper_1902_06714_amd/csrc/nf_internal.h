@@ -103,7 +103,7 @@ struct NarrowDwParams {
   float* bias[NARROW_MAX_LAYERS];
   float* G[NARROW_MAX_LAYERS];             // tendencies, same layout as W / bias
   float* gb[NARROW_MAX_LAYERS];
-  int tile_base[NARROW_MAX_LAYERS + 1];    // first workgroup (16-column tile) of each layer
+  int tile_base[NARROW_MAX_LAYERS + 1];    // first (16-column, 16-unit) tile of each layer
   float scale;
 };
 

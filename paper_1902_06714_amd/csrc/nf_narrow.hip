@@ -3,15 +3,16 @@
 //
 // Kernel 1, per 16-sample tile (one workgroup of 8 waves):
 //   layer 1   z_1 = W_1 x + b_1 on the fp32 matrix cores (16x16x4), the input
-//             width split across the 8 waves and summed in wave order;
+//             width staged through LDS in 128-wide chunks, each wave taking one
+//             16-wide group per chunk, the waves' sums added in wave order;
 //   layers 2+ one thread per (sample, unit) with the previous layer in LDS;
 //   deltas    output delta (a_L - y) f'(z_L) and hidden deltas
 //             (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3), with f'(z_l) kept
 //             in registers from the forward pass.
 // Kernel 2, tendencies of every layer (sections 3.3-3.5): workgroup
-//   (layer, 16-column tile) forms the batch sum of delta (outer) activation
-//   for its columns on the matrix cores (16x16x4), its 8 waves splitting the
-//   batch and their sums added in wave order; it then stores the tendency and
+//   (layer, 16-column tile, 16-unit half) forms the batch sum of delta (outer)
+//   activation for its block on the matrix cores (16x16x4), its 8 waves
+//   splitting the batch and their sums added in wave order; it then stores the tendency and
 //   writes W' = W - (eta/B) G itself (into the other parameter buffer), so no
 //   workgroup waits on another.  The order of every sum is fixed, so results
 //   are reproducible bit for bit.
@@ -23,13 +24,23 @@ namespace nf {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// v if c, else zeros; written per component (a conditional on the vector
+// type itself is lowered through private memory)
+__device__ __forceinline__ float4 keep_if(bool c, float4 v) {
+  return make_float4(c ? v.x : 0.0f, c ? v.y : 0.0f, c ? v.z : 0.0f, c ? v.w : 0.0f);
+}
+
 constexpr int N1_WAVES = 8;
-constexpr int N1_UNROLL = 8;  // 16-wide input groups loaded per wave before use
+constexpr int N1_KC = 16 * N1_WAVES;  // inputs per LDS stage: one 16-wide group per wave
+constexpr int N1_KP = N1_KC + 4;      // padded LDS row
+constexpr int N1_PRE = 8;             // chunks requested together
 
 template <bool TRAIN>
 __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowFwdParams p) {
   constexpr int T = NARROW_TILE;
   constexpr int NW = NARROW_WIDTH;
+  __shared__ __attribute__((aligned(16))) float xs[2][T][N1_KP];     // layer-1 input chunk
+  __shared__ __attribute__((aligned(16))) float wsl[2][NW][N1_KP];   // W_1 chunk
   __shared__ float zp[N1_WAVES][T][NW + 1];
   __shared__ float hs[2][T][NW + 1];                         // activations, then deltas
   __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];    // W_2 .. W_L
@@ -41,25 +52,33 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
   const int s0 = blockIdx.x * T;
 
   // stage the small layers' weights and every bias in LDS (read again and
-  // again by the per-sample threads below); the loads are issued together
-  // and land while layer 1 runs
-  constexpr int NSTAGE = (NARROW_MAX_LAYERS - 1) * NW * NW / (N1_WAVES * 64);
-  static_assert((NARROW_MAX_LAYERS - 1) * NW * NW % (N1_WAVES * 64) == 0, "staging split");
-  float wst[NSTAGE];
+  // again by the per-sample threads below).  The layer loops are unrolled so
+  // that every kernel-argument index is a constant; the loads are issued
+  // together and land while layer 1 runs.  Out-of-range entries read W_1[0][0]
+  // (always present) and are zeroed.
+  constexpr int NPER = NW * NW / (N1_WAVES * 64);
+  static_assert(NW * NW % (N1_WAVES * 64) == 0, "staging split");
+  float wst[NARROW_MAX_LAYERS - 1][NPER];
 #pragma unroll
-  for (int u = 0; u < NSTAGE; ++u) {
-    const int e = tid + u * N1_WAVES * 64;
-    const int l = e / (NW * NW) + 2, rem = e % (NW * NW), row = rem / NW, colw = rem % NW;
-    const bool ok = l <= p.L && row < p.dims[l] && colw < p.dims[l - 1];
-    // out-of-range entries read W_1[0][0] (always present) and are zeroed
-    const float* src = ok ? p.W[l - 1] + (int64_t)row * p.ldw[l - 1] + colw : p.W[0];
-    const float v = *src;
-    wst[u] = ok ? v : 0.0f;
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li) {
+    const int l = li + 2;
+#pragma unroll
+    for (int u = 0; u < NPER; ++u) {
+      const int e = tid + u * N1_WAVES * 64, row = e / NW, colw = e % NW;
+      const bool ok = l <= p.L && row < p.dims[l] && colw < p.dims[l - 1];
+      const float* src = ok ? p.W[l - 1] + (int64_t)row * p.ldw[l - 1] + colw : p.W[0];
+      const float v = *src;
+      wst[li][u] = ok ? v : 0.0f;
+    }
   }
-  float bst = 0.0f;
-  if (tid < NARROW_MAX_LAYERS * NW) {
-    const int l = tid / NW + 1, u = tid % NW;
-    if (l <= p.L && u < p.dims[l]) bst = p.bias[l - 1][u];
+  float bst[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int l = 1; l <= NARROW_MAX_LAYERS; ++l) {
+    const int u = tid & (NW - 1);
+    const bool ok = l <= p.L && u < p.dims[l];
+    const float* src = ok ? p.bias[l - 1] + u : p.W[0];
+    const float v = *src;
+    bst[l - 1] = ok ? v : 0.0f;
   }
   // this thread's target (sample tid / 32, output unit tid % 32)
   float ytg = 0.0f;
@@ -68,41 +87,59 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
     if (ys < p.B && yu < p.dims[p.L]) ytg = p.Y[(int64_t)ys * p.dims[p.L] + yu];
   }
 
-  // ---- layer 1 on the matrix cores: lane (r, g) = (lane % 16, lane / 16)
-  // feeds sample r and units r, 16 + r with the inputs [16 k + 4 g, 16 k + 4 g + 4)
-  // of every 16-wide group k it handles; the four MFMAs of a group take one
-  // of those four inputs each, so every product of the dot product is formed.
-  // Out-of-range rows and inputs are loaded from a valid address and zeroed.
+  // ---- layer 1 on the matrix cores.  The inputs go through LDS in chunks of
+  // N1_KC, read from global memory with contiguous full-line loads (X rows and
+  // W_1 rows) that are all issued before the first chunk is used, and passed
+  // through two LDS buffers chunk by chunk as the data arrives.
+  // Wave w takes the w-th 16-wide group of every chunk; lane (r, g) =
+  // (lane % 16, lane / 16) feeds sample r and units r, 16 + r with inputs
+  // 4 g .. 4 g + 3 of the group, one per MFMA, so every product of the dot
+  // product is formed.  Out-of-range rows and inputs are read from a valid
+  // address and stored as zero.
   {
     const int r = lane & 15, g = lane >> 4;
     const int d1 = p.dims[1];
-    const bool x_ok = s0 + r < p.B;
-    const bool w0_ok = r < d1, w1_ok = 16 + r < d1;
-    const float* xrow = p.X + (int64_t)(x_ok ? s0 + r : p.B - 1) * p.d0;
-    const float* w0 = p.W[0] + (int64_t)(w0_ok ? r : 0) * p.ldw[0];
-    const float* w1 = p.W[0] + (int64_t)(w1_ok ? 16 + r : 0) * p.ldw[0];
+    const int nch = (p.d0 + N1_KC - 1) / N1_KC;
+    // this thread's share of a chunk: one float4 of X, two of W_1
+    const int xrow = tid / (N1_KC / 4), xq = tid % (N1_KC / 4);
+    const bool xrow_ok = s0 + xrow < p.B;
+    const float* xsrc = p.X + (int64_t)(xrow_ok ? s0 + xrow : p.B - 1) * p.d0;
+    const bool w0_ok = xrow < d1, w1_ok = 16 + xrow < d1;
+    const float* wsrc0 = p.W[0] + (int64_t)(w0_ok ? xrow : 0) * p.ldw[0];
+    const float* wsrc1 = p.W[0] + (int64_t)(w1_ok ? 16 + xrow : 0) * p.ldw[0];
     // two accumulator chains per unit block (inputs 4g, 4g+2 and 4g+1, 4g+3
     // of each group) keep more MFMAs in flight; they are added at the end
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
     floatx4 acc2 = {0.f, 0.f, 0.f, 0.f}, acc3 = {0.f, 0.f, 0.f, 0.f};
-    const int ngroups = (p.d0 + 15) / 16;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int gb = wave; gb < ngroups; gb += N1_WAVES * N1_UNROLL) {
-      float4 xv[N1_UNROLL], wa[N1_UNROLL], wb[N1_UNROLL];
+    // every chunk of a block of N1_PRE chunks is requested at once (one memory
+    // latency per block); chunks then pass through LDS as they arrive
+    for (int cb = 0; cb < nch; cb += N1_PRE) {
+      float4 xr[N1_PRE], wr0[N1_PRE], wr1[N1_PRE];
 #pragma unroll
-      for (int u = 0; u < N1_UNROLL; ++u) {
-        const int k = (gb + u * N1_WAVES) * 16 + g * 4;
-        const int kc = k < p.d0 ? k : 0;
-        xv[u] = *reinterpret_cast<const float4*>(xrow + kc);
-        wa[u] = *reinterpret_cast<const float4*>(w0 + kc);
-        wb[u] = *reinterpret_cast<const float4*>(w1 + kc);
+      for (int u = 0; u < N1_PRE; ++u) {
+        const int k = (cb + u) * N1_KC + 4 * xq;
+        const bool k_ok = k < p.d0;
+        const int kc = k_ok ? k : 0;
+        const float4 xv = *reinterpret_cast<const float4*>(xsrc + kc);
+        const float4 w0 = *reinterpret_cast<const float4*>(wsrc0 + kc);
+        const float4 w1 = *reinterpret_cast<const float4*>(wsrc1 + kc);
+        xr[u] = keep_if(k_ok && xrow_ok, xv);
+        wr0[u] = keep_if(k_ok && w0_ok, w0);
+        wr1[u] = keep_if(k_ok && w1_ok, w1);
       }
+      // chunks past the input width were loaded as zeros, so the whole block
+      // is processed unconditionally (keeps the loop fully unrolled)
 #pragma unroll
-      for (int u = 0; u < N1_UNROLL; ++u) {
-        const bool k_ok = (gb + u * N1_WAVES) * 16 + g * 4 < p.d0;
-        const float4 x = (k_ok && x_ok) ? xv[u] : zero;
-        const float4 a = (k_ok && w0_ok) ? wa[u] : zero;
-        const float4 b = (k_ok && w1_ok) ? wb[u] : zero;
+      for (int u = 0; u < N1_PRE; ++u) {
+        const int buf = u & 1;
+        *reinterpret_cast<float4*>(&xs[buf][xrow][4 * xq]) = xr[u];
+        *reinterpret_cast<float4*>(&wsl[buf][xrow][4 * xq]) = wr0[u];
+        *reinterpret_cast<float4*>(&wsl[buf][16 + xrow][4 * xq]) = wr1[u];
+        __syncthreads();
+        const int ko = 16 * wave + 4 * g;
+        const float4 x = *reinterpret_cast<const float4*>(&xs[buf][r][ko]);
+        const float4 a = *reinterpret_cast<const float4*>(&wsl[buf][r][ko]);
+        const float4 b = *reinterpret_cast<const float4*>(&wsl[buf][16 + r][ko]);
         acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, a.x, acc0, 0, 0, 0);
         acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, b.x, acc1, 0, 0, 0);
         acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, a.y, acc2, 0, 0, 0);
@@ -112,6 +149,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
         acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, a.w, acc2, 0, 0, 0);
         acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, b.w, acc3, 0, 0, 0);
       }
+      __syncthreads();   // the next block's first chunk reuses buffer 0
     }
     acc0 += acc2;
     acc1 += acc3;
@@ -123,12 +161,16 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
     }
   }
 #pragma unroll
-  for (int u = 0; u < NSTAGE; ++u) {
-    const int e = tid + u * N1_WAVES * 64;
-    const int l = e / (NW * NW) + 2, rem = e % (NW * NW);
-    ws[l - 2][rem / NW][rem % NW] = wst[u];
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < NPER; ++u) {
+      const int e = tid + u * N1_WAVES * 64;
+      ws[li][e / NW][e % NW] = wst[li][u];
+    }
+  if (tid < NW) {
+#pragma unroll
+    for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bs[l][tid] = bst[l];
   }
-  if (tid < NARROW_MAX_LAYERS * NW) bs[tid / NW][tid % NW] = bst;
   __syncthreads();
 
   // ---- thread (s, j): sample s of the tile, unit j of the current layer
@@ -203,21 +245,21 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
   }
 }
 
-// Workgroup = 8 waves, one (layer, 16-column tile) over the whole batch:
-// G[u][c0 + r] = sum over samples of delta[s][u] a_prev[s][c0 + r] on the
-// 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
+// Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the whole
+// batch: G[16 h + u][c0 + r] = sum over samples of delta[s][16 h + u] a_prev[s][c0 + r]
+// on the 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
 // waves' sums are added in wave order, then the tile applies the SGD step.
 constexpr int N2_WAVES = 8;
 constexpr int N2_UNROLL = 32;  // groups of 4 samples loaded before use
 
 __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDwParams p) {
-  __shared__ float red[N2_WAVES][NARROW_WIDTH][17];
-  __shared__ float bred[N2_WAVES][4][NARROW_WIDTH];
+  __shared__ float red[N2_WAVES][16][17];
+  __shared__ float bred[N2_WAVES][4][16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // consecutive workgroups land on different XCDs (round robin over 8); give
-  // each XCD a contiguous run of tiles so that neighbouring 16-column tiles,
-  // which share 128-byte lines of the input rows, share one L2
+  // each XCD a contiguous run of tiles so that the two unit halves of a column
+  // tile, and neighbouring column tiles, share the input rows in one L2
   const int nwg = p.tile_base[p.L];
   const int per = (nwg + 7) / 8;
   const int full = nwg - 8 * (per - 1);       // XCDs that get `per` tiles
@@ -225,71 +267,63 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   const int tile = xcd < full ? xcd * per + slot : full * per + (xcd - full) * (per - 1) + slot;
   int l = 0;
   while (l + 1 < p.L && tile >= p.tile_base[l + 1]) ++l;
-  const int c = tile - p.tile_base[l];
   const int M = p.dims[l + 1], N = p.dims[l];
-  const int c0 = c * 16;
+  const int nh = (M + 15) / 16;
+  const int c = (tile - p.tile_base[l]) / nh, h = (tile - p.tile_base[l]) % nh;
+  const int c0 = c * 16, u0 = h * 16;
   const float* xop = l == 0 ? p.X : p.A[l - 1];
   const int64_t ldx = l == 0 ? p.dims[0] : NARROW_WIDTH;
-  const float* dl = p.D[l];
+  const float* dl = p.D[l] + u0;
 
   const int r = lane & 15, g = lane >> 4;
   const bool col_ok = c0 + r < N;
   const float* xcol = xop + (col_ok ? c0 + r : 0);
-  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-  float bs0 = 0.0f, bs1 = 0.0f;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  float bsum = 0.0f;
   const int ngroups = (p.B + 3) / 4;
   for (int gb = wave; gb < ngroups; gb += N2_WAVES * N2_UNROLL) {
-    float d0v[N2_UNROLL], d1v[N2_UNROLL], xv[N2_UNROLL];
+    float dv[N2_UNROLL], xv[N2_UNROLL];
 #pragma unroll
     for (int u = 0; u < N2_UNROLL; ++u) {
       const int smp = (gb + u * N2_WAVES) * 4 + g;
       const int sc = smp < p.B ? smp : p.B - 1;
-      d0v[u] = dl[(int64_t)sc * NARROW_WIDTH + r];
-      d1v[u] = dl[(int64_t)sc * NARROW_WIDTH + 16 + r];
+      dv[u] = dl[(int64_t)sc * NARROW_WIDTH + r];
       xv[u] = xcol[(int64_t)sc * ldx];
     }
 #pragma unroll
     for (int u = 0; u < N2_UNROLL; ++u) {
       const bool ok = (gb + u * N2_WAVES) * 4 + g < p.B;
-      const float a0 = ok ? d0v[u] : 0.0f, a1 = ok ? d1v[u] : 0.0f;
+      const float a = ok ? dv[u] : 0.0f;
       const float b = (ok && col_ok) ? xv[u] : 0.0f;
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b, acc1, 0, 0, 0);
-      bs0 += a0;
-      bs1 += a1;
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+      bsum += a;
     }
   }
-  // accumulator register v of lane (r, g): unit 4 g + v (+16), column c0 + r
+  // accumulator register v of lane (r, g): unit u0 + 4 g + v, column c0 + r
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    red[wave][4 * g + v][r] = acc0[v];
-    red[wave][16 + 4 * g + v][r] = acc1[v];
-  }
-  if (c == 0) {
-    bred[wave][g][r] = bs0;
-    bred[wave][g][16 + r] = bs1;
-  }
+  for (int v = 0; v < 4; ++v) red[wave][4 * g + v][r] = acc[v];
+  if (c == 0) bred[wave][g][r] = bsum;
   __syncthreads();
 
-  {
-    const int i = tid >> 4, jj = tid & 15;   // unit, column within the tile
+  if (tid < 256) {
+    const int i = tid >> 4, jj = tid & 15;   // unit within the half, column within the tile
     float gsum = red[0][i][jj];
 #pragma unroll
     for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][i][jj];
-    if (i < M && c0 + jj < N) {
-      const int64_t o = (int64_t)i * p.ldw[l] + c0 + jj;
+    if (u0 + i < M && c0 + jj < N) {
+      const int64_t o = (int64_t)(u0 + i) * p.ldw[l] + c0 + jj;
       p.G[l][o] = gsum;
       p.W[l][o] = fmaf(-p.scale, gsum, p.Win[l][o]);
     }
   }
-  if (c == 0 && tid < M) {
+  if (c == 0 && tid < 16 && u0 + tid < M) {
     float gsum = 0.0f;
 #pragma unroll
     for (int w = 0; w < N2_WAVES; ++w)
 #pragma unroll
       for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
-    p.gb[l][tid] = gsum;
-    p.bias[l][tid] = fmaf(-p.scale, gsum, p.bin[l][tid]);
+    p.gb[l][u0 + tid] = gsum;
+    p.bias[l][u0 + tid] = fmaf(-p.scale, gsum, p.bin[l][u0 + tid]);
   }
 }
 
