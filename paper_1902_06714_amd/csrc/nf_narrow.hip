@@ -33,15 +33,22 @@ __device__ __forceinline__ float4 keep_if(bool c, float4 v) {
 constexpr int N1_WAVES = 8;
 constexpr int N1_KC = 16 * N1_WAVES;  // inputs per LDS stage: one 16-wide group per wave
 constexpr int N1_KP = N1_KC + 4;      // padded LDS row
-constexpr int N1_PRE = 8;             // chunks requested together
+// chunks requested together: 8 for training (one launch of few workgroups),
+// 4 for inference (fewer registers, two workgroups per CU)
+constexpr int N1_PRE_TRAIN = 8;
+constexpr int N1_PRE_INFER = 4;
 
-template <bool TRAIN>
+template <bool TRAIN, int N1_PRE>
 __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowFwdParams p) {
   constexpr int T = NARROW_TILE;
   constexpr int NW = NARROW_WIDTH;
-  __shared__ __attribute__((aligned(16))) float xs[2][T][N1_KP];     // layer-1 input chunk
-  __shared__ __attribute__((aligned(16))) float wsl[2][NW][N1_KP];   // W_1 chunk
-  __shared__ float zp[N1_WAVES][T][NW + 1];
+  // layer-1 staging (input chunk xs, W_1 chunk wsl, two buffers each); the
+  // per-wave partial sums zp reuse the same bytes once layer 1 is done
+  __shared__ __attribute__((aligned(16))) float stage[2 * (T + NW) * N1_KP];
+  static_assert(N1_WAVES * T * (NW + 1) <= 2 * (T + NW) * N1_KP, "zp must fit the staging area");
+  auto xs = reinterpret_cast<float(*)[T][N1_KP]>(stage);
+  auto wsl = reinterpret_cast<float(*)[NW][N1_KP]>(stage + 2 * T * N1_KP);
+  auto zp = reinterpret_cast<float(*)[T][NW + 1]>(stage);
   __shared__ float hs[2][T][NW + 1];                         // activations, then deltas
   __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];    // W_2 .. W_L
   __shared__ float bs[NARROW_MAX_LAYERS][NW];                // b_1 .. b_L
@@ -330,9 +337,9 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s) {
   const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
   if (train)
-    narrow_fwd_kernel<true><<<grid, N1_WAVES * 64, 0, s>>>(p);
+    narrow_fwd_kernel<true, N1_PRE_TRAIN><<<grid, N1_WAVES * 64, 0, s>>>(p);
   else
-    narrow_fwd_kernel<false><<<grid, N1_WAVES * 64, 0, s>>>(p);
+    narrow_fwd_kernel<false, N1_PRE_INFER><<<grid, N1_WAVES * 64, 0, s>>>(p);
   return hipGetLastError();
 }
 
