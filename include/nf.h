@@ -125,6 +125,33 @@ nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_
 nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
                          int64_t batch, float eta, int32_t n_shards, void* stream);
 
+/* One training step on a single sample (section 3.4, train_single): the
+ * forward pass, back-propagation and the update for the sample d_x [d_0] with
+ * target d_y [d_L].  Identical to nf_train_batch with batch 1 and one shard. */
+nf_status nf_train_single(nf_net* net, const float* d_x, const float* d_y, float eta, void* stream);
+
+/* Training on randomly placed windows of the sample set, as the paper's
+ * example program draws its mini-batches (section 4): for t = 0 .. n_steps-1,
+ * in order, one nf_train_batch step on samples [s_t, s_t + batch) with
+ *     s_t = min(int(pos[t] * (n_samples - batch + 1)), n_samples - batch),
+ * the product taken in fp32 (the paper's default real kind) and truncated.
+ * Windows may overlap and samples may be left out, as in the paper.  The
+ * uniform numbers pos[0 .. n_steps-1] in [0, 1) are drawn by the caller and
+ * passed in host memory; NF_EINVAL if one is outside [0, 1) or not finite
+ * (nothing is launched then).  d_x: [n_samples][d_0], d_y: [n_samples][d_L]. */
+nf_status nf_train_windows(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
+                           int64_t batch, const float* host_pos, int64_t n_steps, float eta,
+                           int32_t n_shards, void* stream);
+
+/* Classification accuracy (section 4): the number of the n samples whose
+ * network output and target have their largest entry at the same index (the
+ * first index among equal largest entries, as Fortran's maxloc).  d_x: [n][d_0]
+ * inputs, d_y: [n][d_L] targets (one-hot class vectors in the paper).  A
+ * sample whose output or target holds a NaN counts as incorrect.  Runs on
+ * `stream`, waits for it, and writes the count to *host_correct. */
+nf_status nf_accuracy(nf_net* net, const float* d_x, const float* d_y, int64_t n,
+                      int64_t* host_correct, void* stream);
+
 /* Per-kernel timing, for measuring the method's computational performance the
  * way section 5 reports it (elapsed time), one kernel at a time.  While
  * recording is on, every kernel the net launches is bracketed by a pair of HIP

@@ -308,6 +308,53 @@ def train_epoch(theta, dims, acts, X, Y, batch, eta, shards=1, precision="f32",
     return theta
 
 
+def window_start(pos: float, n: int, batch: int) -> int:
+    """Start of the mini-batch window drawn by the example program of section
+    4: the integer part of pos * (n - batch + 1), with pos uniform in [0, 1).
+    The product is taken in fp32, the paper's default real kind; a product
+    that rounds up to n - batch + 1 is kept inside the sample set."""
+    if not 0.0 <= pos < 1.0:
+        raise ValueError("pos must lie in [0, 1)")
+    if batch > n:
+        raise ValueError("the window is longer than the sample set")
+    prod = np.float32(pos) * np.float32(n - batch + 1)
+    return min(int(prod), n - batch)
+
+
+def train_windows(theta, dims, acts, X, Y, batch, pos, eta, shards=1, precision="f32"):
+    """One mini-batch step per entry of pos, in order, each on the window of
+    ``batch`` samples that window_start places (section 4)."""
+    n = np.asarray(X).shape[0]
+    for p in pos:
+        s = window_start(float(p), n, batch)
+        theta, _ = train_batch(theta, dims, acts, X[s:s + batch], Y[s:s + batch], eta, shards,
+                               precision)
+    return theta
+
+
+def _first_argmax(v: np.ndarray) -> int:
+    """Index of the first largest entry of v (Fortran's maxloc), or -1 when v
+    holds a NaN."""
+    best = 0
+    for j in range(1, v.shape[0]):
+        if np.isnan(v[j]):
+            return -1
+        if v[j] > v[best]:
+            best = j
+    return -1 if np.isnan(v[0]) else best
+
+
+def correct_count(out, Y) -> int:
+    """Number of rows whose output and one-hot target peak at the same index
+    (section 4's accuracy before dividing by the sample count); a row with a
+    NaN counts as incorrect."""
+    n = 0
+    for o, y in zip(np.asarray(out), np.asarray(Y)):
+        i, j = _first_argmax(o), _first_argmax(y)
+        n += int(i >= 0 and i == j)
+    return n
+
+
 def accuracy(theta, dims, acts, X, labels) -> float:
     """Fraction of samples whose largest output (first index among ties) is
     the label."""

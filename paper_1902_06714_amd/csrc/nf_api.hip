@@ -74,6 +74,10 @@ struct nf_net {
   // per-piece tendencies
   float* partial = nullptr;
   int64_t partial_floats = 0;
+  // accuracy: network outputs of one chunk of samples, and the correct count
+  float* evalbuf = nullptr;
+  int64_t eval_floats = 0;
+  unsigned long long* dcount = nullptr;
   // every layer after the input has at most NARROW_WIDTH units
   bool narrow = false;
   hipStream_t last = nullptr;
@@ -482,6 +486,20 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
   return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
 }
 
+// f(z_L) of `batch` samples into out [batch][d_L] (inference, no stash)
+nf_status infer(nf_net* n, const float* x, int64_t batch, float* out, hipStream_t s) {
+  nf_status st = ensure_ws(n, batch);
+  if (st != NF_OK) return st;
+  if (n->narrow && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0])) {
+    double by, fl;
+    narrow_fwd_work(n, batch, false, &by, &fl);
+    const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
+    return timed(n, "narrow_fwd_infer", by, fl, s,
+                 [&] { return nf::launch_narrow_fwd(false, fp, s); });
+  }
+  return run_forward(n, x, nullptr, batch, out, false, s);
+}
+
 nf_status check_net(const nf_net* n) {
   if (!n) return fail(NF_EINVAL, "net is NULL");
   return NF_OK;
@@ -611,6 +629,8 @@ nf_status nf_net_destroy(nf_net* net) {
     clear_recs(net);
     free_ws(net);
     if (net->partial) (void)hipFree(net->partial);
+    if (net->evalbuf) (void)hipFree(net->evalbuf);
+    if (net->dcount) (void)hipFree(net->dcount);
     if (net->pbuf[0]) (void)hipFree(net->pbuf[0]);
     if (net->pbuf[1]) (void)hipFree(net->pbuf[1]);
     if (net->grads) (void)hipFree(net->grads);
@@ -689,17 +709,7 @@ nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out,
     DeviceGuard g(net->device);
     if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    st = ensure_ws(net, batch);
-    if (st != NF_OK) return st;
-    if (net->narrow && net->dims[0] % 4 == 0 && vec_ok(d_x, net->dims[0])) {
-      double by, fl;
-      narrow_fwd_work(net, batch, false, &by, &fl);
-      const nf::NarrowFwdParams fp = narrow_fwd_params(net, d_x, nullptr, batch, d_out);
-      st = timed(net, "narrow_fwd_infer", by, fl, s,
-                 [&] { return nf::launch_narrow_fwd(false, fp, s); });
-    } else {
-      st = run_forward(net, d_x, nullptr, batch, d_out, false, s);
-    }
+    st = infer(net, d_x, batch, d_out, s);
     net->last = s;
     net->used = true;
     return st;
@@ -747,6 +757,105 @@ nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_
     net->last = s;
     net->used = true;
     return st;
+  });
+}
+
+nf_status nf_train_single(nf_net* net, const float* d_x, const float* d_y, float eta, void* stream) {
+  return nf_train_batch(net, d_x, d_y, 1, eta, 1, stream);
+}
+
+nf_status nf_train_windows(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
+                           int64_t batch, const float* host_pos, int64_t n_steps, float eta,
+                           int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    if (n_samples < batch) return fail(NF_ESHAPE, "n_samples must be at least batch");
+    if (n_steps < 0) return fail(NF_EINVAL, "n_steps must not be negative");
+    if (n_steps > 0 && !host_pos) return fail(NF_EINVAL, "host_pos is NULL");
+    // every start is checked before anything is launched
+    const int64_t last = n_samples - batch;
+    const float span = (float)(last + 1);
+    std::vector<int64_t> start((size_t)n_steps);
+    for (int64_t t = 0; t < n_steps; ++t) {
+      const float pos = host_pos[t];
+      if (!(pos >= 0.0f && pos < 1.0f)) return fail(NF_EINVAL, "pos values must lie in [0, 1)");
+      const float prod = pos * span;
+      start[(size_t)t] = std::min((int64_t)prod, last);
+    }
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    for (int64_t t = 0; t < n_steps && st == NF_OK; ++t)
+      st = train_step(net, d_x + start[(size_t)t] * d0, d_y + start[(size_t)t] * dl, batch, eta,
+                      n_shards, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+nf_status nf_accuracy(nf_net* net, const float* d_x, const float* d_y, int64_t n,
+                      int64_t* host_correct, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    if (st != NF_OK) return st;
+    if (!d_x || !d_y || !host_correct) return fail(NF_EINVAL, "x, y or host_correct is NULL");
+    if (n <= 0) return fail(NF_EINVAL, "n must be positive");
+    if (n > (int64_t)1 << 40) return fail(NF_ESHAPE, "n is too large");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    // outputs are produced chunk by chunk into a buffer of at most 16 M floats
+    const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(n, std::min<int64_t>(
+                                                   (int64_t)1 << 14, ((int64_t)1 << 24) / dl)));
+    if (chunk * dl > net->eval_floats || !net->dcount) {
+      st = sync_net(net);
+      if (st != NF_OK) return st;
+      if (!net->dcount) {
+        hipError_t e = hipMalloc(&net->dcount, sizeof(unsigned long long));
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          net->dcount = nullptr;
+          return fail(NF_ENOMEM, "hipMalloc of the counter failed");
+        }
+      }
+      if (chunk * dl > net->eval_floats) {
+        float* buf = nullptr;
+        hipError_t e = hipMalloc(&buf, (size_t)(chunk * dl) * sizeof(float));
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(NF_ENOMEM, "hipMalloc of the output buffer failed");
+        }
+        if (net->evalbuf) (void)hipFree(net->evalbuf);
+        net->evalbuf = buf;
+        net->eval_floats = chunk * dl;
+      }
+    }
+    hipError_t e = hipMemsetAsync(net->dcount, 0, sizeof(unsigned long long), s);
+    net->last = s;
+    net->used = true;
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    for (int64_t b = 0; b < n && st == NF_OK; b += chunk) {
+      const int64_t m = std::min(chunk, n - b);
+      st = infer(net, d_x + b * d0, m, net->evalbuf, s);
+      if (st != NF_OK) break;
+      e = nf::launch_count_correct(net->evalbuf, dl, d_y + b * dl, dl, m, (int)dl, net->dcount, s);
+      if (e != hipSuccess) st = hip_fail(e, "count_correct launch");
+    }
+    if (st != NF_OK) return st;
+    unsigned long long count = 0;
+    e = hipMemcpyAsync(&count, net->dcount, sizeof(count), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "reading the correct count");
+    *host_correct = (int64_t)count;
+    return NF_OK;
   });
 }
 

@@ -110,4 +110,10 @@ struct NarrowDwParams {
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s);
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 
+// Adds to *count the number of rows s < n for which out[s][0..d) and
+// y[s][0..d) have their first largest entry at the same index (rows holding a
+// NaN never count).  Row pitches ldo and ldy in floats.
+hipError_t launch_count_correct(const float* out, int64_t ldo, const float* y, int64_t ldy,
+                                int64_t n, int d, unsigned long long* count, hipStream_t s);
+
 }  // namespace nf

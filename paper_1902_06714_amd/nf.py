@@ -66,6 +66,13 @@ _sig = {
     "nf_train_epoch": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_float, ctypes.c_int32,
                                       ctypes.c_void_p]),
+    "nf_train_single": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+                                       ctypes.c_void_p]),
+    "nf_train_windows": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]),
+    "nf_accuracy": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                   ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p]),
     "nf_profile": (ctypes.c_int, [_net_p, ctypes.c_int32]),
     "nf_profile_read": (ctypes.c_int, [_net_p, ctypes.POINTER(nf_kernel_stat), ctypes.c_int32,
                                        ctypes.POINTER(ctypes.c_int32)]),
@@ -171,6 +178,30 @@ def nf_train_batch(net, x, y, eta: float, n_shards: int = 1, stream=None) -> Non
 def nf_train_epoch(net, x, y, batch: int, eta: float, n_shards: int = 1, stream=None) -> None:
     _check(_lib.nf_train_epoch(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0], int(batch),
                                float(eta), int(n_shards), _stream(stream)), "nf_train_epoch")
+
+
+def nf_train_single(net, x, y, eta: float, stream=None) -> None:
+    """x: [d_0] (or [1][d_0]), y: [d_L] GPU tensors."""
+    _check(_lib.nf_train_single(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), float(eta),
+                                _stream(stream)), "nf_train_single")
+
+
+def nf_train_windows(net, x, y, batch: int, pos, eta: float, n_shards: int = 1,
+                     stream=None) -> None:
+    """One step per entry of pos (uniform numbers in [0, 1), host array) on
+    the window of `batch` samples it places in (x, y)."""
+    p = np.ascontiguousarray(pos, dtype=np.float32)
+    _check(_lib.nf_train_windows(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0], int(batch),
+                                 p.ctypes.data if p.size else None, p.size, float(eta),
+                                 int(n_shards), _stream(stream)), "nf_train_windows")
+
+
+def nf_accuracy(net, x, y, stream=None) -> int:
+    """Number of samples whose output and target peak at the same index."""
+    c = ctypes.c_int64()
+    _check(_lib.nf_accuracy(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0], ctypes.byref(c),
+                            _stream(stream)), "nf_accuracy")
+    return int(c.value)
 
 
 def nf_profile(net, repeats: int) -> None:

@@ -20,7 +20,8 @@ Generator (documented so that any side can reproduce it bit for bit):
 * class label in {0..9}: ``((u >> 32) * 10) >> 32``.
 
 Streams: 0 training inputs, 1 training labels, 3 held-out inputs,
-4 held-out labels, 100 + 2l the weights of layer l (1-based), 101 + 2l the
+4 held-out labels, 5 the uniform numbers that place random mini-batch
+windows (one per step), 100 + 2l the weights of layer l (1-based), 101 + 2l the
 biases of layer l.
 
 The paper trains on MNIST (28x28 greyscale digits scaled to [0, 1], one-hot
@@ -44,6 +45,7 @@ STREAM_X_TRAIN = 0
 STREAM_Y_TRAIN = 1
 STREAM_X_HELDOUT = 3
 STREAM_Y_HELDOUT = 4
+STREAM_WINDOWS = 5
 
 # activation names, in the order of the C enum nf_act
 ACTIVATIONS = ("gaussian", "relu", "sigmoid", "step", "tanh")
@@ -112,6 +114,12 @@ def labels(seed: int, stream: int, n: int, classes: int = 10) -> np.ndarray:
         with np.errstate(over="ignore"):
             out[s:s + c] = ((u >> np.uint64(32)) * np.uint64(classes)) >> np.uint64(32)
     return out
+
+
+def window_positions(seed: int, n_steps: int) -> np.ndarray:
+    """The uniform numbers in [0, 1) that place the mini-batch window of each
+    of n_steps random-window steps."""
+    return uniform(seed, STREAM_WINDOWS, n_steps)
 
 
 def one_hot(lbl: np.ndarray, classes: int = 10) -> np.ndarray:

@@ -306,8 +306,69 @@ def check_kink_side(m) -> List[str]:
     return fails
 
 
+def check_window_starts(m) -> List[str]:
+    """The window start of section 4 is the integer part of pos * (n - B + 1):
+    exact on a grid of pos = k / 64 (products exact in fp32), 0 at pos = 0,
+    the last window n - B at the largest fp32 below 1, and every start in
+    0 .. n - B reached, none outside."""
+    fails = []
+    for n in range(1, 41):
+        for b in range(1, n + 1):
+            span = n - b + 1
+            seen = set()
+            for k in range(64):
+                got = m.window_start(k / 64.0, n, b)
+                if got != (k * span) // 64:
+                    fails.append(f"n={n} B={b} pos={k}/64: start {got}, expected {(k * span) // 64}")
+                    return fails
+                seen.add(got)
+            if span <= 64 and seen != set(range(span)):
+                fails.append(f"n={n} B={b}: starts {sorted(seen)} do not cover 0..{span - 1}")
+                return fails
+    top = float(np.nextafter(np.float32(1.0), np.float32(0.0)))
+    for span in (1, 2, 3, 1000, 59001, (1 << 23) + 1, (1 << 24) - 1):
+        got = m.window_start(top, span + 99, 100)
+        if got != span - 1:
+            fails.append(f"span {span}: start at the top of [0,1) is {got}, expected {span - 1}")
+    return fails
+
+
+def check_windows_sequential(m) -> List[str]:
+    """Windows placed back to back (pos_t = (t B + 1/2) / (n - B + 1)) are the
+    consecutive mini-batches of one epoch, taken in the same order: the two
+    training loops give identical parameters."""
+    rng = np.random.default_rng(7)
+    dims, acts = (3, 4, 2), ["sigmoid", "sigmoid"]
+    theta = rng.normal(size=m.param_count(dims))
+    X, Y = rng.uniform(size=(12, 3)), rng.uniform(size=(12, 2))
+    B = 3
+    pos = [(t * B + 0.5) / (12 - B + 1) for t in range(4)]
+    a = m.train_windows(theta, dims, acts, X, Y, B, pos, 0.5, precision="f64")
+    e = m.train_epoch(theta, dims, acts, X, Y, B, 0.5, precision="f64")
+    fails = [] if np.array_equal(a, e) else ["back-to-back windows differ from one epoch"]
+    rev = m.train_windows(theta, dims, acts, X, Y, B, pos[::-1], 0.5, precision="f64")
+    if np.array_equal(rev, e):
+        fails.append("the order of the windows has no effect")
+    return fails
+
+
+def check_correct_count(m) -> List[str]:
+    """Outputs against one-hot targets, worked by hand: the first index among
+    equal largest outputs is the prediction, and a NaN row never counts."""
+    out = np.array([[0.9, 0.1, 0.2],        # predicts 0, target 0: correct
+                    [0.5, 0.5, 0.1],        # tie, predicts 0, target 1: wrong
+                    [0.0, 0.3, 0.7],        # predicts 2, target 2: correct
+                    [0.2, 0.8, 0.8],        # tie, predicts 1, target 1: correct
+                    [0.1, np.nan, 0.9],     # NaN: wrong
+                    [0.3, 0.3, 0.3]])       # all equal, predicts 0, target 0: correct
+    Y = np.eye(3)[[0, 1, 2, 1, 2, 0]]
+    got = m.correct_count(out, Y)
+    return [] if got == 4 else [f"correct count {got}, expected 4"]
+
+
 ALL_CHECKS: List[Callable] = [
     check_hand_worked, check_activation_values, check_activation_fd, check_gradient_fd,
     check_gradient_autograd, check_sum_of_samples, check_partition, check_replicated_sample,
-    check_uniform_acts, check_accuracy, check_kink_side,
+    check_uniform_acts, check_accuracy, check_kink_side, check_window_starts,
+    check_windows_sequential, check_correct_count,
 ]

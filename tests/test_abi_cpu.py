@@ -76,6 +76,10 @@ def test_null_net_calls():
     assert lib.nf_forward(None, buf, 1, buf, None) == nf.NF_EINVAL
     assert lib.nf_train_batch(None, buf, buf, 1, 1.0, 1, None) == nf.NF_EINVAL
     assert lib.nf_train_epoch(None, buf, buf, 1, 1, 1.0, 1, None) == nf.NF_EINVAL
+    assert lib.nf_train_single(None, buf, buf, 1.0, None) == nf.NF_EINVAL
+    assert lib.nf_train_windows(None, buf, buf, 4, 1, buf, 1, 1.0, 1, None) == nf.NF_EINVAL
+    cnt = ctypes.c_int64()
+    assert lib.nf_accuracy(None, buf, buf, 1, ctypes.byref(cnt), None) == nf.NF_EINVAL
 
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the behaviour without a GPU")

@@ -51,6 +51,15 @@ MUTATIONS = {
     "cost without the one half": [
         ("return 0.5 * float(np.sum(d * d))", "return float(np.sum(d * d))"),
     ],
+    "window span without the last start": [
+        ("np.float32(n - batch + 1)", "np.float32(n - batch)"),
+    ],
+    "window start rounded instead of truncated": [
+        ("return min(int(prod), n - batch)", "return min(int(np.rint(prod)), n - batch)"),
+    ],
+    "equal largest outputs resolved to the last index": [
+        ("if v[j] > v[best]:", "if v[j] >= v[best]:"),
+    ],
     "weight tendency built from z instead of the activation": [
         ("dW[l] = np.outer(delta, a[l])", "dW[l] = np.outer(delta, z[l] if l > 0 else a[l])"),
         ("(D.T @ A[l], D.sum(axis=0))", "(D.T @ (Z[l] if l > 0 else A[l]), D.sum(axis=0))"),
