@@ -80,6 +80,9 @@ struct nf_net {
   unsigned long long* dcount = nullptr;
   // every layer after the input has at most NARROW_WIDTH units
   bool narrow = false;
+  // narrow nets: offset of a zero block (NARROW_WIDTH^2 weights, then
+  // NARROW_WIDTH biases) that stands in for the layers past the last one
+  int64_t zero_off = 0;
   hipStream_t last = nullptr;
   bool used = false;
   // per-kernel timing (nf_profile)
@@ -410,16 +413,24 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
   p.d0 = n->dims[0];
   p.L = L;
   p.dims[0] = n->dims[0];
-  for (int l = 1; l <= L; ++l) {
-    const LayerLayout& ly = n->layers[l];
-    p.dims[l] = ly.out;
-    p.acts[l - 1] = ly.act;
-    p.W[l - 1] = cur_params(n) + ly.w_off;
-    p.ldw[l - 1] = ly.ldw;
-    p.bias[l - 1] = cur_params(n) + ly.b_off;
-    p.A[l - 1] = n->actv[l];
-    p.D[l - 1] = n->dbuf[l];
+  for (int l = 1; l <= nf::NARROW_MAX_LAYERS; ++l) {
+    if (l <= L) {
+      const LayerLayout& ly = n->layers[l];
+      p.dims[l] = ly.out;
+      p.acts[l - 1] = ly.act;
+      p.W[l - 1] = cur_params(n) + ly.w_off;
+      p.ldw[l - 1] = ly.ldw;
+      p.bias[l - 1] = cur_params(n) + ly.b_off;
+      p.A[l - 1] = n->actv[l];
+      p.D[l - 1] = n->dbuf[l];
+    } else {
+      // zero weights and biases for the layers past the last one
+      p.W[l - 1] = cur_params(n) + n->zero_off;
+      p.ldw[l - 1] = nf::NARROW_WIDTH;
+      p.bias[l - 1] = cur_params(n) + n->zero_off + nf::NARROW_WIDTH * nf::NARROW_WIDTH;
+    }
   }
+  p.dout = n->dims[L];
   p.out = out;
   return p;
 }
@@ -452,7 +463,8 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
   narrow_fwd_work(n, batch, true, &by, &fl);
   const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, y, batch, nullptr);
   nf_status st =
-      timed(n, "narrow_fwd_train", by, fl, s, [&] { return nf::launch_narrow_fwd(true, fp, s); });
+      timed(n, nf::narrow_fwd_name(true, (int)batch), by, fl, s,
+            [&] { return nf::launch_narrow_fwd(true, fp, s); });
   if (st != NF_OK) return st;
 
   nf::NarrowDwParams dp{};
@@ -482,7 +494,8 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
     dby += 4.0 * ((double)batch * (M + N) + 3 * M * N + 3 * M);
     dfl += 2.0 * batch * M * N;
   }
-  dp.tile_base[L] = base;
+  for (int l = L; l <= nf::NARROW_MAX_LAYERS; ++l) dp.tile_base[l] = base;
+  dp.ntiles = base;
   return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
 }
 
@@ -494,7 +507,7 @@ nf_status infer(nf_net* n, const float* x, int64_t batch, float* out, hipStream_
     double by, fl;
     narrow_fwd_work(n, batch, false, &by, &fl);
     const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
-    return timed(n, "narrow_fwd_infer", by, fl, s,
+    return timed(n, nf::narrow_fwd_name(false, (int)batch), by, fl, s,
                  [&] { return nf::launch_narrow_fwd(false, fp, s); });
   }
   return run_forward(n, x, nullptr, batch, out, false, s);
@@ -577,24 +590,31 @@ nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts
     n->device = dev;
     n->dims.assign(dims, dims + n_dims);
     n->layers.resize(n_dims);
+    n->narrow = n_dims - 1 <= nf::NARROW_MAX_LAYERS;
+    for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
+    // Narrow nets pad every layer to NARROW_WIDTH rows and the layers after
+    // the first to NARROW_WIDTH columns, so their kernels read whole padded
+    // blocks without bounds tests; the padding stays zero.
+    const int64_t NW = nf::NARROW_WIDTH;
     int64_t off = 0, canon = 0;
     for (int l = 1; l < n_dims; ++l) {
       LayerLayout& ly = n->layers[l];
       ly.in = dims[l - 1];
       ly.out = dims[l];
       ly.act = n_acts == 0 ? NF_SIGMOID : (n_acts == 1 ? acts[0] : acts[l - 1]);
-      ly.ldw = round_up(ly.in, 4);
+      ly.ldw = (n->narrow && l >= 2) ? NW : round_up(ly.in, 4);
+      const int64_t rows = n->narrow ? NW : ly.out;
       ly.w_off = off;
-      off = round_up(off + (int64_t)ly.out * ly.ldw, kAlign);
+      off = round_up(off + rows * ly.ldw, kAlign);
       ly.b_off = off;
-      off = round_up(off + ly.out, kAlign);
-      ly.lda = round_up(ly.out, 4);
+      off = round_up(off + rows, kAlign);
+      ly.lda = n->narrow ? NW : round_up(ly.out, 4);
       canon += (int64_t)ly.out * ly.in + ly.out;
     }
-    n->narrow = n_dims - 1 <= nf::NARROW_MAX_LAYERS;
-    for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
-    if (n->narrow)
-      for (int l = 1; l < n_dims; ++l) n->layers[l].lda = nf::NARROW_WIDTH;
+    if (n->narrow) {
+      n->zero_off = off;
+      off = round_up(off + NW * NW + NW, kAlign);
+    }
     n->n_params = canon;
     n->dev_floats = off;
     n->actv.assign(n_dims, nullptr);

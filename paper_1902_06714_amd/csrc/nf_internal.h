@@ -75,14 +75,22 @@ hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* p
 constexpr int NARROW_MAX_LAYERS = 4;
 constexpr int NARROW_WIDTH = 32;
 constexpr int NARROW_TILE = 16;       // samples per workgroup of the per-sample pass
+// batches up to this size take 4-sample workgroups (enough of them to fill
+// the chip); larger ones take NARROW_TILE-sample workgroups
+constexpr int NARROW_SMALL_BATCH = 2048;
 
+// Parameter layout of narrow nets: W_1 is [NARROW_WIDTH][ldw_1] and W_l, l >= 2,
+// is [NARROW_WIDTH][NARROW_WIDTH]; biases are NARROW_WIDTH long; rows, columns
+// and entries past the layer sizes are zero.  The per-sample kernel reads the
+// layers past the last one (up to NARROW_MAX_LAYERS) from a zero block.
 struct NarrowFwdParams {
   const float* X;                          // [B][d0], d0 % 4 == 0, 16-byte aligned
   const float* Y;                          // [B][d_L] targets (training)
   int B, d0, L;
+  int dout;                                // d_L
   int dims[NARROW_MAX_LAYERS + 1];
   int acts[NARROW_MAX_LAYERS];
-  const float* W[NARROW_MAX_LAYERS];       // W_l [d_l][ldw_l] (index l-1)
+  const float* W[NARROW_MAX_LAYERS];       // W_l (index l-1), padded as above
   int64_t ldw[NARROW_MAX_LAYERS];
   const float* bias[NARROW_MAX_LAYERS];
   float* A[NARROW_MAX_LAYERS];             // f(z_l) [B][32], l = 1..L-1
@@ -103,11 +111,15 @@ struct NarrowDwParams {
   float* bias[NARROW_MAX_LAYERS];
   float* G[NARROW_MAX_LAYERS];             // tendencies, same layout as W / bias
   float* gb[NARROW_MAX_LAYERS];
-  int tile_base[NARROW_MAX_LAYERS + 1];    // first (16-column, 16-unit) tile of each layer
+  int tile_base[NARROW_MAX_LAYERS + 1];    // first (16-column, 16-unit) tile of each layer;
+                                           // ntiles for the layers past the last one
+  int ntiles;                              // tiles of all layers
   float scale;
 };
 
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s);
+// Name of the per-sample kernel launch_narrow_fwd picks for this batch.
+const char* narrow_fwd_name(bool train, int batch);
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 
 // Adds to *count the number of rows s < n for which out[s][0..d) and

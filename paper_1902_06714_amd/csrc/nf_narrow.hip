@@ -1,10 +1,11 @@
 // Training step for narrow networks (every layer after the input has at most
 // 32 units, like the paper's 784-30-10 MNIST network, section 4).
 //
-// Kernel 1, per 16-sample tile (one workgroup of 8 waves):
-//   layer 1   z_1 = W_1 x + b_1 on the fp32 matrix cores (16x16x4), the input
-//             width staged through LDS in 128-wide chunks, each wave taking one
-//             16-wide group per chunk, the waves' sums added in wave order;
+// Kernel 1, per tile of 4 samples (batches up to NARROW_SMALL_BATCH) or 16
+// samples (larger batches), one workgroup of 8 waves:
+//   layer 1   z_1 = W_1 x + b_1 on the fp32 matrix cores (4x4x1 blocks fed
+//             from registers, or 16x16x4 with the input width staged through
+//             LDS), the partial sums added in a fixed order;
 //   layers 2+ one thread per (sample, unit) with the previous layer in LDS;
 //   deltas    output delta (a_L - y) f'(z_L) and hidden deltas
 //             (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3), with f'(z_l) kept
@@ -38,8 +39,152 @@ constexpr int N1_KP = N1_KC + 4;      // padded LDS row
 constexpr int N1_PRE_TRAIN = 8;
 constexpr int N1_PRE_INFER = 4;
 
+// The weights of layers 2..L and every bias, staged in LDS by every tile
+// (the per-sample threads read them again and again).  Each thread loads its
+// share into registers before layer 1 and stores it to LDS afterwards, so the
+// loads land while layer 1 runs.
+constexpr int NSTAGE = NARROW_WIDTH * NARROW_WIDTH / (N1_WAVES * 64);
+static_assert(NARROW_WIDTH * NARROW_WIDTH % (N1_WAVES * 64) == 0, "staging split");
+
+struct SmallLayers {
+  float w[NARROW_MAX_LAYERS - 1][NSTAGE];
+  float b[NARROW_MAX_LAYERS];
+};
+
+// The layer loops are unrolled so that every kernel-argument index is a
+// constant, and the loads carry no conditions: the padded layout (zeros past
+// the layer sizes, a zero block past the last layer) makes every entry of the
+// 32 x 32 blocks readable, so all the loads issue together at kernel start.
+__device__ __forceinline__ void load_small_layers(const NarrowFwdParams& p, int tid,
+                                                  SmallLayers& r) {
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < NSTAGE; ++u) r.w[li][u] = p.W[li + 1][tid + u * N1_WAVES * 64];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) r.b[l] = p.bias[l][tid & (NARROW_WIDTH - 1)];
+}
+
+__device__ __forceinline__ void store_small_layers(const SmallLayers& r, int tid,
+                                                   float (*ws)[NARROW_WIDTH][NARROW_WIDTH + 1],
+                                                   float (*bs)[NARROW_WIDTH]) {
+  constexpr int NW = NARROW_WIDTH;
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < NSTAGE; ++u) {
+      const int e = tid + u * N1_WAVES * 64;
+      ws[li][e / NW][e % NW] = r.w[li][u];
+    }
+  if (tid < NW) {
+#pragma unroll
+    for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bs[l][tid] = r.b[l];
+  }
+}
+
+// Target of thread (sample tid / 32, output unit tid % 32) of a T-sample tile.
+template <int T>
+__device__ __forceinline__ float load_target(const NarrowFwdParams& p, int s0, int tid) {
+  // read from a clamped (always valid) position without a branch, so the
+  // load issues with the others at kernel start
+  const int ys = s0 + (tid >> 5), yu = tid & 31;
+  const bool ok = tid < T * NARROW_WIDTH && ys < p.B && yu < p.dout;
+  const int yr = ys < p.B ? ys : p.B - 1, yc = yu < p.dout ? yu : p.dout - 1;
+  const float v = p.Y[(int64_t)yr * p.dout + yc];
+  return ok ? v : 0.0f;
+}
+
+// Everything after the layer-1 sums, for thread (s, j) = (tid / 32, tid % 32):
+// sample s of the T-sample tile, unit j of the current layer.  Layer 1's
+// activation, layers 2..L with the previous layer in LDS (padded units carry
+// zeros, so every sum runs over 32), the output delta (a_L - y) f'(z_L) and
+// the hidden deltas (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with
+// f'(z_l) kept in registers.  Threads past 32 T only join the barriers.
+template <bool TRAIN, int T>
+__device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, int tid, float z1,
+                                            float ytg, float (*hs)[T][NARROW_WIDTH + 1],
+                                            const float (*ws)[NARROW_WIDTH][NARROW_WIDTH + 1],
+                                            const float (*bs)[NARROW_WIDTH]) {
+  constexpr int NW = NARROW_WIDTH;
+  const bool active = tid < T * NW;
+  const int s = active ? tid >> 5 : 0, j = tid & 31;
+  const int gs = s0 + s;
+  const bool s_ok = active && gs < p.B;
+  float fp[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0f;
+  int cur = 0;
+  if (active) {
+    float a = 0.0f, f = 0.0f;
+    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bs[0][j], a, f);
+    fp[0] = f;
+    if (p.L == 1) {
+      if (TRAIN) {
+        const float d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0f;
+        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < p.dims[1]) {
+        p.out[(int64_t)gs * p.dims[1] + j] = a;
+      }
+    } else {
+      hs[0][s][j] = a;
+      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
+    }
+  }
+  __syncthreads();
+
+  // ---- layers 2..L
+#pragma unroll
+  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
+    if (l > p.L) break;
+    if (active) {
+      const int dl = p.dims[l];
+      float z = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) z = fmaf(ws[l - 2][j][i], hs[cur][s][i], z);
+      float a = 0.0f, f = 0.0f;
+      if (j < dl) act_eval(p.acts[l - 1], z + bs[l - 1][j], a, f);
+      fp[l - 1] = f;
+      if (l == p.L) {
+        if (TRAIN) {
+          const float d = (j < dl && s_ok) ? (a - ytg) * f : 0.0f;
+          hs[cur ^ 1][s][j] = d;
+          if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+        } else if (s_ok && j < dl) {
+          p.out[(int64_t)gs * dl + j] = a;
+        }
+      } else {
+        hs[cur ^ 1][s][j] = a;
+        if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
+      }
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (!TRAIN) return;
+
+  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+#pragma unroll
+  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
+    if (l >= p.L) continue;
+    if (active) {
+      float t = 0.0f;
+#pragma unroll
+      for (int k = 0; k < NW; ++k) t = fmaf(ws[l - 1][k][j], hs[cur][s][k], t);
+      const float d = j < p.dims[l] ? t * fp[l - 1] : 0.0f;
+      hs[cur ^ 1][s][j] = d;
+      if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 16-sample tiles (large batches): layer 1 on the 16x16x4 matrix cores, the
+// input width staged through LDS in 128-wide chunks.
+// ---------------------------------------------------------------------------
 template <bool TRAIN, int N1_PRE>
-__global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowFwdParams p) {
+__global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const NarrowFwdParams p) {
   constexpr int T = NARROW_TILE;
   constexpr int NW = NARROW_WIDTH;
   // layer-1 staging (input chunk xs, W_1 chunk wsl, two buffers each); the
@@ -58,41 +203,9 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
   const int wave = tid >> 6;
   const int s0 = blockIdx.x * T;
 
-  // stage the small layers' weights and every bias in LDS (read again and
-  // again by the per-sample threads below).  The layer loops are unrolled so
-  // that every kernel-argument index is a constant; the loads are issued
-  // together and land while layer 1 runs.  Out-of-range entries read W_1[0][0]
-  // (always present) and are zeroed.
-  constexpr int NPER = NW * NW / (N1_WAVES * 64);
-  static_assert(NW * NW % (N1_WAVES * 64) == 0, "staging split");
-  float wst[NARROW_MAX_LAYERS - 1][NPER];
-#pragma unroll
-  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li) {
-    const int l = li + 2;
-#pragma unroll
-    for (int u = 0; u < NPER; ++u) {
-      const int e = tid + u * N1_WAVES * 64, row = e / NW, colw = e % NW;
-      const bool ok = l <= p.L && row < p.dims[l] && colw < p.dims[l - 1];
-      const float* src = ok ? p.W[l - 1] + (int64_t)row * p.ldw[l - 1] + colw : p.W[0];
-      const float v = *src;
-      wst[li][u] = ok ? v : 0.0f;
-    }
-  }
-  float bst[NARROW_MAX_LAYERS];
-#pragma unroll
-  for (int l = 1; l <= NARROW_MAX_LAYERS; ++l) {
-    const int u = tid & (NW - 1);
-    const bool ok = l <= p.L && u < p.dims[l];
-    const float* src = ok ? p.bias[l - 1] + u : p.W[0];
-    const float v = *src;
-    bst[l - 1] = ok ? v : 0.0f;
-  }
-  // this thread's target (sample tid / 32, output unit tid % 32)
-  float ytg = 0.0f;
-  if (TRAIN) {
-    const int ys = s0 + (tid >> 5), yu = tid & 31;
-    if (ys < p.B && yu < p.dims[p.L]) ytg = p.Y[(int64_t)ys * p.dims[p.L] + yu];
-  }
+  SmallLayers sl;
+  load_small_layers(p, tid, sl);
+  const float ytg = TRAIN ? load_target<T>(p, s0, tid) : 0.0f;
 
   // ---- layer 1 on the matrix cores.  The inputs go through LDS in chunks of
   // N1_KC, read from global memory with contiguous full-line loads (X rows and
@@ -105,15 +218,14 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
   // address and stored as zero.
   {
     const int r = lane & 15, g = lane >> 4;
-    const int d1 = p.dims[1];
     const int nch = (p.d0 + N1_KC - 1) / N1_KC;
-    // this thread's share of a chunk: one float4 of X, two of W_1
+    // this thread's share of a chunk: one float4 of X, two of W_1 (whose
+    // rows are padded to 32 with zeros)
     const int xrow = tid / (N1_KC / 4), xq = tid % (N1_KC / 4);
     const bool xrow_ok = s0 + xrow < p.B;
     const float* xsrc = p.X + (int64_t)(xrow_ok ? s0 + xrow : p.B - 1) * p.d0;
-    const bool w0_ok = xrow < d1, w1_ok = 16 + xrow < d1;
-    const float* wsrc0 = p.W[0] + (int64_t)(w0_ok ? xrow : 0) * p.ldw[0];
-    const float* wsrc1 = p.W[0] + (int64_t)(w1_ok ? 16 + xrow : 0) * p.ldw[0];
+    const float* wsrc0 = p.W[0] + (int64_t)xrow * p.ldw[0];
+    const float* wsrc1 = p.W[0] + (int64_t)(16 + xrow) * p.ldw[0];
     // two accumulator chains per unit block (inputs 4g, 4g+2 and 4g+1, 4g+3
     // of each group) keep more MFMAs in flight; they are added at the end
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
@@ -131,8 +243,8 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
         const float4 w0 = *reinterpret_cast<const float4*>(wsrc0 + kc);
         const float4 w1 = *reinterpret_cast<const float4*>(wsrc1 + kc);
         xr[u] = keep_if(k_ok && xrow_ok, xv);
-        wr0[u] = keep_if(k_ok && w0_ok, w0);
-        wr1[u] = keep_if(k_ok && w1_ok, w1);
+        wr0[u] = keep_if(k_ok, w0);
+        wr1[u] = keep_if(k_ok, w1);
       }
       // chunks past the input width were loaded as zeros, so the whole block
       // is processed unconditionally (keeps the loop fully unrolled)
@@ -167,95 +279,149 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd_kernel(const NarrowF
       zp[wave][4 * g + v][16 + r] = acc1[v];
     }
   }
-#pragma unroll
-  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
-#pragma unroll
-    for (int u = 0; u < NPER; ++u) {
-      const int e = tid + u * N1_WAVES * 64;
-      ws[li][e / NW][e % NW] = wst[li][u];
-    }
-  if (tid < NW) {
-#pragma unroll
-    for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bs[l][tid] = bst[l];
-  }
+  store_small_layers(sl, tid, ws, bs);
   __syncthreads();
 
-  // ---- thread (s, j): sample s of the tile, unit j of the current layer
-  const int s = tid >> 5, j = tid & 31;
-  const int gs = s0 + s;
-  const bool s_ok = gs < p.B;
-  float fp[NARROW_MAX_LAYERS];
-#pragma unroll
-  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0f;
-  int cur = 0;
+  // z_1 of (sample tid / 32, unit tid % 32): the waves' sums in wave order
+  float z1;
   {
-    float z = zp[0][s][j];
+    const int s = tid >> 5, j = tid & 31;
+    z1 = zp[0][s][j];
 #pragma unroll
-    for (int w = 1; w < N1_WAVES; ++w) z += zp[w][s][j];
-    float a = 0.0f, f = 0.0f;
-    if (j < p.dims[1]) act_eval(p.acts[0], z + bs[0][j], a, f);
-    fp[0] = f;
-    if (p.L == 1) {
-      if (TRAIN) {
-        const float d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0f;
-        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
-      } else if (s_ok && j < p.dims[1]) {
-        p.out[(int64_t)gs * p.dims[1] + j] = a;
-      }
-    } else {
-      hs[0][s][j] = a;
-      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
-    }
+    for (int w = 1; w < N1_WAVES; ++w) z1 += zp[w][s][j];
   }
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, bs);
+}
+
+// ---------------------------------------------------------------------------
+// 4-sample tiles (training batches of up to NARROW_SMALL_BATCH samples: a
+// 1000-sample batch is 250 workgroups, one per CU, instead of 63).  Layer 1 on
+// the 4x4x1 matrix cores straight from registers: each instruction forms 16
+// independent 4x4 blocks (4 samples x 4 units), and the 16 blocks take 16
+// different inputs, so one instruction covers 4 samples x 4 units x 16 inputs.
+// Lane (b, q) = (lane / 4, lane % 4) loads one float4 of its sample row q and
+// one float4 of W_1 row 4 ug + q (for each of the 8 unit groups ug) at inputs
+// 64 t + 4 b .. 64 t + 4 b + 3 of step t; the four components feed four
+// MFMAs.  Wave w takes steps w, w + 8, ...  The (wave, block) partial sums of
+// every (sample, unit) are then added in LDS in a fixed order.
+// ---------------------------------------------------------------------------
+constexpr int N4_T = 4;                      // samples per workgroup
+constexpr int N4_KS = 64;                    // inputs per step
+constexpr int N4_UG = NARROW_WIDTH / 4;      // unit groups
+constexpr int N4_PRE = 2;                    // steps per wave requested together
+constexpr int N4_PARTS = N1_WAVES * 16;      // (wave, block) partial sums per output
+constexpr int N4_RP = 36;                    // padded row: conflict-free stores
+constexpr int N4_SS = N4_PARTS * N4_RP + 32; // sample stride (other bank half)
+static_assert(N1_WAVES * 64 == 4 * N4_T * NARROW_WIDTH, "four partial sums per output");
+
+template <bool TRAIN>
+__global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const NarrowFwdParams p) {
+  constexpr int T = N4_T;
+  constexpr int NW = NARROW_WIDTH;
+  __shared__ float red[T * N4_SS];                           // [sample][wave*16+block][unit]
+  __shared__ float psum[4][T][NW];
+  __shared__ float hs[2][T][NW + 1];
+  __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];
+  __shared__ float bs[NARROW_MAX_LAYERS][NW];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int s0 = blockIdx.x * T;
+
+  SmallLayers sl;
+  load_small_layers(p, tid, sl);
+  const float ytg = TRAIN ? load_target<T>(p, s0, tid) : 0.0f;
+
+  {
+    const int b = lane >> 2, q = lane & 3;
+    const bool xrow_ok = s0 + q < p.B;
+    const float* xsrc = p.X + (int64_t)(xrow_ok ? s0 + q : p.B - 1) * p.d0;
+    // W_1 rows are padded to 32 with zeros
+    const float* wsrc[N4_UG];
+#pragma unroll
+    for (int ug = 0; ug < N4_UG; ++ug) wsrc[ug] = p.W[0] + (int64_t)(4 * ug + q) * p.ldw[0];
+    floatx4 acc[N4_UG];
+#pragma unroll
+    for (int ug = 0; ug < N4_UG; ++ug) acc[ug] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int nsteps = (p.d0 + N4_KS - 1) / N4_KS;
+    // workgroups start at different steps (rotated by the tile index), so the
+    // workgroups that start together do not all ask for the same W_1 lines
+    const int rot = (int)(blockIdx.x % (unsigned)nsteps);
+    // the first block runs unconditionally (a wave without steps adds zeros),
+    // so its loads are not held behind a branch
+    int t0 = wave;
+    do {
+      // all loads of the block first; inputs past the width load as zeros
+      // (the width is a multiple of 4, so a float4 is wholly in or out)
+      float4 xr[N4_PRE], wr[N4_PRE][N4_UG];
+#pragma unroll
+      for (int u = 0; u < N4_PRE; ++u) {
+        int t = t0 + u * N1_WAVES;
+        if (t < nsteps) t = t + rot < nsteps ? t + rot : t + rot - nsteps;
+        const int k = t * N4_KS + 4 * b;
+        const bool ok = k < p.d0;
+        const int kc = ok ? k : 0;
+        xr[u] = keep_if(ok && xrow_ok, *reinterpret_cast<const float4*>(xsrc + kc));
+#pragma unroll
+        for (int ug = 0; ug < N4_UG; ++ug)
+          wr[u][ug] = keep_if(ok, *reinterpret_cast<const float4*>(wsrc[ug] + kc));
+      }
+#pragma unroll
+      for (int u = 0; u < N4_PRE; ++u) {
+#pragma unroll
+        for (int ug = 0; ug < N4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f32_4x4x1f32(xr[u].x, wr[u][ug].x, acc[ug], 0, 0, 0);
+#pragma unroll
+        for (int ug = 0; ug < N4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f32_4x4x1f32(xr[u].y, wr[u][ug].y, acc[ug], 0, 0, 0);
+#pragma unroll
+        for (int ug = 0; ug < N4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f32_4x4x1f32(xr[u].z, wr[u][ug].z, acc[ug], 0, 0, 0);
+#pragma unroll
+        for (int ug = 0; ug < N4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f32_4x4x1f32(xr[u].w, wr[u][ug].w, acc[ug], 0, 0, 0);
+      }
+      t0 += N1_WAVES * N4_PRE;
+    } while (t0 < nsteps);
+    // accumulator register v of lane (b, q): block b's sum for sample v, unit 4 ug + q
+#pragma unroll
+    for (int ug = 0; ug < N4_UG; ++ug)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        red[v * N4_SS + (wave * 16 + b) * N4_RP + 4 * ug + q] = acc[ug][v];
+  }
+  store_small_layers(sl, tid, ws, bs);
   __syncthreads();
 
-  // ---- layers 2..L (padded units carry zeros, so every sum runs over 32)
+  // every thread adds a quarter of the (wave, block) sums of one output, in
+  // order; the quarters are then added pairwise
+  {
+    const int part = tid >> 7, s = (tid >> 5) & 3, j = tid & 31;
+    const float* src = red + s * N4_SS + part * (N4_PARTS / 4) * N4_RP + j;
+    float t = src[0];
 #pragma unroll
-  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
-    if (l > p.L) break;
-    const int dl = p.dims[l];
-    float z = 0.0f;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) z = fmaf(ws[l - 2][j][i], hs[cur][s][i], z);
-    float a = 0.0f, f = 0.0f;
-    if (j < dl) act_eval(p.acts[l - 1], z + bs[l - 1][j], a, f);
-    fp[l - 1] = f;
-    if (l == p.L) {
-      if (TRAIN) {
-        const float d = (j < dl && s_ok) ? (a - ytg) * f : 0.0f;
-        hs[cur ^ 1][s][j] = d;
-        if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
-      } else if (s_ok && j < dl) {
-        p.out[(int64_t)gs * dl + j] = a;
-      }
-    } else {
-      hs[cur ^ 1][s][j] = a;
-      if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
-    }
-    cur ^= 1;
-    __syncthreads();
+    for (int r = 1; r < N4_PARTS / 4; ++r) t += src[r * N4_RP];
+    psum[part][s][j] = t;
   }
-  if (!TRAIN) return;
-
-  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
-#pragma unroll
-  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
-    if (l >= p.L) continue;
-    float t = 0.0f;
-#pragma unroll
-    for (int k = 0; k < NW; ++k) t = fmaf(ws[l - 1][k][j], hs[cur][s][k], t);
-    const float d = j < p.dims[l] ? t * fp[l - 1] : 0.0f;
-    hs[cur ^ 1][s][j] = d;
-    if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
-    cur ^= 1;
-    __syncthreads();
+  __syncthreads();
+  float z1 = 0.0f;
+  if (tid < T * NW) {
+    const int s = tid >> 5, j = tid & 31;
+    z1 = (psum[0][s][j] + psum[1][s][j]) + (psum[2][s][j] + psum[3][s][j]);
   }
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, bs);
 }
 
 // Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the whole
 // batch: G[16 h + u][c0 + r] = sum over samples of delta[s][16 h + u] a_prev[s][c0 + r]
 // on the 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
 // waves' sums are added in wave order, then the tile applies the SGD step.
+template <class V>
+__device__ __forceinline__ V pick(int l, V a0, V a1, V a2, V a3) {
+  return l == 0 ? a0 : (l == 1 ? a1 : (l == 2 ? a2 : a3));
+}
+
 constexpr int N2_WAVES = 8;
 constexpr int N2_UNROLL = 32;  // groups of 4 samples loaded before use
 
@@ -267,20 +433,31 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   // consecutive workgroups land on different XCDs (round robin over 8); give
   // each XCD a contiguous run of tiles so that the two unit halves of a column
   // tile, and neighbouring column tiles, share the input rows in one L2
-  const int nwg = p.tile_base[p.L];
+  const int nwg = p.ntiles;
   const int per = (nwg + 7) / 8;
   const int full = nwg - 8 * (per - 1);       // XCDs that get `per` tiles
   const int xcd = (int)blockIdx.x & 7, slot = (int)blockIdx.x >> 3;
   const int tile = xcd < full ? xcd * per + slot : full * per + (xcd - full) * (per - 1) + slot;
-  int l = 0;
-  while (l + 1 < p.L && tile >= p.tile_base[l + 1]) ++l;
-  const int M = p.dims[l + 1], N = p.dims[l];
+  // the layer of this tile (tile_base of the layers past the last is ntiles);
+  // every per-layer argument is picked by value from constant indices, so
+  // the argument loads all issue at kernel start
+  const int l = (tile >= p.tile_base[1]) + (tile >= p.tile_base[2]) + (tile >= p.tile_base[3]);
+  const int M = pick(l, p.dims[1], p.dims[2], p.dims[3], p.dims[4]);
+  const int N = pick(l, p.dims[0], p.dims[1], p.dims[2], p.dims[3]);
+  const int base = pick(l, p.tile_base[0], p.tile_base[1], p.tile_base[2], p.tile_base[3]);
   const int nh = (M + 15) / 16;
-  const int c = (tile - p.tile_base[l]) / nh, h = (tile - p.tile_base[l]) % nh;
+  const int c = (tile - base) / nh, h = (tile - base) % nh;
   const int c0 = c * 16, u0 = h * 16;
-  const float* xop = l == 0 ? p.X : p.A[l - 1];
+  const float* xop = pick(l, p.X, p.A[0], p.A[1], p.A[2]);
   const int64_t ldx = l == 0 ? p.dims[0] : NARROW_WIDTH;
-  const float* dl = p.D[l] + u0;
+  const float* dl = pick(l, p.D[0], p.D[1], p.D[2], p.D[3]) + u0;
+  const int64_t ldw = pick(l, p.ldw[0], p.ldw[1], p.ldw[2], p.ldw[3]);
+  float* G = pick(l, p.G[0], p.G[1], p.G[2], p.G[3]);
+  float* W = pick(l, p.W[0], p.W[1], p.W[2], p.W[3]);
+  const float* Win = pick(l, p.Win[0], p.Win[1], p.Win[2], p.Win[3]);
+  float* gb = pick(l, p.gb[0], p.gb[1], p.gb[2], p.gb[3]);
+  float* bias = pick(l, p.bias[0], p.bias[1], p.bias[2], p.bias[3]);
+  const float* bin = pick(l, p.bin[0], p.bin[1], p.bin[2], p.bin[3]);
 
   const int r = lane & 15, g = lane >> 4;
   const bool col_ok = c0 + r < N;
@@ -318,9 +495,9 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
 #pragma unroll
     for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][i][jj];
     if (u0 + i < M && c0 + jj < N) {
-      const int64_t o = (int64_t)(u0 + i) * p.ldw[l] + c0 + jj;
-      p.G[l][o] = gsum;
-      p.W[l][o] = fmaf(-p.scale, gsum, p.Win[l][o]);
+      const int64_t o = (int64_t)(u0 + i) * ldw + c0 + jj;
+      G[o] = gsum;
+      W[o] = fmaf(-p.scale, gsum, Win[o]);
     }
   }
   if (c == 0 && tid < 16 && u0 + tid < M) {
@@ -329,22 +506,35 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
     for (int w = 0; w < N2_WAVES; ++w)
 #pragma unroll
       for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
-    p.gb[l][u0 + tid] = gsum;
-    p.bias[l][u0 + tid] = fmaf(-p.scale, gsum, p.bin[l][u0 + tid]);
+    gb[u0 + tid] = gsum;
+    bias[u0 + tid] = fmaf(-p.scale, gsum, bin[u0 + tid]);
   }
 }
 
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s) {
-  const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
-  if (train)
-    narrow_fwd_kernel<true, N1_PRE_TRAIN><<<grid, N1_WAVES * 64, 0, s>>>(p);
-  else
-    narrow_fwd_kernel<false, N1_PRE_INFER><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  if (p.B <= NARROW_SMALL_BATCH) {
+    const dim3 grid((p.B + N4_T - 1) / N4_T);
+    if (train)
+      narrow_fwd4_kernel<true><<<grid, N1_WAVES * 64, 0, s>>>(p);
+    else
+      narrow_fwd4_kernel<false><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  } else {
+    const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
+    if (train)
+      narrow_fwd16_kernel<true, N1_PRE_TRAIN><<<grid, N1_WAVES * 64, 0, s>>>(p);
+    else
+      narrow_fwd16_kernel<false, N1_PRE_INFER><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  }
   return hipGetLastError();
 }
 
+const char* narrow_fwd_name(bool train, int batch) {
+  if (batch <= NARROW_SMALL_BATCH) return train ? "narrow_fwd4_train" : "narrow_fwd4_infer";
+  return train ? "narrow_fwd16_train" : "narrow_fwd16_infer";
+}
+
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s) {
-  narrow_dw_kernel<<<dim3(p.tile_base[p.L]), N2_WAVES * 64, 0, s>>>(p);
+  narrow_dw_kernel<<<dim3(p.ntiles), N2_WAVES * 64, 0, s>>>(p);
   return hipGetLastError();
 }
 
