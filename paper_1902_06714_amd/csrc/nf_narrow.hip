@@ -459,24 +459,33 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   float* bias = pick(l, p.bias[0], p.bias[1], p.bias[2], p.bias[3]);
   const float* bin = pick(l, p.bin[0], p.bin[1], p.bin[2], p.bin[3]);
 
+  // the parameters this thread updates at the end, requested now so that
+  // their latency hides behind the batch loop (clamped, always valid)
+  const int ui = (tid >> 4) & 15, uj = tid & 15;   // unit within the half, column within the tile
+  const bool w_mine = tid < 256 && u0 + ui < M && c0 + uj < N;
+  const int64_t wo = w_mine ? (int64_t)(u0 + ui) * ldw + c0 + uj : 0;
+  const float w_old = Win[wo];
+  const bool b_mine = c == 0 && tid < 16 && u0 + tid < M;
+  const float b_old = bin[b_mine ? u0 + tid : 0];
+
   const int r = lane & 15, g = lane >> 4;
   const bool col_ok = c0 + r < N;
   const float* xcol = xop + (col_ok ? c0 + r : 0);
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   float bsum = 0.0f;
   const int ngroups = (p.B + 3) / 4;
-  for (int gb = wave; gb < ngroups; gb += N2_WAVES * N2_UNROLL) {
+  for (int g0 = wave; g0 < ngroups; g0 += N2_WAVES * N2_UNROLL) {
     float dv[N2_UNROLL], xv[N2_UNROLL];
 #pragma unroll
     for (int u = 0; u < N2_UNROLL; ++u) {
-      const int smp = (gb + u * N2_WAVES) * 4 + g;
+      const int smp = (g0 + u * N2_WAVES) * 4 + g;
       const int sc = smp < p.B ? smp : p.B - 1;
       dv[u] = dl[(int64_t)sc * NARROW_WIDTH + r];
       xv[u] = xcol[(int64_t)sc * ldx];
     }
 #pragma unroll
     for (int u = 0; u < N2_UNROLL; ++u) {
-      const bool ok = (gb + u * N2_WAVES) * 4 + g < p.B;
+      const bool ok = (g0 + u * N2_WAVES) * 4 + g < p.B;
       const float a = ok ? dv[u] : 0.0f;
       const float b = (ok && col_ok) ? xv[u] : 0.0f;
       acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
@@ -489,25 +498,21 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   if (c == 0) bred[wave][g][r] = bsum;
   __syncthreads();
 
-  if (tid < 256) {
-    const int i = tid >> 4, jj = tid & 15;   // unit within the half, column within the tile
-    float gsum = red[0][i][jj];
+  if (w_mine) {
+    float gsum = red[0][ui][uj];
 #pragma unroll
-    for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][i][jj];
-    if (u0 + i < M && c0 + jj < N) {
-      const int64_t o = (int64_t)(u0 + i) * ldw + c0 + jj;
-      G[o] = gsum;
-      W[o] = fmaf(-p.scale, gsum, Win[o]);
-    }
+    for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][ui][uj];
+    G[wo] = gsum;
+    W[wo] = fmaf(-p.scale, gsum, w_old);
   }
-  if (c == 0 && tid < 16 && u0 + tid < M) {
+  if (b_mine) {
     float gsum = 0.0f;
 #pragma unroll
     for (int w = 0; w < N2_WAVES; ++w)
 #pragma unroll
       for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
     gb[u0 + tid] = gsum;
-    bias[u0 + tid] = fmaf(-p.scale, gsum, bin[u0 + tid]);
+    bias[u0 + tid] = fmaf(-p.scale, gsum, b_old);
   }
 }
 
