@@ -200,7 +200,7 @@ def main(argv=None) -> int:
     for k in stats:
         avg = k["total_ms"] / k["launches"]
         print(f"[kernel] {k['name']:<28} launches {k['launches']:>6}  avg {avg * 1e3:9.2f} us  "
-              f"total {k['total_ms']:9.3f} ms  {k['bytes'] / k['launches'] / 1e6:9.3f} MB/launch  "
+              f"total {k['total_ms']:9.3f} ms  {k['bytes'] / k['launches'] / 1e6:11.6f} MB/launch  "
               f"{k['flops'] / k['launches'] / 1e9:9.4f} GFLOP/launch", file=sys.stderr)
     dom = stats[0]
     avg_s = dom["total_ms"] / dom["launches"] / 1e3
