@@ -5,7 +5,11 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- * - All real data is IEEE fp32 (the paper's default real32 kind, section 3.1).
+ * - Real data is IEEE fp32, the paper's default real32 kind (section 3.1), or
+ *   IEEE fp64, its real64 kind, chosen per net at creation (nf_net_create_ex).
+ *   The entry points without a suffix take fp32 data and serve fp32 nets;
+ *   their _f64 twins take fp64 data and serve fp64 nets.  Calling one family on
+ *   a net of the other precision returns NF_EINVAL.
  * - Batches are row-major: a batch of B samples of width d is B rows of d
  *   contiguous floats, sample after sample.  This is byte-identical to the
  *   paper's column-major x(d, B) (section 3.4, batch training).
@@ -56,6 +60,13 @@ typedef enum {
   NF_TANH = 4
 } nf_act;
 
+/* Element type of a net's parameters and data (section 3.1: the real kind is
+ * chosen when the library is built, real32 by default). */
+typedef enum {
+  NF_F32 = 0,
+  NF_F64 = 1
+} nf_dtype;
+
 typedef enum {
   NF_OK = 0,
   NF_EINVAL = -1,  /* bad argument: NULL pointer, bad enum, count <= 0 ...   */
@@ -77,10 +88,20 @@ typedef enum {
 nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts,
                         int32_t n_acts, nf_net** out);
 
+/* nf_net_create with a choice of element type: dtype is an nf_dtype.  An
+ * NF_F64 net keeps its parameters, tendencies and per-sample buffers in fp64
+ * and computes in fp64 (the real64 kind of section 3.1); it is driven with
+ * the _f64 entry points below. */
+nf_status nf_net_create_ex(const int32_t* dims, int32_t n_dims, const int32_t* acts,
+                           int32_t n_acts, int32_t dtype, nf_net** out);
+
+/* The nf_dtype of a net, or -1 for NULL. */
+int32_t nf_net_dtype(const nf_net* net);
+
 /* Destroy a network; waits for its outstanding work.  NULL is a no-op. */
 nf_status nf_net_destroy(nf_net* net);
 
-/* Number of floats in the canonical parameter vector:
+/* Number of elements in the canonical parameter vector:
  * sum over l of d_l * d_{l-1} + d_l.  Returns -1 for NULL. */
 int64_t nf_param_count(const nf_net* net);
 
@@ -151,6 +172,27 @@ nf_status nf_train_windows(nf_net* net, const float* d_x, const float* d_y, int6
  * `stream`, waits for it, and writes the count to *host_correct. */
 nf_status nf_accuracy(nf_net* net, const float* d_x, const float* d_y, int64_t n,
                       int64_t* host_correct, void* stream);
+
+/* The fp64 twins of the calls above, for nets created with dtype NF_F64: the
+ * same operations, arguments and errors, with every real array (parameters,
+ * tendencies, inputs, targets, outputs, window positions) in fp64 and eta in
+ * fp64.  nf_train_windows_f64 forms pos * (n_samples - batch + 1) in fp64. */
+nf_status nf_set_params_f64(nf_net* net, const double* host_src, int64_t n);
+nf_status nf_get_params_f64(nf_net* net, double* host_dst, int64_t n);
+nf_status nf_get_grads_f64(nf_net* net, double* host_dst, int64_t n);
+nf_status nf_forward_f64(nf_net* net, const double* d_x, int64_t batch, double* d_out,
+                         void* stream);
+nf_status nf_train_batch_f64(nf_net* net, const double* d_x, const double* d_y, int64_t batch,
+                             double eta, int32_t n_shards, void* stream);
+nf_status nf_train_epoch_f64(nf_net* net, const double* d_x, const double* d_y, int64_t n_samples,
+                             int64_t batch, double eta, int32_t n_shards, void* stream);
+nf_status nf_train_single_f64(nf_net* net, const double* d_x, const double* d_y, double eta,
+                              void* stream);
+nf_status nf_train_windows_f64(nf_net* net, const double* d_x, const double* d_y,
+                               int64_t n_samples, int64_t batch, const double* host_pos,
+                               int64_t n_steps, double eta, int32_t n_shards, void* stream);
+nf_status nf_accuracy_f64(nf_net* net, const double* d_x, const double* d_y, int64_t n,
+                          int64_t* host_correct, void* stream);
 
 /* Per-kernel timing, for measuring the method's computational performance the
  * way section 5 reports it (elapsed time), one kernel at a time.  While

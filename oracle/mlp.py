@@ -308,16 +308,20 @@ def train_epoch(theta, dims, acts, X, Y, batch, eta, shards=1, precision="f32",
     return theta
 
 
-def window_start(pos: float, n: int, batch: int) -> int:
+def window_start(pos: float, n: int, batch: int, precision: str = "f32") -> int:
     """Start of the mini-batch window drawn by the example program of section
     4: the integer part of pos * (n - batch + 1), with pos uniform in [0, 1).
-    The product is taken in fp32, the paper's default real kind; a product
-    that rounds up to n - batch + 1 is kept inside the sample set."""
+    The product is taken in the real kind of the run: fp32 (the paper's
+    default) or fp64 (its real64 kind); a product that rounds up to
+    n - batch + 1 is kept inside the sample set."""
     if not 0.0 <= pos < 1.0:
         raise ValueError("pos must lie in [0, 1)")
     if batch > n:
         raise ValueError("the window is longer than the sample set")
-    prod = np.float32(pos) * np.float32(n - batch + 1)
+    if precision == "f32":
+        prod = np.float32(pos) * np.float32(n - batch + 1)
+    else:
+        prod = np.float64(pos) * np.float64(n - batch + 1)
     return min(int(prod), n - batch)
 
 
@@ -326,7 +330,7 @@ def train_windows(theta, dims, acts, X, Y, batch, pos, eta, shards=1, precision=
     ``batch`` samples that window_start places (section 4)."""
     n = np.asarray(X).shape[0]
     for p in pos:
-        s = window_start(float(p), n, batch)
+        s = window_start(float(p), n, batch, precision)
         theta, _ = train_batch(theta, dims, acts, X[s:s + batch], Y[s:s + batch], eta, shards,
                                precision)
     return theta

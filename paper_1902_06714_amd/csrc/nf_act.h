@@ -1,4 +1,6 @@
-// f(z) and f'(z) of the activation functions, shared by the device kernels.
+// f(z) and f'(z) of the activation functions, shared by the device kernels,
+// in the two precisions of the library (fp32, the paper's default real kind,
+// and fp64, its real64 kind).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -7,38 +9,47 @@ namespace nf {
 
 enum { ACT_GAUSSIAN = 0, ACT_RELU = 1, ACT_SIGMOID = 2, ACT_STEP = 3, ACT_TANH = 4 };
 
+__device__ __forceinline__ float act_exp(float x) { return expf(x); }
+__device__ __forceinline__ double act_exp(double x) { return exp(x); }
+__device__ __forceinline__ float act_tanh(float x) { return tanhf(x); }
+__device__ __forceinline__ double act_tanh(double x) { return tanh(x); }
+__device__ __forceinline__ float act_abs(float x) { return fabsf(x); }
+__device__ __forceinline__ double act_abs(double x) { return fabs(x); }
+
 // f(z) and f'(z) of the five activations (section 2; sigmoid from section 3.1).
 // The sigmoid and tanh derivatives are formed from exp(-|z|) so that they keep
 // their relative accuracy when the unit saturates.
-__device__ __forceinline__ void act_eval(int act, float z, float& f, float& fp) {
+template <class T>
+__device__ __forceinline__ void act_eval(int act, T z, T& f, T& fp) {
+  const T zero = T(0), one = T(1);
   switch (act) {
     case ACT_SIGMOID: {
-      const float e = expf(-fabsf(z));
-      const float r = 1.0f / (1.0f + e);
-      f = z >= 0.0f ? r : e * r;
+      const T e = act_exp(-act_abs(z));
+      const T r = one / (one + e);
+      f = z >= zero ? r : e * r;
       fp = e * r * r;  // sigma(z) sigma(-z)
       break;
     }
     case ACT_TANH: {
-      f = tanhf(z);
-      const float e = expf(-2.0f * fabsf(z));
-      const float r = 1.0f / (1.0f + e);
-      fp = 4.0f * e * r * r;  // 1 - tanh^2 = 4 e^{-2|z|} / (1 + e^{-2|z|})^2
+      f = act_tanh(z);
+      const T e = act_exp(T(-2) * act_abs(z));
+      const T r = one / (one + e);
+      fp = T(4) * e * r * r;  // 1 - tanh^2 = 4 e^{-2|z|} / (1 + e^{-2|z|})^2
       break;
     }
     case ACT_RELU:
-      f = z > 0.0f ? z : 0.0f;
-      fp = z > 0.0f ? 1.0f : 0.0f;
+      f = z > zero ? z : zero;
+      fp = z > zero ? one : zero;
       break;
     case ACT_GAUSSIAN: {
-      const float g = expf(-z * z);
+      const T g = act_exp(-z * z);
       f = g;
-      fp = -2.0f * z * g;
+      fp = T(-2) * z * g;
       break;
     }
     default:  // ACT_STEP
-      f = z > 0.0f ? 1.0f : 0.0f;
-      fp = 0.0f;
+      f = z > zero ? one : zero;
+      fp = zero;
       break;
   }
 }

@@ -1,5 +1,6 @@
 // Host runtime behind include/nf.h: argument validation, the device layout of
-// a network, its workspace, and the launch sequence of one training step.
+// a network, its workspace, and the launch sequence of one training step, in
+// the network's element type (fp32 or fp64).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -26,14 +27,14 @@ nf_status hip_fail(hipError_t e, const char* what) {
   return fail(NF_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-constexpr int64_t kAlign = 64;  // floats (256 bytes) between tensors
+constexpr int64_t kAlign = 64;  // elements between tensors (256 bytes in fp32)
 
 int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
 struct LayerLayout {
   int in = 0, out = 0, act = 0;
-  int64_t ldw = 0;    // row pitch of W_l (floats), multiple of 4; padding is zero
-  int64_t w_off = 0;  // offsets in floats inside the parameter / tendency buffers
+  int64_t ldw = 0;    // row pitch of W_l (elements), multiple of 4; padding is zero
+  int64_t w_off = 0;  // offsets in elements inside the parameter / tendency buffers
   int64_t b_off = 0;
   int64_t lda = 0;    // row pitch of the per-sample buffers of this layer
 };
@@ -52,33 +53,40 @@ struct DeviceGuard {
   }
 };
 
+template <class T>
+constexpr int dtype_of() {
+  return sizeof(T) == 8 ? nf::DT_F64 : nf::DT_F32;
+}
+
 }  // namespace
 
 struct nf_net {
   int device = 0;
+  int dtype = nf::DT_F32;
+  size_t esz = sizeof(float);  // bytes per element
   std::vector<int> dims;
   std::vector<LayerLayout> layers;
-  int64_t n_params = 0;       // canonical floats
-  int64_t dev_floats = 0;     // device layout floats
+  int64_t n_params = 0;       // canonical elements
+  int64_t dev_elems = 0;      // device layout elements
   // parameters, double-buffered: a step reads pbuf[cur] and writes the
   // updated parameters to pbuf[cur ^ 1], then cur flips
-  float* pbuf[2] = {nullptr, nullptr};
+  void* pbuf[2] = {nullptr, nullptr};
   int cur = 0;
-  float* grads = nullptr;     // device layout, tendencies of the last step
+  void* grads = nullptr;      // device layout, tendencies of the last step
   // workspace for up to ws_batch samples
   int64_t ws_batch = 0;
-  float* ws = nullptr;
-  std::vector<float*> actv;   // actv[l]: f(z_l) [B][lda_l], l = 1..L-1
-  std::vector<float*> fbuf;   // fbuf[l]: f'(z_l) [B][lda_l], l = 1..L-1
-  std::vector<float*> dbuf;   // dbuf[l]: delta_l [B][lda_l], l = 1..L
+  void* ws = nullptr;
+  std::vector<void*> actv;    // actv[l]: f(z_l) [B][lda_l], l = 1..L-1
+  std::vector<void*> fbuf;    // fbuf[l]: f'(z_l) [B][lda_l], l = 1..L-1
+  std::vector<void*> dbuf;    // dbuf[l]: delta_l [B][lda_l], l = 1..L
   // per-piece tendencies
-  float* partial = nullptr;
-  int64_t partial_floats = 0;
+  void* partial = nullptr;
+  int64_t partial_elems = 0;
   // accuracy: network outputs of one chunk of samples, and the correct count
-  float* evalbuf = nullptr;
-  int64_t eval_floats = 0;
+  void* evalbuf = nullptr;
+  int64_t eval_elems = 0;
   unsigned long long* dcount = nullptr;
-  // every layer after the input has at most NARROW_WIDTH units
+  // fp32 nets whose every layer after the input has at most NARROW_WIDTH units
   bool narrow = false;
   // narrow nets: offset of a zero block (NARROW_WIDTH^2 weights, then
   // NARROW_WIDTH biases) that stands in for the layers past the last one
@@ -101,8 +109,18 @@ namespace {
 int num_layers(const nf_net* n) { return (int)n->dims.size() - 1; }
 
 // parameters read by this step, and the buffer its update is written to
-float* cur_params(const nf_net* n) { return n->pbuf[n->cur]; }
-float* next_params(const nf_net* n) { return n->pbuf[n->cur ^ 1]; }
+template <class T>
+T* cur_params(const nf_net* n) {
+  return static_cast<T*>(n->pbuf[n->cur]);
+}
+template <class T>
+T* next_params(const nf_net* n) {
+  return static_cast<T*>(n->pbuf[n->cur ^ 1]);
+}
+template <class T>
+T* as(void* p) {
+  return static_cast<T*>(p);
+}
 
 nf_status sync_net(nf_net* n) {
   if (!n->used) return NF_OK;
@@ -140,13 +158,13 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
     doff[l] = total;
     total += sz;
   }
-  float* buf = nullptr;
-  hipError_t e = hipMalloc(&buf, (size_t)total * sizeof(float));
+  void* buf = nullptr;
+  hipError_t e = hipMalloc(&buf, (size_t)total * n->esz);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(NF_ENOMEM, "hipMalloc of the workspace failed: " + std::string(hipGetErrorString(e)));
   }
-  e = hipMemset(buf, 0, (size_t)total * sizeof(float));  // pitch padding must read as zero
+  e = hipMemset(buf, 0, (size_t)total * n->esz);  // pitch padding must read as zero
   if (e != hipSuccess) {
     (void)hipFree(buf);
     return hip_fail(e, "hipMemset");
@@ -154,32 +172,35 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
   free_ws(n);
   n->ws = buf;
   n->ws_batch = batch;
+  char* base = static_cast<char*>(buf);
   for (int l = 1; l <= L; ++l) {
-    n->actv[l] = aoff[l] >= 0 ? buf + aoff[l] : nullptr;
-    n->fbuf[l] = foff[l] >= 0 ? buf + foff[l] : nullptr;
-    n->dbuf[l] = buf + doff[l];
+    n->actv[l] = aoff[l] >= 0 ? base + aoff[l] * n->esz : nullptr;
+    n->fbuf[l] = foff[l] >= 0 ? base + foff[l] * n->esz : nullptr;
+    n->dbuf[l] = base + doff[l] * n->esz;
   }
   return NF_OK;
 }
 
-nf_status ensure_partial(nf_net* n, int64_t floats) {
-  if (floats <= n->partial_floats) return NF_OK;
+nf_status ensure_partial(nf_net* n, int64_t elems) {
+  if (elems <= n->partial_elems) return NF_OK;
   nf_status st = sync_net(n);
   if (st != NF_OK) return st;
-  float* buf = nullptr;
-  hipError_t e = hipMalloc(&buf, (size_t)floats * sizeof(float));
+  void* buf = nullptr;
+  hipError_t e = hipMalloc(&buf, (size_t)elems * n->esz);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(NF_ENOMEM, "hipMalloc of the piece buffer failed");
   }
   if (n->partial) (void)hipFree(n->partial);
   n->partial = buf;
-  n->partial_floats = floats;
+  n->partial_elems = elems;
   return NF_OK;
 }
 
-bool vec_ok(const float* p, int64_t ld) {
-  return ld % 4 == 0 && (reinterpret_cast<uintptr_t>(p) & 15) == 0;
+// rows of pitch ld starting at p can be read with aligned 16-byte loads
+template <class T>
+bool vec_ok(const T* p, int64_t ld) {
+  return ld % (int64_t)(16 / sizeof(T)) == 0 && (reinterpret_cast<uintptr_t>(p) & 15) == 0;
 }
 
 int pick_tile(int64_t M, int64_t N, int64_t splits) {
@@ -235,73 +256,76 @@ nf_status timed(nf_net* n, const char* name, double bytes, double flops, hipStre
 }
 
 // Algorithmic bytes of one contraction launch: each operand read once, each
-// result written once (4 bytes per float).
-double gemm_bytes(int epi, const nf::GemmParams& p, int nsplit) {
-  const double M = p.M, N = p.N, K = p.K;
+// result written once (esz bytes per element).
+double gemm_bytes(int epi, int M_, int N_, int K_, int nsplit, double esz) {
+  const double M = M_, N = N_, K = K_;
   switch (epi) {
-    case nf::EPI_FWD_STASH: return 4.0 * (M * K + N * K + N + 2 * M * N);
-    case nf::EPI_FWD_DELTA: return 4.0 * (M * K + N * K + N + 2 * M * N);
-    case nf::EPI_FWD_OUT: return 4.0 * (M * K + N * K + N + M * N);
-    case nf::EPI_BWD: return 4.0 * (M * K + K * N + 2 * M * N);
-    case nf::EPI_DW_SGD: return 4.0 * (K * M + K * N + 3 * M * N + 3 * M);
-    default: return 4.0 * (K * M + K * N + nsplit * (M * N + M));
+    case nf::EPI_FWD_STASH: return esz * (M * K + N * K + N + 2 * M * N);
+    case nf::EPI_FWD_DELTA: return esz * (M * K + N * K + N + 2 * M * N);
+    case nf::EPI_FWD_OUT: return esz * (M * K + N * K + N + M * N);
+    case nf::EPI_BWD: return esz * (M * K + K * N + 2 * M * N);
+    case nf::EPI_DW_SGD: return esz * (K * M + K * N + 3 * M * N + 3 * M);
+    default: return esz * (K * M + K * N + nsplit * (M * N + M));
   }
 }
 
+template <class T>
 nf_status launch(nf_net* n, int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
-                 const nf::GemmParams& p, hipStream_t s) {
+                 const nf::GemmParamsT<T>& p, hipStream_t s) {
   const int tile = pick_tile(p.M, p.N, nsplit);
-  return timed(n, nf::gemm_name(epi, tile), gemm_bytes(epi, p, nsplit),
+  return timed(n, nf::gemm_name(epi, tile, dtype_of<T>()),
+               gemm_bytes(epi, p.M, p.N, p.K, nsplit, (double)sizeof(T)),
                2.0 * p.M * (double)p.N * p.K, s,
-               [&] { return nf::launch_gemm(epi, tile, akc, bkc, av, bv, nsplit, p, s); });
+               [&] { return nf::launch_gemm<T>(epi, tile, akc, bkc, av, bv, nsplit, p, s); });
 }
 
 // Forward propagation of `batch` samples through every layer (section 3.2).
 // train: keep f(z_l) and f'(z_l) for back-propagation and finish with the
 // output delta; otherwise write f(z_L) to `out`.
-nf_status run_forward(nf_net* n, const float* x, const float* y, int64_t batch, float* out,
-                      bool train, hipStream_t s) {
+template <class T>
+nf_status run_forward(nf_net* n, const T* x, const T* y, int64_t batch, T* out, bool train,
+                      hipStream_t s) {
   const int L = num_layers(n);
   for (int l = 1; l <= L; ++l) {
     const LayerLayout& ly = n->layers[l];
-    nf::GemmParams p{};
-    p.A = l == 1 ? x : n->actv[l - 1];
+    nf::GemmParamsT<T> p{};
+    p.A = l == 1 ? x : as<T>(n->actv[l - 1]);
     p.lda = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
-    p.B = cur_params(n) + ly.w_off;
+    p.B = cur_params<T>(n) + ly.w_off;
     p.ldb = ly.ldw;
     p.M = (int)batch;
     p.N = ly.out;
     p.K = ly.in;
     p.nsub = 1;
-    p.bias = cur_params(n) + ly.b_off;
+    p.bias = cur_params<T>(n) + ly.b_off;
     p.act = ly.act;
     const bool av = l == 1 ? vec_ok(x, n->dims[0]) : true;
     int epi;
     if (train) {
       if (l < L) {
         epi = nf::EPI_FWD_STASH;
-        p.out0 = n->actv[l];
+        p.out0 = as<T>(n->actv[l]);
         p.ld0 = ly.lda;
-        p.out1 = n->fbuf[l];
+        p.out1 = as<T>(n->fbuf[l]);
         p.ld1 = ly.lda;
       } else {
         epi = nf::EPI_FWD_DELTA;
         p.aux = y;
         p.ldaux = ly.out;
-        p.out0 = n->dbuf[l];
+        p.out0 = as<T>(n->dbuf[l]);
         p.ld0 = ly.lda;
       }
     } else {
       epi = nf::EPI_FWD_OUT;
       if (l < L) {
-        p.out0 = n->actv[l];
+        p.out0 = as<T>(n->actv[l]);
         p.ld0 = ly.lda;
       } else {
         p.out0 = out;
         p.ld0 = ly.out;
       }
     }
-    nf_status st = launch(n, epi, true, true, av, true, 1, p, s);
+    nf_status st = launch<T>(n, epi, true, true, av, true, 1, p, s);
     if (st != NF_OK) return st;
   }
   return NF_OK;
@@ -309,34 +333,35 @@ nf_status run_forward(nf_net* n, const float* x, const float* y, int64_t batch, 
 
 // Back-propagation and the SGD step (sections 3.3-3.5).  Layer l's weights are
 // updated only after delta_{l-1}, which reads them, has been formed.
-nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float eta, int shards,
+template <class T>
+nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, int shards,
                               hipStream_t s) {
   const int L = num_layers(n);
-  const float scale = (float)((double)eta / (double)batch);
+  const T scale = (T)(eta / (double)batch);
   const int64_t shard_len = batch / shards;
   for (int l = L; l >= 1; --l) {
     const LayerLayout& ly = n->layers[l];
     if (l > 1) {
       // delta_{l-1} = (delta_l W_l) * f'(z_{l-1}), with this step's W_l
       const LayerLayout& lp = n->layers[l - 1];
-      nf::GemmParams p{};
-      p.A = n->dbuf[l];
+      nf::GemmParamsT<T> p{};
+      p.A = as<T>(n->dbuf[l]);
       p.lda = ly.lda;
-      p.B = cur_params(n) + ly.w_off;
+      p.B = cur_params<T>(n) + ly.w_off;
       p.ldb = ly.ldw;
       p.M = (int)batch;
       p.N = lp.out;
       p.K = ly.out;
       p.nsub = 1;
-      p.aux = n->fbuf[l - 1];
+      p.aux = as<T>(n->fbuf[l - 1]);
       p.ldaux = lp.lda;
-      p.out0 = n->dbuf[l - 1];
+      p.out0 = as<T>(n->dbuf[l - 1]);
       p.ld0 = lp.lda;
-      nf_status st = launch(n, nf::EPI_BWD, true, false, true, true, 1, p, s);
+      nf_status st = launch<T>(n, nf::EPI_BWD, true, false, true, true, 1, p, s);
       if (st != NF_OK) return st;
     }
     // tendencies of layer l: G = delta_l^T A_{l-1}, g = sum of delta_l rows
-    const float* aprev = l == 1 ? x : n->actv[l - 1];
+    const T* aprev = l == 1 ? x : as<T>(n->actv[l - 1]);
     const int64_t ldprev = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
     const bool bv = l == 1 ? vec_ok(x, n->dims[0]) : true;
     const int64_t M = ly.out, N = ly.in;
@@ -352,8 +377,11 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
     }
     const int64_t sub_len = (shard_len + nsub - 1) / nsub;
     const int nsplit = shards * nsub;
-    nf::GemmParams p{};
-    p.A = n->dbuf[l];
+    T* P = cur_params<T>(n);
+    T* Q = next_params<T>(n);
+    T* G = as<T>(n->grads);
+    nf::GemmParamsT<T> p{};
+    p.A = as<T>(n->dbuf[l]);
     p.lda = ly.lda;
     p.B = aprev;
     p.ldb = ldprev;
@@ -365,40 +393,43 @@ nf_status run_backward_update(nf_net* n, const float* x, int64_t batch, float et
     p.sub_len = (int)sub_len;
     p.scale = scale;
     if (nsplit == 1) {
-      p.out0 = n->grads + ly.w_off;
+      p.out0 = G + ly.w_off;
       p.ld0 = ly.ldw;
-      p.W = next_params(n) + ly.w_off;
-      p.Win = cur_params(n) + ly.w_off;
+      p.W = Q + ly.w_off;
+      p.Win = P + ly.w_off;
       p.ldw = ly.ldw;
-      p.bvec = next_params(n) + ly.b_off;
-      p.bin = cur_params(n) + ly.b_off;
-      p.gbias = n->grads + ly.b_off;
-      nf_status st = launch(n, nf::EPI_DW_SGD, false, false, true, bv, 1, p, s);
+      p.bvec = Q + ly.b_off;
+      p.bin = P + ly.b_off;
+      p.gbias = G + ly.b_off;
+      nf_status st = launch<T>(n, nf::EPI_DW_SGD, false, false, true, bv, 1, p, s);
       if (st != NF_OK) return st;
     } else {
       const int64_t pstride = round_up(M * ly.ldw, kAlign);
       nf_status st = ensure_partial(n, (int64_t)nsplit * (pstride + round_up(M, kAlign)));
       if (st != NF_OK) return st;
-      p.partial = n->partial;
+      p.partial = as<T>(n->partial);
       p.pstride = pstride;
       p.ld0 = ly.ldw;
-      p.pbias = n->partial + (int64_t)nsplit * pstride;
-      st = launch(n, nf::EPI_DW_PARTIAL, false, false, true, bv, nsplit, p, s);
+      p.pbias = p.partial + (int64_t)nsplit * pstride;
+      st = launch<T>(n, nf::EPI_DW_PARTIAL, false, false, true, bv, nsplit, p, s);
       if (st != NF_OK) return st;
       const double elems = (double)M * N + M;
-      st = timed(n, "fold_sgd", 4.0 * elems * (nsplit + 3), elems * (nsplit + 1), s, [&] {
-        return nf::launch_fold_sgd(p.partial, pstride, p.pbias, shards, nsub, (int)M, (int)N,
-                                   ly.ldw, n->grads + ly.w_off, n->grads + ly.b_off,
-                                   cur_params(n) + ly.w_off, cur_params(n) + ly.b_off,
-                                   next_params(n) + ly.w_off, next_params(n) + ly.b_off, scale,
-                                   s);
-      });
+      st = timed(n, sizeof(T) == 8 ? "fold64_sgd" : "fold_sgd",
+                 (double)sizeof(T) * elems * (nsplit + 3), elems * (nsplit + 1), s, [&] {
+                   return nf::launch_fold_sgd<T>(p.partial, pstride, p.pbias, shards, nsub, (int)M,
+                                                 (int)N, ly.ldw, G + ly.w_off, G + ly.b_off,
+                                                 P + ly.w_off, P + ly.b_off, Q + ly.w_off,
+                                                 Q + ly.b_off, scale, s);
+                 });
       if (st != NF_OK) return st;
     }
   }
   return NF_OK;
 }
 
+// ---------------------------------------------------------------------------
+// narrow fp32 networks: the two-kernel step of csrc/nf_narrow.hip
+// ---------------------------------------------------------------------------
 bool narrow_ok(const nf_net* n, const float* x, int shards) {
   return n->narrow && shards == 1 && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0]);
 }
@@ -407,6 +438,7 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
                                       int64_t batch, float* out) {
   nf::NarrowFwdParams p{};
   const int L = num_layers(n);
+  float* P = cur_params<float>(n);
   p.X = x;
   p.Y = y;
   p.B = (int)batch;
@@ -418,16 +450,16 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
       const LayerLayout& ly = n->layers[l];
       p.dims[l] = ly.out;
       p.acts[l - 1] = ly.act;
-      p.W[l - 1] = cur_params(n) + ly.w_off;
+      p.W[l - 1] = P + ly.w_off;
       p.ldw[l - 1] = ly.ldw;
-      p.bias[l - 1] = cur_params(n) + ly.b_off;
-      p.A[l - 1] = n->actv[l];
-      p.D[l - 1] = n->dbuf[l];
+      p.bias[l - 1] = P + ly.b_off;
+      p.A[l - 1] = as<float>(n->actv[l]);
+      p.D[l - 1] = as<float>(n->dbuf[l]);
     } else {
       // zero weights and biases for the layers past the last one
-      p.W[l - 1] = cur_params(n) + n->zero_off;
+      p.W[l - 1] = P + n->zero_off;
       p.ldw[l - 1] = nf::NARROW_WIDTH;
-      p.bias[l - 1] = cur_params(n) + n->zero_off + nf::NARROW_WIDTH * nf::NARROW_WIDTH;
+      p.bias[l - 1] = P + n->zero_off + nf::NARROW_WIDTH * nf::NARROW_WIDTH;
     }
   }
   p.dout = n->dims[L];
@@ -456,7 +488,7 @@ void narrow_fwd_work(const nf_net* n, int64_t B, bool train, double* bytes, doub
   *flops = fl;
 }
 
-nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
+nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t batch, double eta,
                             hipStream_t s) {
   const int L = num_layers(n);
   double by, fl;
@@ -467,26 +499,29 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
             [&] { return nf::launch_narrow_fwd(true, fp, s); });
   if (st != NF_OK) return st;
 
+  float* P = cur_params<float>(n);
+  float* Q = next_params<float>(n);
+  float* G = as<float>(n->grads);
   nf::NarrowDwParams dp{};
   dp.B = (int)batch;
   dp.L = L;
   dp.X = x;
-  dp.scale = (float)((double)eta / (double)batch);
+  dp.scale = (float)(eta / (double)batch);
   dp.dims[0] = n->dims[0];
   int base = 0;
   double dby = 0.0, dfl = 0.0;
   for (int l = 1; l <= L; ++l) {
     const LayerLayout& ly = n->layers[l];
     dp.dims[l] = ly.out;
-    dp.A[l - 1] = l < L ? n->actv[l] : nullptr;
-    dp.D[l - 1] = n->dbuf[l];
-    dp.Win[l - 1] = cur_params(n) + ly.w_off;
-    dp.bin[l - 1] = cur_params(n) + ly.b_off;
-    dp.W[l - 1] = next_params(n) + ly.w_off;
+    dp.A[l - 1] = l < L ? as<float>(n->actv[l]) : nullptr;
+    dp.D[l - 1] = as<float>(n->dbuf[l]);
+    dp.Win[l - 1] = P + ly.w_off;
+    dp.bin[l - 1] = P + ly.b_off;
+    dp.W[l - 1] = Q + ly.w_off;
     dp.ldw[l - 1] = ly.ldw;
-    dp.bias[l - 1] = next_params(n) + ly.b_off;
-    dp.G[l - 1] = n->grads + ly.w_off;
-    dp.gb[l - 1] = n->grads + ly.b_off;
+    dp.bias[l - 1] = Q + ly.b_off;
+    dp.G[l - 1] = G + ly.w_off;
+    dp.gb[l - 1] = G + ly.b_off;
     dp.tile_base[l - 1] = base;
     base += (ly.in + 15) / 16 * ((ly.out + 15) / 16);
     // deltas and previous activations read, tendencies written, parameters updated
@@ -499,33 +534,23 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
   return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
 }
 
-// f(z_L) of `batch` samples into out [batch][d_L] (inference, no stash)
-nf_status infer(nf_net* n, const float* x, int64_t batch, float* out, hipStream_t s) {
-  nf_status st = ensure_ws(n, batch);
-  if (st != NF_OK) return st;
-  if (n->narrow && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0])) {
-    double by, fl;
-    narrow_fwd_work(n, batch, false, &by, &fl);
-    const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
-    return timed(n, nf::narrow_fwd_name(false, (int)batch), by, fl, s,
-                 [&] { return nf::launch_narrow_fwd(false, fp, s); });
-  }
-  return run_forward(n, x, nullptr, batch, out, false, s);
-}
-
-nf_status check_net(const nf_net* n) {
-  if (!n) return fail(NF_EINVAL, "net is NULL");
-  return NF_OK;
-}
-
-nf_status train_step(nf_net* n, const float* x, const float* y, int64_t batch, float eta,
-                     int shards, hipStream_t s) {
+// ---------------------------------------------------------------------------
+// the step and inference in element type T
+// ---------------------------------------------------------------------------
+template <class T>
+nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double eta, int shards,
+                     hipStream_t s) {
   nf_status st;
-  if (narrow_ok(n, x, shards)) {
-    st = narrow_train_step(n, x, y, batch, eta, s);
-  } else {
-    st = run_forward(n, x, y, batch, nullptr, true, s);
-    if (st == NF_OK) st = run_backward_update(n, x, batch, eta, shards, s);
+  bool done = false;
+  if constexpr (sizeof(T) == 4) {
+    if (narrow_ok(n, x, shards)) {
+      st = narrow_train_step(n, x, y, batch, eta, s);
+      done = true;
+    }
+  }
+  if (!done) {
+    st = run_forward<T>(n, x, y, batch, nullptr, true, s);
+    if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s);
   }
   // the updated parameters are in the other buffer from here on (a failed
   // launch leaves the net in an undefined state, reported as NF_EDEVICE)
@@ -533,17 +558,50 @@ nf_status train_step(nf_net* n, const float* x, const float* y, int64_t batch, f
   return st;
 }
 
-nf_status check_train_args(const nf_net* n, const float* x, const float* y, int64_t batch,
-                           float eta, int32_t shards) {
+// f(z_L) of `batch` samples into out [batch][d_L] (inference, no stash)
+template <class T>
+nf_status infer(nf_net* n, const T* x, int64_t batch, T* out, hipStream_t s) {
+  nf_status st = ensure_ws(n, batch);
+  if (st != NF_OK) return st;
+  if constexpr (sizeof(T) == 4) {
+    if (n->narrow && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0])) {
+      double by, fl;
+      narrow_fwd_work(n, batch, false, &by, &fl);
+      const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
+      return timed(n, nf::narrow_fwd_name(false, (int)batch), by, fl, s,
+                   [&] { return nf::launch_narrow_fwd(false, fp, s); });
+    }
+  }
+  return run_forward<T>(n, x, nullptr, batch, out, false, s);
+}
+
+nf_status check_net(const nf_net* n) {
+  if (!n) return fail(NF_EINVAL, "net is NULL");
+  return NF_OK;
+}
+
+// the entry point's element type must be the net's
+template <class T>
+nf_status check_net_t(const nf_net* n) {
+  nf_status st = check_net(n);
+  if (st != NF_OK) return st;
+  if (n->dtype != dtype_of<T>())
+    return fail(NF_EINVAL, n->dtype == nf::DT_F64
+                               ? "the net holds fp64 values: use the _f64 entry points"
+                               : "the net holds fp32 values: use the entry points without _f64");
+  return NF_OK;
+}
+
+nf_status check_train_args(const void* x, const void* y, int64_t batch, double eta,
+                           int32_t shards) {
   if (!x || !y) return fail(NF_EINVAL, "x or y is NULL");
   if (batch <= 0) return fail(NF_EINVAL, "batch must be positive");
   if (batch > (int64_t)1 << 30) return fail(NF_ESHAPE, "batch is too large");
   if (shards < 1) return fail(NF_EINVAL, "n_shards must be at least 1");
   if (shards > 65535) return fail(NF_ESHAPE, "n_shards must be at most 65535");
   if (batch % shards != 0) return fail(NF_ESHAPE, "batch must split evenly into n_shards pieces");
-  if (!(eta == eta) || eta == __builtin_inff() || eta == -__builtin_inff())
+  if (!(eta == eta) || eta == __builtin_inf() || eta == -__builtin_inf())
     return fail(NF_EINVAL, "eta must be finite");
-  (void)n;
   return NF_OK;
 }
 
@@ -561,84 +619,322 @@ nf_status guarded(F&& f) {
   }
 }
 
+nf_status create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32_t n_acts,
+                 int32_t dtype, nf_net** out) {
+  if (!out) return fail(NF_EINVAL, "out is NULL");
+  if (!dims) return fail(NF_EINVAL, "dims is NULL");
+  if (dtype != NF_F32 && dtype != NF_F64) return fail(NF_EINVAL, "unknown dtype");
+  if (n_dims < 2) return fail(NF_ESHAPE, "need at least an input and an output layer");
+  if (n_dims > 1024) return fail(NF_ESHAPE, "too many layers");
+  for (int i = 0; i < n_dims; ++i)
+    if (dims[i] < 1 || dims[i] > 65536) return fail(NF_ESHAPE, "layer sizes must be in 1..65536");
+  if (n_acts != 0 && n_acts != 1 && n_acts != n_dims - 1)
+    return fail(NF_ESHAPE, "n_acts must be 0, 1 or n_dims - 1");
+  if (n_acts > 0 && !acts) return fail(NF_EINVAL, "acts is NULL");
+  for (int i = 0; i < n_acts; ++i)
+    if (acts[i] < NF_GAUSSIAN || acts[i] > NF_TANH) return fail(NF_EINVAL, "unknown activation");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return hip_fail(e, "no usable HIP device");
+  }
+  nf_net* n = new nf_net();
+  n->device = dev;
+  n->dtype = dtype == NF_F64 ? nf::DT_F64 : nf::DT_F32;
+  n->esz = dtype == NF_F64 ? sizeof(double) : sizeof(float);
+  n->dims.assign(dims, dims + n_dims);
+  n->layers.resize(n_dims);
+  n->narrow = n->dtype == nf::DT_F32 && n_dims - 1 <= nf::NARROW_MAX_LAYERS;
+  for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
+  // Narrow nets pad every layer to NARROW_WIDTH rows and the layers after
+  // the first to NARROW_WIDTH columns, so their kernels read whole padded
+  // blocks without bounds tests; the padding stays zero.
+  const int64_t NW = nf::NARROW_WIDTH;
+  int64_t off = 0, canon = 0;
+  for (int l = 1; l < n_dims; ++l) {
+    LayerLayout& ly = n->layers[l];
+    ly.in = dims[l - 1];
+    ly.out = dims[l];
+    ly.act = n_acts == 0 ? NF_SIGMOID : (n_acts == 1 ? acts[0] : acts[l - 1]);
+    ly.ldw = (n->narrow && l >= 2) ? NW : round_up(ly.in, 4);
+    const int64_t rows = n->narrow ? NW : ly.out;
+    ly.w_off = off;
+    off = round_up(off + rows * ly.ldw, kAlign);
+    ly.b_off = off;
+    off = round_up(off + rows, kAlign);
+    ly.lda = n->narrow ? NW : round_up(ly.out, 4);
+    canon += (int64_t)ly.out * ly.in + ly.out;
+  }
+  if (n->narrow) {
+    n->zero_off = off;
+    off = round_up(off + NW * NW + NW, kAlign);
+  }
+  n->n_params = canon;
+  n->dev_elems = off;
+  n->actv.assign(n_dims, nullptr);
+  n->fbuf.assign(n_dims, nullptr);
+  n->dbuf.assign(n_dims, nullptr);
+  // both parameter buffers and the tendencies start at zero, padding included
+  const size_t bytes = (size_t)off * n->esz;
+  e = hipMalloc(&n->pbuf[0], bytes);
+  if (e == hipSuccess) e = hipMalloc(&n->pbuf[1], bytes);
+  if (e == hipSuccess) e = hipMalloc(&n->grads, bytes);
+  if (e == hipSuccess) e = hipMemset(n->pbuf[0], 0, bytes);
+  if (e == hipSuccess) e = hipMemset(n->pbuf[1], 0, bytes);
+  if (e == hipSuccess) e = hipMemset(n->grads, 0, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    if (n->pbuf[0]) (void)hipFree(n->pbuf[0]);
+    if (n->pbuf[1]) (void)hipFree(n->pbuf[1]);
+    if (n->grads) (void)hipFree(n->grads);
+    delete n;
+    return fail(e == hipErrorOutOfMemory ? NF_ENOMEM : NF_EDEVICE,
+                std::string("device allocation failed: ") + hipGetErrorString(e));
+  }
+  *out = n;
+  return NF_OK;
+}
+
+// canonical host array <-> device layout (host_src to dev, or dev to host_dst)
+nf_status copy_params(nf_net* n, void* dev, const void* host_src, void* host_dst, int64_t count) {
+  if (count != n->n_params) return fail(NF_ESHAPE, "parameter count does not match the net");
+  DeviceGuard g(n->device);
+  if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+  nf_status st = sync_net(n);
+  if (st != NF_OK) return st;
+  const size_t es = n->esz;
+  char* d = static_cast<char*>(dev);
+  int64_t canon = 0;
+  for (size_t l = 1; l < n->layers.size(); ++l) {
+    const LayerLayout& ly = n->layers[l];
+    const size_t wbytes = (size_t)ly.in * es;
+    hipError_t e;
+    if (host_src) {
+      const char* h = static_cast<const char*>(host_src);
+      e = hipMemcpy2D(d + ly.w_off * es, ly.ldw * es, h + canon * es, wbytes, wbytes, ly.out,
+                      hipMemcpyHostToDevice);
+      if (e == hipSuccess)
+        e = hipMemcpy(d + ly.b_off * es, h + (canon + (int64_t)ly.out * ly.in) * es,
+                      (size_t)ly.out * es, hipMemcpyHostToDevice);
+    } else {
+      char* h = static_cast<char*>(host_dst);
+      e = hipMemcpy2D(h + canon * es, wbytes, d + ly.w_off * es, ly.ldw * es, wbytes, ly.out,
+                      hipMemcpyDeviceToHost);
+      if (e == hipSuccess)
+        e = hipMemcpy(h + (canon + (int64_t)ly.out * ly.in) * es, d + ly.b_off * es,
+                      (size_t)ly.out * es, hipMemcpyDeviceToHost);
+    }
+    if (e != hipSuccess) return hip_fail(e, "parameter copy");
+    canon += (int64_t)ly.out * ly.in + ly.out;
+  }
+  return NF_OK;
+}
+
+template <class T>
+nf_status set_params(nf_net* net, const T* host_src, int64_t n) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    if (!host_src) return fail(NF_EINVAL, "host_src is NULL");
+    return copy_params(net, net->pbuf[net->cur], host_src, nullptr, n);
+  });
+}
+
+template <class T>
+nf_status get_params(nf_net* net, T* host_dst, int64_t n, bool grads) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
+    return copy_params(net, grads ? net->grads : net->pbuf[net->cur], nullptr, host_dst, n);
+  });
+}
+
+template <class T>
+nf_status forward(nf_net* net, const T* d_x, int64_t batch, T* d_out, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    if (!d_x || !d_out) return fail(NF_EINVAL, "x or out is NULL");
+    if (batch <= 0) return fail(NF_EINVAL, "batch must be positive");
+    if (batch > (int64_t)1 << 30) return fail(NF_ESHAPE, "batch is too large");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = infer<T>(net, d_x, batch, d_out, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+template <class T>
+nf_status train_batch(nf_net* net, const T* d_x, const T* d_y, int64_t batch, double eta,
+                      int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    st = train_step<T>(net, d_x, d_y, batch, eta, n_shards, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+template <class T>
+nf_status train_epoch(nf_net* net, const T* d_x, const T* d_y, int64_t n_samples, int64_t batch,
+                      double eta, int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    if (n_samples <= 0 || n_samples % batch != 0)
+      return fail(NF_ESHAPE, "n_samples must be a positive multiple of batch");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    for (int64_t t = 0; t < n_samples / batch; ++t) {
+      st = train_step<T>(net, d_x + t * batch * d0, d_y + t * batch * dl, batch, eta, n_shards, s);
+      if (st != NF_OK) break;
+    }
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+// Windows of the sample set, placed as the example program of section 4
+// places its mini-batches: start = int(pos * (n_samples - batch + 1)) with
+// the product in the net's element type (the paper's real kind), clamped to
+// the last window.
+template <class T>
+nf_status train_windows(nf_net* net, const T* d_x, const T* d_y, int64_t n_samples, int64_t batch,
+                        const T* host_pos, int64_t n_steps, double eta, int32_t n_shards,
+                        void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    if (n_samples < batch) return fail(NF_ESHAPE, "n_samples must be at least batch");
+    if (n_steps < 0) return fail(NF_EINVAL, "n_steps must not be negative");
+    if (n_steps > 0 && !host_pos) return fail(NF_EINVAL, "host_pos is NULL");
+    // every start is checked before anything is launched
+    const int64_t last = n_samples - batch;
+    const T span = (T)(last + 1);
+    std::vector<int64_t> start((size_t)n_steps);
+    for (int64_t t = 0; t < n_steps; ++t) {
+      const T pos = host_pos[t];
+      if (!(pos >= T(0) && pos < T(1))) return fail(NF_EINVAL, "pos values must lie in [0, 1)");
+      const T prod = pos * span;
+      start[(size_t)t] = std::min((int64_t)prod, last);
+    }
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = ensure_ws(net, batch);
+    if (st != NF_OK) return st;
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    for (int64_t t = 0; t < n_steps && st == NF_OK; ++t)
+      st = train_step<T>(net, d_x + start[(size_t)t] * d0, d_y + start[(size_t)t] * dl, batch, eta,
+                         n_shards, s);
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
+template <class T>
+nf_status accuracy(nf_net* net, const T* d_x, const T* d_y, int64_t n, int64_t* host_correct,
+                   void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    if (!d_x || !d_y || !host_correct) return fail(NF_EINVAL, "x, y or host_correct is NULL");
+    if (n <= 0) return fail(NF_EINVAL, "n must be positive");
+    if (n > (int64_t)1 << 40) return fail(NF_ESHAPE, "n is too large");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t d0 = net->dims.front(), dl = net->dims.back();
+    // outputs are produced chunk by chunk into a buffer of at most 16 M elements
+    const int64_t chunk = std::max<int64_t>(
+        1, std::min<int64_t>(n, std::min<int64_t>((int64_t)1 << 14, ((int64_t)1 << 24) / dl)));
+    if (chunk * dl > net->eval_elems || !net->dcount) {
+      st = sync_net(net);
+      if (st != NF_OK) return st;
+      if (!net->dcount) {
+        hipError_t e = hipMalloc(&net->dcount, sizeof(unsigned long long));
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          net->dcount = nullptr;
+          return fail(NF_ENOMEM, "hipMalloc of the counter failed");
+        }
+      }
+      if (chunk * dl > net->eval_elems) {
+        void* buf = nullptr;
+        hipError_t e = hipMalloc(&buf, (size_t)(chunk * dl) * net->esz);
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(NF_ENOMEM, "hipMalloc of the output buffer failed");
+        }
+        if (net->evalbuf) (void)hipFree(net->evalbuf);
+        net->evalbuf = buf;
+        net->eval_elems = chunk * dl;
+      }
+    }
+    hipError_t e = hipMemsetAsync(net->dcount, 0, sizeof(unsigned long long), s);
+    net->last = s;
+    net->used = true;
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    T* outb = as<T>(net->evalbuf);
+    for (int64_t b = 0; b < n && st == NF_OK; b += chunk) {
+      const int64_t m = std::min(chunk, n - b);
+      st = infer<T>(net, d_x + b * d0, m, outb, s);
+      if (st != NF_OK) break;
+      e = nf::launch_count_correct<T>(outb, dl, d_y + b * dl, dl, m, (int)dl, net->dcount, s);
+      if (e != hipSuccess) st = hip_fail(e, "count_correct launch");
+    }
+    if (st != NF_OK) return st;
+    unsigned long long count = 0;
+    e = hipMemcpyAsync(&count, net->dcount, sizeof(count), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "reading the correct count");
+    *host_correct = (int64_t)count;
+    return NF_OK;
+  });
+}
+
 }  // namespace
 
 extern "C" {
 
 nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32_t n_acts,
                         nf_net** out) {
-  return guarded([&]() -> nf_status {
-    if (!out) return fail(NF_EINVAL, "out is NULL");
-    if (!dims) return fail(NF_EINVAL, "dims is NULL");
-    if (n_dims < 2) return fail(NF_ESHAPE, "need at least an input and an output layer");
-    if (n_dims > 1024) return fail(NF_ESHAPE, "too many layers");
-    for (int i = 0; i < n_dims; ++i)
-      if (dims[i] < 1 || dims[i] > 65536) return fail(NF_ESHAPE, "layer sizes must be in 1..65536");
-    if (n_acts != 0 && n_acts != 1 && n_acts != n_dims - 1)
-      return fail(NF_ESHAPE, "n_acts must be 0, 1 or n_dims - 1");
-    if (n_acts > 0 && !acts) return fail(NF_EINVAL, "acts is NULL");
-    for (int i = 0; i < n_acts; ++i)
-      if (acts[i] < NF_GAUSSIAN || acts[i] > NF_TANH) return fail(NF_EINVAL, "unknown activation");
+  return guarded([&]() { return create(dims, n_dims, acts, n_acts, NF_F32, out); });
+}
 
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) {
-      (void)hipGetLastError();
-      return hip_fail(e, "no usable HIP device");
-    }
-    nf_net* n = new nf_net();
-    n->device = dev;
-    n->dims.assign(dims, dims + n_dims);
-    n->layers.resize(n_dims);
-    n->narrow = n_dims - 1 <= nf::NARROW_MAX_LAYERS;
-    for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
-    // Narrow nets pad every layer to NARROW_WIDTH rows and the layers after
-    // the first to NARROW_WIDTH columns, so their kernels read whole padded
-    // blocks without bounds tests; the padding stays zero.
-    const int64_t NW = nf::NARROW_WIDTH;
-    int64_t off = 0, canon = 0;
-    for (int l = 1; l < n_dims; ++l) {
-      LayerLayout& ly = n->layers[l];
-      ly.in = dims[l - 1];
-      ly.out = dims[l];
-      ly.act = n_acts == 0 ? NF_SIGMOID : (n_acts == 1 ? acts[0] : acts[l - 1]);
-      ly.ldw = (n->narrow && l >= 2) ? NW : round_up(ly.in, 4);
-      const int64_t rows = n->narrow ? NW : ly.out;
-      ly.w_off = off;
-      off = round_up(off + rows * ly.ldw, kAlign);
-      ly.b_off = off;
-      off = round_up(off + rows, kAlign);
-      ly.lda = n->narrow ? NW : round_up(ly.out, 4);
-      canon += (int64_t)ly.out * ly.in + ly.out;
-    }
-    if (n->narrow) {
-      n->zero_off = off;
-      off = round_up(off + NW * NW + NW, kAlign);
-    }
-    n->n_params = canon;
-    n->dev_floats = off;
-    n->actv.assign(n_dims, nullptr);
-    n->fbuf.assign(n_dims, nullptr);
-    n->dbuf.assign(n_dims, nullptr);
-    // both parameter buffers and the tendencies start at zero, padding included
-    e = hipMalloc(&n->pbuf[0], (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc(&n->pbuf[1], (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc(&n->grads, (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(n->pbuf[0], 0, (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(n->pbuf[1], 0, (size_t)off * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(n->grads, 0, (size_t)off * sizeof(float));
-    if (e != hipSuccess) {
-      (void)hipGetLastError();
-      if (n->pbuf[0]) (void)hipFree(n->pbuf[0]);
-      if (n->pbuf[1]) (void)hipFree(n->pbuf[1]);
-      if (n->grads) (void)hipFree(n->grads);
-      delete n;
-      return fail(e == hipErrorOutOfMemory ? NF_ENOMEM : NF_EDEVICE,
-                  std::string("device allocation failed: ") + hipGetErrorString(e));
-    }
-    *out = n;
-    return NF_OK;
-  });
+nf_status nf_net_create_ex(const int32_t* dims, int32_t n_dims, const int32_t* acts,
+                           int32_t n_acts, int32_t dtype, nf_net** out) {
+  return guarded([&]() { return create(dims, n_dims, acts, n_acts, dtype, out); });
+}
+
+int32_t nf_net_dtype(const nf_net* net) {
+  if (!net) return -1;
+  return net->dtype == nf::DT_F64 ? NF_F64 : NF_F32;
 }
 
 nf_status nf_net_destroy(nf_net* net) {
@@ -661,222 +957,74 @@ nf_status nf_net_destroy(nf_net* net) {
 
 int64_t nf_param_count(const nf_net* net) { return net ? net->n_params : -1; }
 
-static nf_status copy_params(nf_net* n, float* dev, const float* host_src, float* host_dst,
-                             int64_t count) {
-  if (count != n->n_params) return fail(NF_ESHAPE, "parameter count does not match the net");
-  DeviceGuard g(n->device);
-  if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-  nf_status st = sync_net(n);
-  if (st != NF_OK) return st;
-  int64_t canon = 0;
-  for (size_t l = 1; l < n->layers.size(); ++l) {
-    const LayerLayout& ly = n->layers[l];
-    const size_t wbytes = (size_t)ly.in * sizeof(float);
-    hipError_t e;
-    if (host_src) {
-      e = hipMemcpy2D(dev + ly.w_off, ly.ldw * sizeof(float), host_src + canon, wbytes, wbytes,
-                      ly.out, hipMemcpyHostToDevice);
-      if (e == hipSuccess)
-        e = hipMemcpy(dev + ly.b_off, host_src + canon + (int64_t)ly.out * ly.in,
-                      (size_t)ly.out * sizeof(float), hipMemcpyHostToDevice);
-    } else {
-      e = hipMemcpy2D(host_dst + canon, wbytes, dev + ly.w_off, ly.ldw * sizeof(float), wbytes,
-                      ly.out, hipMemcpyDeviceToHost);
-      if (e == hipSuccess)
-        e = hipMemcpy(host_dst + canon + (int64_t)ly.out * ly.in, dev + ly.b_off,
-                      (size_t)ly.out * sizeof(float), hipMemcpyDeviceToHost);
-    }
-    if (e != hipSuccess) return hip_fail(e, "parameter copy");
-    canon += (int64_t)ly.out * ly.in + ly.out;
-  }
-  return NF_OK;
-}
-
 nf_status nf_set_params(nf_net* net, const float* host_src, int64_t n) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    if (!host_src) return fail(NF_EINVAL, "host_src is NULL");
-    return copy_params(net, cur_params(net), host_src, nullptr, n);
-  });
+  return set_params<float>(net, host_src, n);
 }
-
 nf_status nf_get_params(nf_net* net, float* host_dst, int64_t n) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
-    return copy_params(net, cur_params(net), nullptr, host_dst, n);
-  });
+  return get_params<float>(net, host_dst, n, false);
 }
-
 nf_status nf_get_grads(nf_net* net, float* host_dst, int64_t n) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
-    return copy_params(net, net->grads, nullptr, host_dst, n);
-  });
+  return get_params<float>(net, host_dst, n, true);
 }
-
 nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out, void* stream) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    if (!d_x || !d_out) return fail(NF_EINVAL, "x or out is NULL");
-    if (batch <= 0) return fail(NF_EINVAL, "batch must be positive");
-    if (batch > (int64_t)1 << 30) return fail(NF_ESHAPE, "batch is too large");
-    DeviceGuard g(net->device);
-    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    st = infer(net, d_x, batch, d_out, s);
-    net->last = s;
-    net->used = true;
-    return st;
-  });
+  return forward<float>(net, d_x, batch, d_out, stream);
 }
-
 nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_t batch, float eta,
                          int32_t n_shards, void* stream) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
-    if (st != NF_OK) return st;
-    DeviceGuard g(net->device);
-    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    st = ensure_ws(net, batch);
-    if (st != NF_OK) return st;
-    st = train_step(net, d_x, d_y, batch, eta, n_shards, s);
-    net->last = s;
-    net->used = true;
-    return st;
-  });
+  return train_batch<float>(net, d_x, d_y, batch, (double)eta, n_shards, stream);
 }
-
 nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
                          int64_t batch, float eta, int32_t n_shards, void* stream) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
-    if (st != NF_OK) return st;
-    if (n_samples <= 0 || n_samples % batch != 0)
-      return fail(NF_ESHAPE, "n_samples must be a positive multiple of batch");
-    DeviceGuard g(net->device);
-    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    st = ensure_ws(net, batch);
-    if (st != NF_OK) return st;
-    const int64_t d0 = net->dims.front(), dl = net->dims.back();
-    for (int64_t t = 0; t < n_samples / batch; ++t) {
-      st = train_step(net, d_x + t * batch * d0, d_y + t * batch * dl, batch, eta, n_shards, s);
-      if (st != NF_OK) break;
-    }
-    net->last = s;
-    net->used = true;
-    return st;
-  });
+  return train_epoch<float>(net, d_x, d_y, n_samples, batch, (double)eta, n_shards, stream);
 }
-
 nf_status nf_train_single(nf_net* net, const float* d_x, const float* d_y, float eta, void* stream) {
-  return nf_train_batch(net, d_x, d_y, 1, eta, 1, stream);
+  return train_batch<float>(net, d_x, d_y, 1, (double)eta, 1, stream);
 }
-
 nf_status nf_train_windows(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
                            int64_t batch, const float* host_pos, int64_t n_steps, float eta,
                            int32_t n_shards, void* stream) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    st = check_train_args(net, d_x, d_y, batch, eta, n_shards);
-    if (st != NF_OK) return st;
-    if (n_samples < batch) return fail(NF_ESHAPE, "n_samples must be at least batch");
-    if (n_steps < 0) return fail(NF_EINVAL, "n_steps must not be negative");
-    if (n_steps > 0 && !host_pos) return fail(NF_EINVAL, "host_pos is NULL");
-    // every start is checked before anything is launched
-    const int64_t last = n_samples - batch;
-    const float span = (float)(last + 1);
-    std::vector<int64_t> start((size_t)n_steps);
-    for (int64_t t = 0; t < n_steps; ++t) {
-      const float pos = host_pos[t];
-      if (!(pos >= 0.0f && pos < 1.0f)) return fail(NF_EINVAL, "pos values must lie in [0, 1)");
-      const float prod = pos * span;
-      start[(size_t)t] = std::min((int64_t)prod, last);
-    }
-    DeviceGuard g(net->device);
-    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    st = ensure_ws(net, batch);
-    if (st != NF_OK) return st;
-    const int64_t d0 = net->dims.front(), dl = net->dims.back();
-    for (int64_t t = 0; t < n_steps && st == NF_OK; ++t)
-      st = train_step(net, d_x + start[(size_t)t] * d0, d_y + start[(size_t)t] * dl, batch, eta,
-                      n_shards, s);
-    net->last = s;
-    net->used = true;
-    return st;
-  });
+  return train_windows<float>(net, d_x, d_y, n_samples, batch, host_pos, n_steps, (double)eta,
+                              n_shards, stream);
 }
-
 nf_status nf_accuracy(nf_net* net, const float* d_x, const float* d_y, int64_t n,
                       int64_t* host_correct, void* stream) {
-  return guarded([&]() -> nf_status {
-    nf_status st = check_net(net);
-    if (st != NF_OK) return st;
-    if (!d_x || !d_y || !host_correct) return fail(NF_EINVAL, "x, y or host_correct is NULL");
-    if (n <= 0) return fail(NF_EINVAL, "n must be positive");
-    if (n > (int64_t)1 << 40) return fail(NF_ESHAPE, "n is too large");
-    DeviceGuard g(net->device);
-    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const int64_t d0 = net->dims.front(), dl = net->dims.back();
-    // outputs are produced chunk by chunk into a buffer of at most 16 M floats
-    const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(n, std::min<int64_t>(
-                                                   (int64_t)1 << 14, ((int64_t)1 << 24) / dl)));
-    if (chunk * dl > net->eval_floats || !net->dcount) {
-      st = sync_net(net);
-      if (st != NF_OK) return st;
-      if (!net->dcount) {
-        hipError_t e = hipMalloc(&net->dcount, sizeof(unsigned long long));
-        if (e != hipSuccess) {
-          (void)hipGetLastError();
-          net->dcount = nullptr;
-          return fail(NF_ENOMEM, "hipMalloc of the counter failed");
-        }
-      }
-      if (chunk * dl > net->eval_floats) {
-        float* buf = nullptr;
-        hipError_t e = hipMalloc(&buf, (size_t)(chunk * dl) * sizeof(float));
-        if (e != hipSuccess) {
-          (void)hipGetLastError();
-          return fail(NF_ENOMEM, "hipMalloc of the output buffer failed");
-        }
-        if (net->evalbuf) (void)hipFree(net->evalbuf);
-        net->evalbuf = buf;
-        net->eval_floats = chunk * dl;
-      }
-    }
-    hipError_t e = hipMemsetAsync(net->dcount, 0, sizeof(unsigned long long), s);
-    net->last = s;
-    net->used = true;
-    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
-    for (int64_t b = 0; b < n && st == NF_OK; b += chunk) {
-      const int64_t m = std::min(chunk, n - b);
-      st = infer(net, d_x + b * d0, m, net->evalbuf, s);
-      if (st != NF_OK) break;
-      e = nf::launch_count_correct(net->evalbuf, dl, d_y + b * dl, dl, m, (int)dl, net->dcount, s);
-      if (e != hipSuccess) st = hip_fail(e, "count_correct launch");
-    }
-    if (st != NF_OK) return st;
-    unsigned long long count = 0;
-    e = hipMemcpyAsync(&count, net->dcount, sizeof(count), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) return hip_fail(e, "reading the correct count");
-    *host_correct = (int64_t)count;
-    return NF_OK;
-  });
+  return accuracy<float>(net, d_x, d_y, n, host_correct, stream);
+}
+
+nf_status nf_set_params_f64(nf_net* net, const double* host_src, int64_t n) {
+  return set_params<double>(net, host_src, n);
+}
+nf_status nf_get_params_f64(nf_net* net, double* host_dst, int64_t n) {
+  return get_params<double>(net, host_dst, n, false);
+}
+nf_status nf_get_grads_f64(nf_net* net, double* host_dst, int64_t n) {
+  return get_params<double>(net, host_dst, n, true);
+}
+nf_status nf_forward_f64(nf_net* net, const double* d_x, int64_t batch, double* d_out,
+                         void* stream) {
+  return forward<double>(net, d_x, batch, d_out, stream);
+}
+nf_status nf_train_batch_f64(nf_net* net, const double* d_x, const double* d_y, int64_t batch,
+                             double eta, int32_t n_shards, void* stream) {
+  return train_batch<double>(net, d_x, d_y, batch, eta, n_shards, stream);
+}
+nf_status nf_train_epoch_f64(nf_net* net, const double* d_x, const double* d_y, int64_t n_samples,
+                             int64_t batch, double eta, int32_t n_shards, void* stream) {
+  return train_epoch<double>(net, d_x, d_y, n_samples, batch, eta, n_shards, stream);
+}
+nf_status nf_train_single_f64(nf_net* net, const double* d_x, const double* d_y, double eta,
+                              void* stream) {
+  return train_batch<double>(net, d_x, d_y, 1, eta, 1, stream);
+}
+nf_status nf_train_windows_f64(nf_net* net, const double* d_x, const double* d_y,
+                               int64_t n_samples, int64_t batch, const double* host_pos,
+                               int64_t n_steps, double eta, int32_t n_shards, void* stream) {
+  return train_windows<double>(net, d_x, d_y, n_samples, batch, host_pos, n_steps, eta, n_shards,
+                               stream);
+}
+nf_status nf_accuracy_f64(nf_net* net, const double* d_x, const double* d_y, int64_t n,
+                          int64_t* host_correct, void* stream) {
+  return accuracy<double>(net, d_x, d_y, n, host_correct, stream);
 }
 
 nf_status nf_profile(nf_net* net, int32_t repeats) {

@@ -6,7 +6,7 @@
 
 namespace nf {
 
-// Epilogue of the tiled fp32 MFMA contraction C = A(m,k) * B(k,n).
+// Epilogue of the tiled MFMA contraction C = A(m,k) * B(k,n).
 enum Epilogue : int {
   EPI_FWD_STASH = 0,  // z = C + b[n]; out0 = f(z) (activation), out1 = f'(z)
   EPI_FWD_DELTA = 1,  // z = C + b[n]; out0 = (f(z) - y) * f'(z)  (output delta)
@@ -16,11 +16,16 @@ enum Epilogue : int {
   EPI_DW_PARTIAL = 5  // partial[split] = C; bias partial sums
 };
 
-// One launch of the contraction.  Operand A is read as A(m,k) and operand B
-// as B(k,n); `a_kcontig` / `b_kcontig` say whether k is the contiguous index.
-struct GemmParams {
-  const float* A;
-  const float* B;
+// Element types of a network's parameters and per-sample buffers.
+enum Dtype : int { DT_F32 = 0, DT_F64 = 1 };
+
+// One launch of the contraction, in element type T (float or double).
+// Operand A is read as A(m,k) and operand B as B(k,n); `a_kcontig` /
+// `b_kcontig` say whether k is the contiguous index.
+template <class T>
+struct GemmParamsT {
+  const T* A;
+  const T* B;
   int64_t lda, ldb;
   int M, N, K;
   // split of the k range into pieces: piece z = shard * nsub + sub covers
@@ -28,42 +33,46 @@ struct GemmParams {
   int nsub;
   int shard_len, sub_len;
   // epilogue operands
-  const float* bias;   // [N]
-  const float* aux;    // y (EPI_FWD_DELTA) or f'(z) (EPI_BWD), [M][ldaux]
+  const T* bias;       // [N]
+  const T* aux;        // y (EPI_FWD_DELTA) or f'(z) (EPI_BWD), [M][ldaux]
   int64_t ldaux;
-  float* out0;         // [M][ld0]
+  T* out0;             // [M][ld0]
   int64_t ld0;
-  float* out1;         // [M][ld1]
+  T* out1;             // [M][ld1]
   int64_t ld1;
-  float* W;            // EPI_DW_SGD: updated weights [M][ldw] (W = Win - scale * G)
-  const float* Win;    // EPI_DW_SGD: weights before the step, same layout
+  T* W;                // EPI_DW_SGD: updated weights [M][ldw] (W = Win - scale * G)
+  const T* Win;        // EPI_DW_SGD: weights before the step, same layout
   int64_t ldw;
-  float* bvec;         // EPI_DW_SGD: updated biases [M]
-  const float* bin;    // EPI_DW_SGD: biases before the step
-  float* gbias;        // EPI_DW_SGD: bias tendency [M]
-  float* partial;      // EPI_DW_PARTIAL: [nsplit][M][ld0]
+  T* bvec;             // EPI_DW_SGD: updated biases [M]
+  const T* bin;        // EPI_DW_SGD: biases before the step
+  T* gbias;            // EPI_DW_SGD: bias tendency [M]
+  T* partial;          // EPI_DW_PARTIAL: [nsplit][M][ld0]
   int64_t pstride;
-  float* pbias;        // EPI_DW_PARTIAL: [nsplit][M]
-  float scale;         // eta / batch
+  T* pbias;            // EPI_DW_PARTIAL: [nsplit][M]
+  T scale;             // eta / batch
   int act;
 };
+using GemmParams = GemmParamsT<float>;
 
 // Tile shapes available to the host side.
 enum TileShape : int { TILE_128x128 = 0, TILE_64x64 = 1 };
 
-hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec,
-                       bool b_vec, int nsplit, const GemmParams& p, hipStream_t s);
+// Row pitches and base addresses that allow 16-byte vector loads must be
+// multiples of 16 / sizeof(T) elements and 16-byte aligned.
+template <class T>
+hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec, bool b_vec,
+                       int nsplit, const GemmParamsT<T>& p, hipStream_t s);
 
 // Name of the kernel instance launch_gemm picks for these arguments.
-const char* gemm_name(int epi, int tile);
+const char* gemm_name(int epi, int tile, int dtype);
 
 // Fold the per-piece tendencies of one layer in piece order, store the sum as
 // the tendency, and write the SGD step W = Win - scale * G, b = bin - scale * g
 // (W [M][ldw], b [M]).
-hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* pbias,
-                           int nshards, int nsub, int M, int N, int64_t ldw, float* G,
-                           float* gbias, const float* Win, const float* bin, float* W, float* b,
-                           float scale, hipStream_t s);
+template <class T>
+hipError_t launch_fold_sgd(const T* partial, int64_t pstride, const T* pbias, int nshards,
+                           int nsub, int M, int N, int64_t ldw, T* G, T* gbias, const T* Win,
+                           const T* bin, T* W, T* b, T scale, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Narrow networks: every layer after the input has at most NARROW_WIDTH units
@@ -124,8 +133,9 @@ hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 
 // Adds to *count the number of rows s < n for which out[s][0..d) and
 // y[s][0..d) have their first largest entry at the same index (rows holding a
-// NaN never count).  Row pitches ldo and ldy in floats.
-hipError_t launch_count_correct(const float* out, int64_t ldo, const float* y, int64_t ldy,
-                                int64_t n, int d, unsigned long long* count, hipStream_t s);
+// NaN never count).  Row pitches ldo and ldy in elements.
+template <class T>
+hipError_t launch_count_correct(const T* out, int64_t ldo, const T* y, int64_t ldy, int64_t n,
+                                int d, unsigned long long* count, hipStream_t s);
 
 }  // namespace nf

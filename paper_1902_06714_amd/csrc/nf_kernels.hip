@@ -1,8 +1,9 @@
-// fp32 kernels for mini-batch MLP training on gfx950 (CDNA4).
+// Kernels for mini-batch MLP training on gfx950 (CDNA4), in fp32 (the
+// paper's default real kind) and fp64 (its real64 kind).
 //
-// Every layer step of the method is one tiled contraction on the fp32 matrix
-// cores (v_mfma_f32_32x32x2_f32) with the rest of the step fused into its
-// epilogue:
+// Every layer step of the method is one tiled contraction on the matrix cores
+// (v_mfma_f32_32x32x2_f32, or v_mfma_f64_16x16x4_f64) with the rest of the
+// step fused into its epilogue:
 //   forward     Z = A_{l-1} W_l^T, + b_l, activation and its derivative
 //               (section 3.2, Eq. 2; f' is kept for back-propagation)
 //   output      delta_L = (f(z_L) - y) f'(z_L)   (section 3.3)
@@ -14,48 +15,94 @@
 //               buffer, so every kernel leaves its inputs untouched
 // Reductions run in a fixed order (each accumulator walks k upwards; pieces
 // of a split batch are added in piece order), so results are bitwise
-// reproducible from run to run.  No float atomics are used.
+// reproducible from run to run.  No floating-point atomics are used.
 #include "nf_act.h"
 #include "nf_internal.h"
 
 namespace nf {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
+// The matrix-core instruction of each element type, as the contraction uses
+// it: a BLK x BLK block of C per instruction, KS values of k per instruction.
+// Lane l supplies A(a_row(l), k0 + k_of(l)) and B(k0 + k_of(l), a_row(l)), and
+// accumulator register v of lane l holds C(row(v, l), col(l)) of the block.
+template <class T>
+struct Mma;
+
+template <>
+struct Mma<float> {
+  static constexpr int BLK = 32, KS = 2, NACC = 16;
+  typedef floatx16 acc_t;
+  __device__ static __forceinline__ acc_t mma(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ int a_row(int l) { return l & 31; }
+  __device__ static __forceinline__ int k_of(int l) { return l >> 5; }
+  __device__ static __forceinline__ int row(int v, int l) { return 8 * (v >> 2) + 4 * (l >> 5) + (v & 3); }
+  __device__ static __forceinline__ int col(int l) { return l & 31; }
+};
+
+template <>
+struct Mma<double> {
+  static constexpr int BLK = 16, KS = 4, NACC = 4;
+  typedef doublex4 acc_t;
+  __device__ static __forceinline__ acc_t mma(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ int a_row(int l) { return l & 15; }
+  __device__ static __forceinline__ int k_of(int l) { return l >> 4; }
+  __device__ static __forceinline__ int row(int v, int l) { return 4 * v + (l >> 4); }
+  __device__ static __forceinline__ int col(int l) { return l & 15; }
+};
+
+__device__ __forceinline__ float fma_t(float a, float b, float c) { return fmaf(a, b, c); }
+__device__ __forceinline__ double fma_t(double a, double b, double c) { return fma(a, b, c); }
+
+// 16 bytes of elements, the unit of a vector load
+template <class T>
+struct alignas(16) Vec16 {
+  static constexpr int N = 16 / sizeof(T);
+  T e[N];
+};
 
 // Global -> register -> LDS staging of one R x BK operand tile X(r, k),
 // r in [r0, r0 + R), k in [k0, k0 + BK).  In LDS the tile is k-major,
 // lds[k * (R + 4) + r], which is the order the MFMA operand reads want.
 // KC: k is the contiguous index in memory (X[r*ld + k]), else X[k*ld + r].
-// VEC: rows are 16-byte aligned with a pitch that is a multiple of 4 and the
-// pitch padding is zero, so aligned float4 loads are safe.
-template <int R, int BK, int NT, bool KC, bool VEC>
+// VEC: rows are 16-byte aligned with a pitch that is a multiple of VW and the
+// pitch padding is zero, so aligned 16-byte loads are safe.
+template <class T, int R, int BK, int NT, bool KC, bool VEC>
 struct TileLoader {
+  static constexpr int VW = Vec16<T>::N;
   static constexpr int SR = R + 4;
-  static constexpr int NV = VEC ? (R * BK / 4) / NT : (R * BK) / NT;
-  static_assert(VEC ? (R * BK / 4) % NT == 0 : (R * BK) % NT == 0, "tile not divisible");
-  float4 v[VEC ? NV : 1];
-  float s[VEC ? 1 : NV];
+  static constexpr int NV = VEC ? (R * BK / VW) / NT : (R * BK) / NT;
+  static_assert(VEC ? (R * BK / VW) % NT == 0 : (R * BK) % NT == 0, "tile not divisible");
+  Vec16<T> v[VEC ? NV : 1];
+  T s[VEC ? 1 : NV];
 
-  __device__ __forceinline__ void load(const float* __restrict__ X, int64_t ld, int rmax,
-                                       int kend, int r0, int k0, int tid) {
+  __device__ __forceinline__ void load(const T* __restrict__ X, int64_t ld, int rmax, int kend,
+                                       int r0, int k0, int tid) {
     if constexpr (VEC) {
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         const int q = tid + i * NT;
         int r, k;
         if constexpr (KC) {
-          r = q / (BK / 4);
-          k = (q % (BK / 4)) * 4;
+          r = q / (BK / VW);
+          k = (q % (BK / VW)) * VW;
         } else {
-          k = q / (R / 4);
-          r = (q % (R / 4)) * 4;
+          k = q / (R / VW);
+          r = (q % (R / VW)) * VW;
         }
         const int gr = r0 + r, gk = k0 + k;
         if (gr < rmax && gk < kend) {
-          const float* ptr = KC ? X + (int64_t)gr * ld + gk : X + (int64_t)gk * ld + gr;
-          v[i] = *reinterpret_cast<const float4*>(ptr);
+          const T* ptr = KC ? X + (int64_t)gr * ld + gk : X + (int64_t)gk * ld + gr;
+          v[i] = *reinterpret_cast<const Vec16<T>*>(ptr);
         } else {
-          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int c = 0; c < VW; ++c) v[i].e[c] = T(0);
         }
       }
     } else {
@@ -72,25 +119,23 @@ struct TileLoader {
         }
         const int gr = r0 + r, gk = k0 + k;
         s[i] = (gr < rmax && gk < kend) ? (KC ? X[(int64_t)gr * ld + gk] : X[(int64_t)gk * ld + gr])
-                                        : 0.0f;
+                                        : T(0);
       }
     }
   }
 
-  __device__ __forceinline__ void store(float* lds, int tid) const {
+  __device__ __forceinline__ void store(T* lds, int tid) const {
     if constexpr (VEC) {
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         const int q = tid + i * NT;
         if constexpr (KC) {
-          const int r = q / (BK / 4), k = (q % (BK / 4)) * 4;
-          lds[(k + 0) * SR + r] = v[i].x;
-          lds[(k + 1) * SR + r] = v[i].y;
-          lds[(k + 2) * SR + r] = v[i].z;
-          lds[(k + 3) * SR + r] = v[i].w;
+          const int r = q / (BK / VW), k = (q % (BK / VW)) * VW;
+#pragma unroll
+          for (int c = 0; c < VW; ++c) lds[(k + c) * SR + r] = v[i].e[c];
         } else {
-          const int k = q / (R / 4), r = (q % (R / 4)) * 4;
-          *reinterpret_cast<float4*>(lds + k * SR + r) = v[i];
+          const int k = q / (R / VW), r = (q % (R / VW)) * VW;
+          *reinterpret_cast<Vec16<T>*>(lds + k * SR + r) = v[i];
         }
       }
     } else {
@@ -112,16 +157,18 @@ struct TileLoader {
 };
 
 // C[BM x BN] tile per workgroup; (BM/WM) x (BN/WN) waves, each owning a
-// WM x WN sub-tile made of 32 x 32 MFMA blocks.  grid = (M tiles, N tiles,
-// pieces of the k range).
-template <int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV, int EPI>
+// WM x WN sub-tile made of BLK x BLK matrix-core blocks.  grid = (M tiles,
+// N tiles, pieces of the k range).
+template <class T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV,
+          int EPI>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
-gemm_kernel(const GemmParams p) {
+gemm_kernel(const GemmParamsT<T> p) {
+  using MM = Mma<T>;
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
-  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int TM = WM / MM::BLK, TN = WN / MM::BLK;
   constexpr int SA = BM + 4, SB = BN + 4;
-  __shared__ __attribute__((aligned(16))) float As[2][BK * SA];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BK * SB];
+  __shared__ __attribute__((aligned(16))) T As[2][BK * SA];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BK * SB];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -142,17 +189,17 @@ gemm_kernel(const GemmParams p) {
   }
   const bool do_bias = (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) && blockIdx.y == 0;
 
-  TileLoader<BM, BK, NT, AKC, AV> la;
-  TileLoader<BN, BK, NT, BKC, BV> lb;
+  TileLoader<T, BM, BK, NT, AKC, AV> la;
+  TileLoader<T, BN, BK, NT, BKC, BV> lb;
 
-  floatx16 acc[TM][TN];
+  typename MM::acc_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-  float bsum = 0.0f;
+      for (int v = 0; v < MM::NACC; ++v) acc[i][j][v] = T(0);
+  T bsum = T(0);
 
   const int ntiles = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   if (ntiles > 0) {
@@ -171,21 +218,20 @@ gemm_kernel(const GemmParams p) {
       la.load(p.A, p.lda, p.M, kend, m0, kn, tid);
       lb.load(p.B, p.ldb, p.N, kend, n0, kn, tid);
     }
-    const float* a_s = As[buf];
-    const float* b_s = Bs[buf];
+    const T* a_s = As[buf];
+    const T* b_s = Bs[buf];
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 2) {
-      float av[TM], bv[TN];
-      const int krow = kk + (lane >> 5);
+    for (int kk = 0; kk < BK; kk += MM::KS) {
+      T av[TM], bv[TN];
+      const int krow = kk + MM::k_of(lane);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) av[i] = a_s[krow * SA + wm + i * 32 + (lane & 31)];
+      for (int i = 0; i < TM; ++i) av[i] = a_s[krow * SA + wm + i * MM::BLK + MM::a_row(lane)];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bv[j] = b_s[krow * SB + wn + j * 32 + (lane & 31)];
+      for (int j = 0; j < TN; ++j) bv[j] = b_s[krow * SB + wn + j * MM::BLK + MM::a_row(lane)];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(av[i], bv[j], acc[i][j]);
     }
     if (do_bias && tid < BM) {
       // column sums of delta (the bias tendency), k in increasing order
@@ -199,32 +245,32 @@ gemm_kernel(const GemmParams p) {
     __syncthreads();
   }
 
-  // Epilogue.  Accumulator register v of lane l in a 32x32 block holds row
-  // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of the block.
+  // Epilogue: accumulator register v of this lane holds row MM::row(v, lane)
+  // and column MM::col(lane) of its block.
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn + j * 32 + (lane & 31);
+      const int n = n0 + wn + j * MM::BLK + MM::col(lane);
       if (n >= p.N) continue;
-      float bn = 0.0f;
+      T bn = T(0);
       if constexpr (EPI == EPI_FWD_STASH || EPI == EPI_FWD_DELTA || EPI == EPI_FWD_OUT) bn = p.bias[n];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      for (int v = 0; v < MM::NACC; ++v) {
+        const int m = m0 + wm + i * MM::BLK + MM::row(v, lane);
         if (m >= p.M) continue;
-        const float c = acc[i][j][v];
+        const T c = acc[i][j][v];
         if constexpr (EPI == EPI_FWD_STASH) {
-          float f, fp;
+          T f, fp;
           act_eval(p.act, c + bn, f, fp);
           p.out0[(int64_t)m * p.ld0 + n] = f;
           p.out1[(int64_t)m * p.ld1 + n] = fp;
         } else if constexpr (EPI == EPI_FWD_DELTA) {
-          float f, fp;
+          T f, fp;
           act_eval(p.act, c + bn, f, fp);
           p.out0[(int64_t)m * p.ld0 + n] = (f - p.aux[(int64_t)m * p.ldaux + n]) * fp;
         } else if constexpr (EPI == EPI_FWD_OUT) {
-          float f, fp;
+          T f, fp;
           act_eval(p.act, c + bn, f, fp);
           p.out0[(int64_t)m * p.ld0 + n] = f;
         } else if constexpr (EPI == EPI_BWD) {
@@ -232,7 +278,7 @@ gemm_kernel(const GemmParams p) {
         } else if constexpr (EPI == EPI_DW_SGD) {
           const int64_t o = (int64_t)m * p.ldw + n;
           p.out0[o] = c;
-          p.W[o] = fmaf(-p.scale, c, p.Win[o]);
+          p.W[o] = fma_t(-p.scale, c, p.Win[o]);
         } else {  // EPI_DW_PARTIAL
           p.partial[(int64_t)blockIdx.z * p.pstride + (int64_t)m * p.ld0 + n] = c;
         }
@@ -244,7 +290,7 @@ gemm_kernel(const GemmParams p) {
     if (m < p.M) {
       if constexpr (EPI == EPI_DW_SGD) {
         p.gbias[m] = bsum;
-        p.bvec[m] = fmaf(-p.scale, bsum, p.bin[m]);
+        p.bvec[m] = fma_t(-p.scale, bsum, p.bin[m]);
       } else if constexpr (EPI == EPI_DW_PARTIAL) {
         p.pbias[(int64_t)blockIdx.z * p.M + m] = bsum;
       }
@@ -254,52 +300,53 @@ gemm_kernel(const GemmParams p) {
 
 // Sum of the per-piece tendencies in piece order, then the SGD step (from the
 // parameters before the step into the other parameter buffer).
-__global__ void fold_sgd_kernel(const float* __restrict__ partial, int64_t pstride,
-                                const float* __restrict__ pbias, int nshards, int nsub, int M,
-                                int N, int64_t ldw, float* __restrict__ G,
-                                float* __restrict__ gbias, const float* __restrict__ Win,
-                                const float* __restrict__ bin, float* __restrict__ W,
-                                float* __restrict__ b, float scale) {
+template <class T>
+__global__ void fold_sgd_kernel(const T* __restrict__ partial, int64_t pstride,
+                                const T* __restrict__ pbias, int nshards, int nsub, int M, int N,
+                                int64_t ldw, T* __restrict__ G, T* __restrict__ gbias,
+                                const T* __restrict__ Win, const T* __restrict__ bin,
+                                T* __restrict__ W, T* __restrict__ b, T scale) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nw = (int64_t)M * N;
   if (idx < nw) {
     const int m = (int)(idx / N), n = (int)(idx % N);
     const int64_t o = (int64_t)m * ldw + n;
-    float tot = 0.0f;
+    T tot = T(0);
     for (int s = 0; s < nshards; ++s) {
-      float piece = partial[(int64_t)(s * nsub) * pstride + o];
+      T piece = partial[(int64_t)(s * nsub) * pstride + o];
       for (int q = 1; q < nsub; ++q) piece += partial[(int64_t)(s * nsub + q) * pstride + o];
       tot = s == 0 ? piece : tot + piece;
     }
     G[o] = tot;
-    W[o] = fmaf(-scale, tot, Win[o]);
+    W[o] = fma_t(-scale, tot, Win[o]);
   } else if (idx < nw + M) {
     const int m = (int)(idx - nw);
-    float tot = 0.0f;
+    T tot = T(0);
     for (int s = 0; s < nshards; ++s) {
-      float piece = pbias[(int64_t)(s * nsub) * M + m];
+      T piece = pbias[(int64_t)(s * nsub) * M + m];
       for (int q = 1; q < nsub; ++q) piece += pbias[(int64_t)(s * nsub + q) * M + m];
       tot = s == 0 ? piece : tot + piece;
     }
     gbias[m] = tot;
-    b[m] = fmaf(-scale, tot, bin[m]);
+    b[m] = fma_t(-scale, tot, bin[m]);
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV, int EPI>
-static hipError_t launch_one(int nsplit, const GemmParams& p, hipStream_t s) {
+template <class T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV,
+          int EPI>
+static hipError_t launch_one(int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, nsplit);
-  gemm_kernel<BM, BN, BK, WM, WN, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
+  gemm_kernel<T, BM, BN, BK, WM, WN, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
+template <class T, int BM, int BN, int BK, int WM, int WN>
 static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
-                                const GemmParams& p, hipStream_t s) {
+                                const GemmParamsT<T>& p, hipStream_t s) {
 #define NF_CASE(AKC, BKC, AV, BV, E)                                     \
   if (akc == AKC && bkc == BKC && av == AV && bv == BV && epi == E)      \
-    return launch_one<BM, BN, BK, WM, WN, AKC, BKC, AV, BV, E>(nsplit, p, s);
+    return launch_one<T, BM, BN, BK, WM, WN, AKC, BKC, AV, BV, E>(nsplit, p, s);
   // forward: A = activations [m][k], B(k, n) = W[n][k]
   NF_CASE(true, true, true, true, EPI_FWD_STASH)
   NF_CASE(true, true, false, true, EPI_FWD_STASH)
@@ -318,35 +365,56 @@ static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, i
   return hipErrorInvalidValue;
 }
 
+template <class T>
 hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec, bool b_vec,
-                       int nsplit, const GemmParams& p, hipStream_t s) {
+                       int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
+  // fp64 accumulators take twice the registers: its 128 x 128 tile uses 8
+  // waves of 64 x 32 instead of 4 of 64 x 64
+  constexpr int WN128 = sizeof(T) == 8 ? 32 : 64;
   if (tile == TILE_128x128)
-    return dispatch_tile<128, 128, 16, 64, 64>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
-  return dispatch_tile<64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
+    return dispatch_tile<T, 128, 128, 16, 64, WN128>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
+                                                     nsplit, p, s);
+  return dispatch_tile<T, 64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
 }
 
-const char* gemm_name(int epi, int tile) {
-  static const char* names[2][6] = {
-      {"gemm_fwd_stash_128x128", "gemm_fwd_delta_128x128", "gemm_fwd_out_128x128",
-       "gemm_bwd_128x128", "gemm_dw_sgd_128x128", "gemm_dw_partial_128x128"},
-      {"gemm_fwd_stash_64x64", "gemm_fwd_delta_64x64", "gemm_fwd_out_64x64", "gemm_bwd_64x64",
-       "gemm_dw_sgd_64x64", "gemm_dw_partial_64x64"}};
-  if (epi < 0 || epi > 5 || tile < 0 || tile > 1) return "gemm";
-  return names[tile][epi];
+template hipError_t launch_gemm<float>(int, int, bool, bool, bool, bool, int,
+                                       const GemmParamsT<float>&, hipStream_t);
+template hipError_t launch_gemm<double>(int, int, bool, bool, bool, bool, int,
+                                        const GemmParamsT<double>&, hipStream_t);
+
+const char* gemm_name(int epi, int tile, int dtype) {
+  static const char* names[2][2][6] = {
+      {{"gemm_fwd_stash_128x128", "gemm_fwd_delta_128x128", "gemm_fwd_out_128x128",
+        "gemm_bwd_128x128", "gemm_dw_sgd_128x128", "gemm_dw_partial_128x128"},
+       {"gemm_fwd_stash_64x64", "gemm_fwd_delta_64x64", "gemm_fwd_out_64x64", "gemm_bwd_64x64",
+        "gemm_dw_sgd_64x64", "gemm_dw_partial_64x64"}},
+      {{"gemm64_fwd_stash_128x128", "gemm64_fwd_delta_128x128", "gemm64_fwd_out_128x128",
+        "gemm64_bwd_128x128", "gemm64_dw_sgd_128x128", "gemm64_dw_partial_128x128"},
+       {"gemm64_fwd_stash_64x64", "gemm64_fwd_delta_64x64", "gemm64_fwd_out_64x64",
+        "gemm64_bwd_64x64", "gemm64_dw_sgd_64x64", "gemm64_dw_partial_64x64"}}};
+  if (epi < 0 || epi > 5 || tile < 0 || tile > 1 || dtype < 0 || dtype > 1) return "gemm";
+  return names[dtype][tile][epi];
 }
 
-hipError_t launch_fold_sgd(const float* partial, int64_t pstride, const float* pbias, int nshards,
-                           int nsub, int M, int N, int64_t ldw, float* G, float* gbias,
-                           const float* Win, const float* bin, float* W, float* b, float scale,
-                           hipStream_t s) {
+template <class T>
+hipError_t launch_fold_sgd(const T* partial, int64_t pstride, const T* pbias, int nshards,
+                           int nsub, int M, int N, int64_t ldw, T* G, T* gbias, const T* Win,
+                           const T* bin, T* W, T* b, T scale, hipStream_t s) {
   const int64_t total = (int64_t)M * N + M;
   const int threads = 256;
   const int64_t blocks = (total + threads - 1) / threads;
-  fold_sgd_kernel<<<dim3((unsigned)blocks), threads, 0, s>>>(partial, pstride, pbias, nshards, nsub,
-                                                           M, N, ldw, G, gbias, Win, bin, W, b,
-                                                           scale);
+  fold_sgd_kernel<T><<<dim3((unsigned)blocks), threads, 0, s>>>(partial, pstride, pbias, nshards,
+                                                              nsub, M, N, ldw, G, gbias, Win, bin,
+                                                              W, b, scale);
   return hipGetLastError();
 }
+
+template hipError_t launch_fold_sgd<float>(const float*, int64_t, const float*, int, int, int, int,
+                                           int64_t, float*, float*, const float*, const float*,
+                                           float*, float*, float, hipStream_t);
+template hipError_t launch_fold_sgd<double>(const double*, int64_t, const double*, int, int, int,
+                                            int, int64_t, double*, double*, const double*,
+                                            const double*, double*, double*, double, hipStream_t);
 
 }  // namespace nf

@@ -4,8 +4,9 @@ other implementation behind these functions.  Importing this module fails
 loudly when the library has not been built.
 
 Device buffers are passed as torch CUDA (HIP) tensors, which supply the device
-pointer; streams default to torch's current stream.  Tensors must be fp32 and
-contiguous on the net's device.
+pointer; streams default to torch's current stream.  Tensors must be
+contiguous on the net's device, fp32 for the plain entry points and fp64 for
+their _f64 twins (nets created with dtype NF_F64).
 """
 
 from __future__ import annotations
@@ -39,6 +40,7 @@ NF_GAUSSIAN, NF_RELU, NF_SIGMOID, NF_STEP, NF_TANH = 0, 1, 2, 3, 4
 ACT_CODES = {"gaussian": NF_GAUSSIAN, "relu": NF_RELU, "sigmoid": NF_SIGMOID,
              "step": NF_STEP, "tanh": NF_TANH}
 NF_OK, NF_EINVAL, NF_ESHAPE, NF_ENOMEM, NF_EDEVICE = 0, -1, -2, -3, -4
+NF_F32, NF_F64 = 0, 1
 STATUS_NAMES = {0: "NF_OK", -1: "NF_EINVAL", -2: "NF_ESHAPE", -3: "NF_ENOMEM", -4: "NF_EDEVICE"}
 
 _c_i32p = ctypes.POINTER(ctypes.c_int32)
@@ -54,6 +56,9 @@ class nf_kernel_stat(ctypes.Structure):
 _sig = {
     "nf_net_create": (ctypes.c_int, [_c_i32p, ctypes.c_int32, _c_i32p, ctypes.c_int32,
                                      ctypes.POINTER(ctypes.c_void_p)]),
+    "nf_net_create_ex": (ctypes.c_int, [_c_i32p, ctypes.c_int32, _c_i32p, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
+    "nf_net_dtype": (ctypes.c_int32, [_net_p]),
     "nf_net_destroy": (ctypes.c_int, [_net_p]),
     "nf_param_count": (ctypes.c_int64, [_net_p]),
     "nf_set_params": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
@@ -73,6 +78,25 @@ _sig = {
                                         ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]),
     "nf_accuracy": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                    ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p]),
+    "nf_set_params_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
+    "nf_get_params_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
+    "nf_get_grads_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
+    "nf_forward_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                      ctypes.c_void_p]),
+    "nf_train_batch_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_double, ctypes.c_int32,
+                                          ctypes.c_void_p]),
+    "nf_train_epoch_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_double,
+                                          ctypes.c_int32, ctypes.c_void_p]),
+    "nf_train_single_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_double, ctypes.c_void_p]),
+    "nf_train_windows_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                                            ctypes.c_int64, ctypes.c_double, ctypes.c_int32,
+                                            ctypes.c_void_p]),
+    "nf_accuracy_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                       ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p]),
     "nf_profile": (ctypes.c_int, [_net_p, ctypes.c_int32]),
     "nf_profile_read": (ctypes.c_int, [_net_p, ctypes.POINTER(nf_kernel_stat), ctypes.c_int32,
                                        ctypes.POINTER(ctypes.c_int32)]),
@@ -104,12 +128,13 @@ def _check(status: int, where: str) -> None:
         raise NfError(status, where)
 
 
-def _dev_ptr(t, name: str) -> int:
+def _dev_ptr(t, name: str, f64: bool = False) -> int:
     import torch
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch tensor on the GPU")
-    if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
-        raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
+    want = torch.float64 if f64 else torch.float32
+    if t.dtype != want or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {want} GPU tensor")
     return t.data_ptr()
 
 
@@ -122,9 +147,11 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream or None
 
 
-def nf_net_create(dims: Sequence[int], acts: Union[None, str, Sequence[str], Sequence[int]] = None):
+def nf_net_create(dims: Sequence[int], acts: Union[None, str, Sequence[str], Sequence[int]] = None,
+                  dtype: int = NF_F32):
     """Returns an opaque handle (int).  acts: None (sigmoid everywhere), one
-    name, or one per layer after the input."""
+    name, or one per layer after the input.  dtype NF_F64 creates an fp64 net
+    (nf_net_create_ex), driven with the _f64 functions."""
     d = (ctypes.c_int32 * len(dims))(*[int(v) for v in dims])
     if acts is None:
         codes = []
@@ -134,9 +161,17 @@ def nf_net_create(dims: Sequence[int], acts: Union[None, str, Sequence[str], Seq
         codes = [ACT_CODES[a] if isinstance(a, str) else int(a) for a in acts]
     a = (ctypes.c_int32 * max(1, len(codes)))(*codes)
     out = ctypes.c_void_p()
-    _check(_lib.nf_net_create(d, len(dims), a if codes else None, len(codes), ctypes.byref(out)),
-           "nf_net_create")
+    if dtype == NF_F32:
+        _check(_lib.nf_net_create(d, len(dims), a if codes else None, len(codes),
+                                  ctypes.byref(out)), "nf_net_create")
+    else:
+        _check(_lib.nf_net_create_ex(d, len(dims), a if codes else None, len(codes), int(dtype),
+                                     ctypes.byref(out)), "nf_net_create_ex")
     return out.value
+
+
+def nf_net_dtype(net) -> int:
+    return int(_lib.nf_net_dtype(net))
 
 
 def nf_net_destroy(net) -> None:
@@ -201,6 +236,61 @@ def nf_accuracy(net, x, y, stream=None) -> int:
     c = ctypes.c_int64()
     _check(_lib.nf_accuracy(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0], ctypes.byref(c),
                             _stream(stream)), "nf_accuracy")
+    return int(c.value)
+
+
+def nf_set_params_f64(net, params: np.ndarray) -> None:
+    p = np.ascontiguousarray(params, dtype=np.float64)
+    _check(_lib.nf_set_params_f64(net, p.ctypes.data, p.size), "nf_set_params_f64")
+
+
+def nf_get_params_f64(net) -> np.ndarray:
+    out = np.empty(nf_param_count(net), dtype=np.float64)
+    _check(_lib.nf_get_params_f64(net, out.ctypes.data, out.size), "nf_get_params_f64")
+    return out
+
+
+def nf_get_grads_f64(net) -> np.ndarray:
+    out = np.empty(nf_param_count(net), dtype=np.float64)
+    _check(_lib.nf_get_grads_f64(net, out.ctypes.data, out.size), "nf_get_grads_f64")
+    return out
+
+
+def nf_forward_f64(net, x, out, stream=None) -> None:
+    _check(_lib.nf_forward_f64(net, _dev_ptr(x, "x", True), x.shape[0], _dev_ptr(out, "out", True),
+                               _stream(stream)), "nf_forward_f64")
+
+
+def nf_train_batch_f64(net, x, y, eta: float, n_shards: int = 1, stream=None) -> None:
+    _check(_lib.nf_train_batch_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True), x.shape[0],
+                                   float(eta), int(n_shards), _stream(stream)),
+           "nf_train_batch_f64")
+
+
+def nf_train_epoch_f64(net, x, y, batch: int, eta: float, n_shards: int = 1, stream=None) -> None:
+    _check(_lib.nf_train_epoch_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True), x.shape[0],
+                                   int(batch), float(eta), int(n_shards), _stream(stream)),
+           "nf_train_epoch_f64")
+
+
+def nf_train_single_f64(net, x, y, eta: float, stream=None) -> None:
+    _check(_lib.nf_train_single_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True),
+                                    float(eta), _stream(stream)), "nf_train_single_f64")
+
+
+def nf_train_windows_f64(net, x, y, batch: int, pos, eta: float, n_shards: int = 1,
+                         stream=None) -> None:
+    p = np.ascontiguousarray(pos, dtype=np.float64)
+    _check(_lib.nf_train_windows_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True),
+                                     x.shape[0], int(batch), p.ctypes.data if p.size else None,
+                                     p.size, float(eta), int(n_shards), _stream(stream)),
+           "nf_train_windows_f64")
+
+
+def nf_accuracy_f64(net, x, y, stream=None) -> int:
+    c = ctypes.c_int64()
+    _check(_lib.nf_accuracy_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True), x.shape[0],
+                                ctypes.byref(c), _stream(stream)), "nf_accuracy_f64")
     return int(c.value)
 
 

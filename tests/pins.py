@@ -330,6 +330,19 @@ def check_window_starts(m) -> List[str]:
         got = m.window_start(top, span + 99, 100)
         if got != span - 1:
             fails.append(f"span {span}: start at the top of [0,1) is {got}, expected {span - 1}")
+    # the real64 kind: the same grid, and the largest double below 1
+    for n, b in ((40, 7), (1000, 100), (60000, 1000)):
+        span = n - b + 1
+        for k in range(64):
+            got = m.window_start(k / 64.0, n, b, "f64")
+            if got != (k * span) // 64:
+                fails.append(f"f64 n={n} B={b} pos={k}/64: start {got}")
+                return fails
+    top64 = float(np.nextafter(1.0, 0.0))
+    for span in (1, 3, 59001, (1 << 24) - 1, (1 << 40) + 1):
+        got = m.window_start(top64, span + 99, 100, "f64")
+        if got != span - 1:
+            fails.append(f"f64 span {span}: start at the top of [0,1) is {got}, expected {span - 1}")
     return fails
 
 

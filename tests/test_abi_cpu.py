@@ -60,6 +60,14 @@ def test_create_rejects_bad_arguments(dims, acts, expect):
     assert nf.nf_last_error() != ""
 
 
+@pytest.mark.parametrize("dtype,expect", [(2, nf.NF_EINVAL), (-1, nf.NF_EINVAL)])
+def test_create_ex_rejects_unknown_dtype(dtype, expect):
+    d = (ctypes.c_int32 * 3)(4, 3, 2)
+    out = ctypes.c_void_p(12345)
+    assert nf.raw().nf_net_create_ex(d, 3, None, 0, dtype, ctypes.byref(out)) == expect
+    assert out.value == 12345
+
+
 def test_create_null_out():
     d = (ctypes.c_int32 * 2)(3, 2)
     assert nf.raw().nf_net_create(d, 2, None, 0, None) == nf.NF_EINVAL
@@ -80,6 +88,17 @@ def test_null_net_calls():
     assert lib.nf_train_windows(None, buf, buf, 4, 1, buf, 1, 1.0, 1, None) == nf.NF_EINVAL
     cnt = ctypes.c_int64()
     assert lib.nf_accuracy(None, buf, buf, 1, ctypes.byref(cnt), None) == nf.NF_EINVAL
+    assert lib.nf_net_dtype(None) == -1
+    dbuf = (ctypes.c_double * 4)()
+    assert lib.nf_set_params_f64(None, dbuf, 4) == nf.NF_EINVAL
+    assert lib.nf_get_params_f64(None, dbuf, 4) == nf.NF_EINVAL
+    assert lib.nf_get_grads_f64(None, dbuf, 4) == nf.NF_EINVAL
+    assert lib.nf_forward_f64(None, dbuf, 1, dbuf, None) == nf.NF_EINVAL
+    assert lib.nf_train_batch_f64(None, dbuf, dbuf, 1, 1.0, 1, None) == nf.NF_EINVAL
+    assert lib.nf_train_epoch_f64(None, dbuf, dbuf, 1, 1, 1.0, 1, None) == nf.NF_EINVAL
+    assert lib.nf_train_single_f64(None, dbuf, dbuf, 1.0, None) == nf.NF_EINVAL
+    assert lib.nf_train_windows_f64(None, dbuf, dbuf, 4, 1, dbuf, 1, 1.0, 1, None) == nf.NF_EINVAL
+    assert lib.nf_accuracy_f64(None, dbuf, dbuf, 1, ctypes.byref(cnt), None) == nf.NF_EINVAL
 
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the behaviour without a GPU")
