@@ -1,12 +1,16 @@
 """Throughput of mini-batch MLP training on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2] [--dtype f32]
 
 One step is one pass of the whole training path over the workload's data:
 every SGD step of one epoch (forward, back-propagation, batch tendencies,
 update) plus, where the workload has a held-out set, batched inference on it.
 Inputs are resident in device memory before timing starts.  Prints one JSON
 line on stdout; per-kernel timings go to stderr.
+
+--dtype f64 runs the same workload with an fp64 net (the paper's real64 kind):
+inputs, targets and parameters in fp64, every kernel in fp64, the roofline
+against the fp64 matrix peak.
 
 The default workload is the paper's MNIST network shape (784-30-10, sigmoid,
 section 4) on synthetic MNIST-shaped data: 60000 uniform [0,1) 784-vectors
@@ -29,7 +33,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
-RIDGE = FP32_MFMA_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)   # flop per byte
+FP64_MFMA_PEAK_TFS = 78.6      # MI355X dense fp64 matrix, TFLOP/s
 PROFILE_REPEATS = 20
 
 METRIC = "training samples/sec (fwd+bwd+SGD) at 784-30-10 and wide MLP; % HBM/MFMA roofline"
@@ -70,7 +74,7 @@ def read_traffic(kernel: str, workload: str, sha: str):
     return None
 
 
-def cpu_baseline(w, X, Y, Xh, budget_s: float):
+def cpu_baseline(w, X, Y, Xh, budget_s: float, precision: str = "f32"):
     """The CPU reference (unchanged) timed on the host cores: whole steps of
     the same workload, repeated until about budget_s seconds have passed."""
     import numpy as np
@@ -90,7 +94,8 @@ def cpu_baseline(w, X, Y, Xh, budget_s: float):
     while not stop:
         for t in range(w.steps):
             sl = slice(t * w.batch, (t + 1) * w.batch)
-            theta, _ = mlp.train_batch(theta, w.dims, list(w.acts), X[sl], Y[sl], w.eta, w.shards)
+            theta, _ = mlp.train_batch(theta, w.dims, list(w.acts), X[sl], Y[sl], w.eta, w.shards,
+                                       precision=precision)
             sgd_steps += 1
             if time.perf_counter() - t0 > 3 * budget_s:
                 stop = True
@@ -117,6 +122,8 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c2", choices=sorted(DESCRIBE))
+    ap.add_argument("--dtype", default="f32", choices=("f32", "f64"),
+                    help="element type of the net (f64: the real64 variant)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU-reference timing (0 skips it)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -150,24 +157,32 @@ def main(argv=None) -> int:
         return 0
 
     w = W.WORKLOADS[args.workload]
+    f64 = args.dtype == "f64"
+    npt = np.float64 if f64 else np.float32
+    tdt = torch.float64 if f64 else torch.float32
     print(f"[bench] generating {w.name} data", file=sys.stderr, flush=True)
     X, Y = W.make_data(w)
     Xh = W.make_data(w, heldout=True)[0] if w.heldout else None
     theta0 = W.make_params(w)
-    xd = torch.from_numpy(X).to(dev)
-    yd = torch.from_numpy(Y).to(dev)
-    xhd = torch.from_numpy(Xh).to(dev) if Xh is not None else None
-    outd = torch.empty((Xh.shape[0], w.dims[-1]), dtype=torch.float32, device=dev) if Xh is not None else None
+    xd = torch.from_numpy(X.astype(npt)).to(dev)
+    yd = torch.from_numpy(Y.astype(npt)).to(dev)
+    xhd = torch.from_numpy(Xh.astype(npt)).to(dev) if Xh is not None else None
+    outd = torch.empty((Xh.shape[0], w.dims[-1]), dtype=tdt, device=dev) if Xh is not None else None
     n_train = w.batch * w.steps
+    train_epoch = nf.nf_train_epoch_f64 if f64 else nf.nf_train_epoch
+    forward = nf.nf_forward_f64 if f64 else nf.nf_forward
 
-    net = nf.nf_net_create(w.dims, list(w.acts))
+    net = nf.nf_net_create(w.dims, list(w.acts), dtype=nf.NF_F64 if f64 else nf.NF_F32)
     try:
-        nf.nf_set_params(net, theta0)
+        if f64:
+            nf.nf_set_params_f64(net, theta0.astype(np.float64))
+        else:
+            nf.nf_set_params(net, theta0)
 
         def step():
-            nf.nf_train_epoch(net, xd[:n_train], yd[:n_train], w.batch, w.eta, w.shards)
+            train_epoch(net, xd[:n_train], yd[:n_train], w.batch, w.eta, w.shards)
             if xhd is not None:
-                nf.nf_forward(net, xhd, outd)
+                forward(net, xhd, outd)
 
         print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
         for _ in range(args.warmup):
@@ -193,7 +208,7 @@ def main(argv=None) -> int:
         step()
         stats = nf.nf_profile_read(net)
         nf.nf_profile(net, 0)
-        finite = bool(np.all(np.isfinite(nf.nf_get_params(net))))
+        finite = bool(np.all(np.isfinite(nf.nf_get_params_f64(net) if f64 else nf.nf_get_params(net))))
     finally:
         nf.nf_net_destroy(net)
 
@@ -207,15 +222,17 @@ def main(argv=None) -> int:
     bytes_l = dom["bytes"] / dom["launches"]
     flops_l = dom["flops"] / dom["launches"]
     sha = kernel_sources_sha()
-    if flops_l / bytes_l < RIDGE:
+    mfma_peak = FP64_MFMA_PEAK_TFS if f64 else FP32_MFMA_PEAK_TFS
+    ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)   # flop per byte
+    if flops_l / bytes_l < ridge:
         achieved = bytes_l / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
     else:
         achieved = flops_l / avg_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFS,
-                "unit": "TFLOP/s", "frac": achieved / FP32_MFMA_PEAK_TFS}
-    roof["traffic"] = read_traffic(dom["name"], w.name, sha)
+        roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
+                "unit": "TFLOP/s", "frac": achieved / mfma_peak}
+    roof["traffic"] = read_traffic(dom["name"], w.name + ("_f64" if f64 else ""), sha)
     roof["kernel"] = dom["name"]
     roof["avg_us"] = avg_s * 1e6
     roof["bytes_per_launch"] = bytes_l
@@ -233,9 +250,10 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": args.dtype,
         "data": "synthetic",
-        "config": {"workload": DESCRIBE[w.name], "dims": list(w.dims), "batch": w.batch,
+        "config": {"workload": DESCRIBE[w.name].replace("fp32", "fp64") if f64 else DESCRIBE[w.name],
+                   "dims": list(w.dims), "batch": w.batch,
                    "sgd_steps_per_step": w.steps, "training_samples_per_step": n_train,
                    "heldout_per_step": int(Xh.shape[0]) if Xh is not None else 0,
                    "shards": w.shards, "kernel_sources": sha},
@@ -245,7 +263,7 @@ def main(argv=None) -> int:
     if args.cpu_seconds > 0:
         print(f"[bench] timing the CPU reference (~{args.cpu_seconds:.0f} s)", file=sys.stderr,
               flush=True)
-        line["cpu_baseline"] = cpu_baseline(w, X, Y, Xh, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, X, Y, Xh, args.cpu_seconds, args.dtype)
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)
