@@ -194,6 +194,22 @@ nf_status nf_train_windows_f64(nf_net* net, const double* d_x, const double* d_y
 nf_status nf_accuracy_f64(nf_net* net, const double* d_x, const double* d_y, int64_t n,
                           int64_t* host_correct, void* stream);
 
+/* Save a network to a file and create one from it (section 2 lists saving
+ * and loading networks among the framework's features; the paper does not
+ * fix a format).  The file is little-endian binary:
+ *   bytes 0..7  "NFNET01\n"
+ *   int32       element type (nf_dtype)
+ *   int32       n_dims, then int32 dims[n_dims] and int32 acts[n_dims - 1]
+ *   int64       n_params, then the parameters in canonical order, in the
+ *               net's element type
+ *   uint64      FNV-1a 64-bit hash of every preceding byte
+ * nf_save waits for the net's outstanding work.  nf_load checks the whole file
+ * (magic, sizes, length, hash) before it creates the net on the current
+ * device; a file that fails a check gives NF_EINVAL and *out is not written.
+ * Tendencies and per-sample buffers are not saved. */
+nf_status nf_save(nf_net* net, const char* path);
+nf_status nf_load(const char* path, nf_net** out);
+
 /* Per-kernel timing, for measuring the method's computational performance the
  * way section 5 reports it (elapsed time), one kernel at a time.  While
  * recording is on, every kernel the net launches is bracketed by a pair of HIP

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <exception>
@@ -918,9 +919,153 @@ nf_status accuracy(nf_net* net, const T* d_x, const T* d_y, int64_t n, int64_t* 
   });
 }
 
+// ---------------------------------------------------------------------------
+// save / load: a self-describing little-endian binary file
+//   bytes 0..7   magic "NFNET01\n"
+//   int32        element type (nf_dtype)
+//   int32        n_dims, then int32 dims[n_dims], int32 acts[n_dims - 1]
+//   int64        n_params, then n_params elements in canonical order
+//   uint64       FNV-1a hash of every byte before it
+// ---------------------------------------------------------------------------
+constexpr char kMagic[8] = {'N', 'F', 'N', 'E', 'T', '0', '1', '\n'};
+
+struct Fnv {
+  uint64_t h = 1469598103934665603ull;
+  void add(const void* p, size_t n) {
+    const unsigned char* b = static_cast<const unsigned char*>(p);
+    for (size_t i = 0; i < n; ++i) {
+      h ^= b[i];
+      h *= 1099511628211ull;
+    }
+  }
+};
+
+struct File {
+  FILE* f = nullptr;
+  ~File() {
+    if (f) std::fclose(f);
+  }
+};
+
+bool little_endian() {
+  const uint32_t one = 1;
+  unsigned char c;
+  std::memcpy(&c, &one, 1);
+  return c == 1;
+}
+
+nf_status save(nf_net* net, const char* path) {
+  if (!path) return fail(NF_EINVAL, "path is NULL");
+  if (!little_endian()) return fail(NF_EINVAL, "the file format is little-endian");
+  std::vector<char> params((size_t)net->n_params * net->esz);
+  nf_status st = copy_params(net, net->pbuf[net->cur], nullptr, params.data(), net->n_params);
+  if (st != NF_OK) return st;
+  std::vector<char> out;
+  auto put = [&](const void* p, size_t n) {
+    out.insert(out.end(), static_cast<const char*>(p), static_cast<const char*>(p) + n);
+  };
+  const int32_t dtype = net->dtype == nf::DT_F64 ? NF_F64 : NF_F32;
+  const int32_t nd = (int32_t)net->dims.size();
+  put(kMagic, sizeof(kMagic));
+  put(&dtype, 4);
+  put(&nd, 4);
+  for (int32_t d : net->dims) put(&d, 4);
+  for (size_t l = 1; l < net->layers.size(); ++l) {
+    const int32_t a = net->layers[l].act;
+    put(&a, 4);
+  }
+  const int64_t np = net->n_params;
+  put(&np, 8);
+  put(params.data(), params.size());
+  Fnv h;
+  h.add(out.data(), out.size());
+  put(&h.h, 8);
+  File f;
+  f.f = std::fopen(path, "wb");
+  if (!f.f) return fail(NF_EINVAL, std::string("cannot open ") + path + " for writing");
+  if (std::fwrite(out.data(), 1, out.size(), f.f) != out.size() || std::fflush(f.f) != 0)
+    return fail(NF_EINVAL, std::string("cannot write ") + path);
+  return NF_OK;
+}
+
+nf_status load(const char* path, nf_net** out) {
+  if (!path || !out) return fail(NF_EINVAL, "path or out is NULL");
+  if (!little_endian()) return fail(NF_EINVAL, "the file format is little-endian");
+  File f;
+  f.f = std::fopen(path, "rb");
+  if (!f.f) return fail(NF_EINVAL, std::string("cannot open ") + path);
+  std::vector<char> buf;
+  char chunk[1 << 16];
+  size_t got;
+  while ((got = std::fread(chunk, 1, sizeof(chunk), f.f)) > 0) {
+    buf.insert(buf.end(), chunk, chunk + got);
+    if (buf.size() > ((size_t)1 << 36)) return fail(NF_EINVAL, "file too large");
+  }
+  size_t pos = 0;
+  auto take = [&](void* dst, size_t n) {
+    if (buf.size() < pos + n) return false;
+    std::memcpy(dst, buf.data() + pos, n);
+    pos += n;
+    return true;
+  };
+  const std::string bad = std::string("not a valid network file: ") + path;
+  char magic[8];
+  int32_t dtype = 0, nd = 0;
+  if (!take(magic, 8) || std::memcmp(magic, kMagic, 8) != 0) return fail(NF_EINVAL, bad);
+  if (!take(&dtype, 4) || !take(&nd, 4)) return fail(NF_EINVAL, bad);
+  if (dtype != NF_F32 && dtype != NF_F64) return fail(NF_EINVAL, bad + " (element type)");
+  if (nd < 2 || nd > 1024) return fail(NF_EINVAL, bad + " (layer count)");
+  std::vector<int32_t> dims(nd), acts(nd - 1);
+  for (auto& d : dims)
+    if (!take(&d, 4)) return fail(NF_EINVAL, bad);
+  for (auto& a : acts)
+    if (!take(&a, 4)) return fail(NF_EINVAL, bad);
+  int64_t np = 0;
+  if (!take(&np, 8)) return fail(NF_EINVAL, bad);
+  int64_t want = 0;
+  for (int l = 1; l < nd; ++l) {
+    if (dims[l - 1] < 1 || dims[l - 1] > 65536 || dims[l] < 1 || dims[l] > 65536)
+      return fail(NF_EINVAL, bad + " (layer sizes)");
+    want += (int64_t)dims[l] * dims[l - 1] + dims[l];
+  }
+  const size_t es = dtype == NF_F64 ? sizeof(double) : sizeof(float);
+  if (np != want) return fail(NF_EINVAL, bad + " (parameter count)");
+  if (buf.size() != pos + (size_t)np * es + 8) return fail(NF_EINVAL, bad + " (length)");
+  Fnv h;
+  h.add(buf.data(), pos + (size_t)np * es);
+  uint64_t stored = 0;
+  std::memcpy(&stored, buf.data() + pos + (size_t)np * es, 8);
+  if (stored != h.h) return fail(NF_EINVAL, bad + " (checksum)");
+  nf_net* n = nullptr;
+  nf_status st = create(dims.data(), nd, acts.data(), nd - 1, dtype, &n);
+  if (st != NF_OK) return st;
+  st = copy_params(n, n->pbuf[n->cur], buf.data() + pos, nullptr, np);
+  if (st != NF_OK) {
+    const std::string msg = g_err;
+    (void)hipFree(n->pbuf[0]);
+    (void)hipFree(n->pbuf[1]);
+    (void)hipFree(n->grads);
+    delete n;
+    return fail(st, msg);
+  }
+  *out = n;
+  return NF_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+nf_status nf_save(nf_net* net, const char* path) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net(net);
+    return st != NF_OK ? st : save(net, path);
+  });
+}
+
+nf_status nf_load(const char* path, nf_net** out) {
+  return guarded([&]() { return load(path, out); });
+}
 
 nf_status nf_net_create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32_t n_acts,
                         nf_net** out) {

@@ -97,6 +97,8 @@ _sig = {
                                             ctypes.c_void_p]),
     "nf_accuracy_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                        ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p]),
+    "nf_save": (ctypes.c_int, [_net_p, ctypes.c_char_p]),
+    "nf_load": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p)]),
     "nf_profile": (ctypes.c_int, [_net_p, ctypes.c_int32]),
     "nf_profile_read": (ctypes.c_int, [_net_p, ctypes.POINTER(nf_kernel_stat), ctypes.c_int32,
                                        ctypes.POINTER(ctypes.c_int32)]),
@@ -292,6 +294,17 @@ def nf_accuracy_f64(net, x, y, stream=None) -> int:
     _check(_lib.nf_accuracy_f64(net, _dev_ptr(x, "x", True), _dev_ptr(y, "y", True), x.shape[0],
                                 ctypes.byref(c), _stream(stream)), "nf_accuracy_f64")
     return int(c.value)
+
+
+def nf_save(net, path: str) -> None:
+    _check(_lib.nf_save(net, os.fsencode(path)), "nf_save")
+
+
+def nf_load(path: str):
+    """Returns the handle of a new net created from the file."""
+    out = ctypes.c_void_p()
+    _check(_lib.nf_load(os.fsencode(path), ctypes.byref(out)), "nf_load")
+    return out.value
 
 
 def nf_profile(net, repeats: int) -> None:

@@ -120,3 +120,58 @@ def test_one_hip_runtime_per_process():
                          cwd=__import__("os").path.dirname(nf.LIB_PATH) + "/..")
     assert res.returncode == 0, res.stderr
     assert res.stdout.strip() == "1"
+
+
+def _net_file(dtype=0, dims=(3, 2), acts=(2,), params=None, magic=b"NFNET01\n", count=None,
+              corrupt_hash=False, extra=b""):
+    """A network file written by the test itself, following the layout
+    include/nf.h documents."""
+    import struct
+    n = sum(dims[l] * dims[l - 1] + dims[l] for l in range(1, len(dims)))
+    params = [0.5] * n if params is None else params
+    body = magic + struct.pack("<ii", dtype, len(dims)) + struct.pack(f"<{len(dims)}i", *dims)
+    body += struct.pack(f"<{len(acts)}i", *acts) + struct.pack("<q", n if count is None else count)
+    body += struct.pack(f"<{len(params)}{'d' if dtype else 'f'}", *params)
+    h = 1469598103934665603
+    for b in body:
+        h = ((h ^ b) * 1099511628211) & 0xFFFFFFFFFFFFFFFF
+    if corrupt_hash:
+        h ^= 1
+    return body + struct.pack("<Q", h) + extra
+
+
+@pytest.mark.parametrize("case", ["missing", "magic", "count", "hash", "trailing", "truncated",
+                                  "dtype", "layers"])
+def test_load_rejects_bad_files(tmp_path, case):
+    path = tmp_path / "net.bin"
+    if case == "magic":
+        path.write_bytes(_net_file(magic=b"NFNET02\n"))
+    elif case == "count":
+        path.write_bytes(_net_file(count=7))
+    elif case == "hash":
+        path.write_bytes(_net_file(corrupt_hash=True))
+    elif case == "trailing":
+        path.write_bytes(_net_file(extra=b"\0"))
+    elif case == "truncated":
+        path.write_bytes(_net_file()[:-3])
+    elif case == "dtype":
+        path.write_bytes(_net_file(dtype=5))
+    elif case == "layers":
+        path.write_bytes(_net_file(dims=(3,), acts=()))
+    out = ctypes.c_void_p(12345)
+    st = nf.raw().nf_load(str(path).encode(), ctypes.byref(out))
+    assert st == nf.NF_EINVAL, nf.nf_last_error()
+    assert out.value == 12345
+    assert nf.nf_last_error() != ""
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the behaviour without a GPU")
+def test_load_of_a_valid_file_needs_a_device(tmp_path):
+    path = tmp_path / "net.bin"
+    path.write_bytes(_net_file())
+    out = ctypes.c_void_p(12345)
+    assert nf.raw().nf_load(str(path).encode(), ctypes.byref(out)) == nf.NF_EDEVICE
+
+
+def test_save_rejects_null():
+    assert nf.raw().nf_save(None, b"/tmp/x") == nf.NF_EINVAL
