@@ -65,8 +65,17 @@ __device__ __forceinline__ void load_small_layers(const NarrowFwdParams& p, int 
   for (int l = 0; l < NARROW_MAX_LAYERS; ++l) r.b[l] = p.bias[l][tid & (NARROW_WIDTH - 1)];
 }
 
+// LDS row pitch of the per-sample activations and the small layers' weights:
+// 16-byte aligned rows, so a row is read with eight 16-byte loads.
+constexpr int NWP = NARROW_WIDTH + 4;
+
+// The small layers' weights go to LDS twice when training: ws[l][j][i] = W(j, i)
+// for the forward sums and wsT[l][i][j] = W(j, i) for the delta sums, so
+// both read whole rows.
+template <bool TRANSPOSED>
 __device__ __forceinline__ void store_small_layers(const SmallLayers& r, int tid,
-                                                   float (*ws)[NARROW_WIDTH][NARROW_WIDTH + 1],
+                                                   float (*ws)[NARROW_WIDTH][NWP],
+                                                   float (*wsT)[NARROW_WIDTH][NWP],
                                                    float (*bs)[NARROW_WIDTH]) {
   constexpr int NW = NARROW_WIDTH;
 #pragma unroll
@@ -75,11 +84,28 @@ __device__ __forceinline__ void store_small_layers(const SmallLayers& r, int tid
     for (int u = 0; u < NSTAGE; ++u) {
       const int e = tid + u * N1_WAVES * 64;
       ws[li][e / NW][e % NW] = r.w[li][u];
+      if (TRANSPOSED) wsT[li][e % NW][e / NW] = r.w[li][u];
     }
   if (tid < NW) {
 #pragma unroll
     for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bs[l][tid] = r.b[l];
   }
+}
+
+// sum over i < 32 of w[i] h[i] from two 16-byte aligned LDS rows, in four
+// interleaved partial sums added pairwise
+__device__ __forceinline__ float dot32(const float* w, const float* h) {
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int m = 0; m < NARROW_WIDTH / 4; ++m) {
+    const float4 a = *reinterpret_cast<const float4*>(w + 4 * m);
+    const float4 x = *reinterpret_cast<const float4*>(h + 4 * m);
+    acc[0] = fmaf(a.x, x.x, acc[0]);
+    acc[1] = fmaf(a.y, x.y, acc[1]);
+    acc[2] = fmaf(a.z, x.z, acc[2]);
+    acc[3] = fmaf(a.w, x.w, acc[3]);
+  }
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
 // Target of thread (sample tid / 32, output unit tid % 32) of a T-sample tile.
@@ -102,8 +128,9 @@ __device__ __forceinline__ float load_target(const NarrowFwdParams& p, int s0, i
 // f'(z_l) kept in registers.  Threads past 32 T only join the barriers.
 template <bool TRAIN, int T>
 __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, int tid, float z1,
-                                            float ytg, float (*hs)[T][NARROW_WIDTH + 1],
-                                            const float (*ws)[NARROW_WIDTH][NARROW_WIDTH + 1],
+                                            float ytg, float (*hs)[T][NWP],
+                                            const float (*ws)[NARROW_WIDTH][NWP],
+                                            const float (*wsT)[NARROW_WIDTH][NWP],
                                             const float (*bs)[NARROW_WIDTH]) {
   constexpr int NW = NARROW_WIDTH;
   const bool active = tid < T * NW;
@@ -138,9 +165,7 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
     if (l > p.L) break;
     if (active) {
       const int dl = p.dims[l];
-      float z = 0.0f;
-#pragma unroll
-      for (int i = 0; i < NW; ++i) z = fmaf(ws[l - 2][j][i], hs[cur][s][i], z);
+      const float z = dot32(ws[l - 2][j], hs[cur][s]);
       float a = 0.0f, f = 0.0f;
       if (j < dl) act_eval(p.acts[l - 1], z + bs[l - 1][j], a, f);
       fp[l - 1] = f;
@@ -167,9 +192,7 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
   for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
     if (l >= p.L) continue;
     if (active) {
-      float t = 0.0f;
-#pragma unroll
-      for (int k = 0; k < NW; ++k) t = fmaf(ws[l - 1][k][j], hs[cur][s][k], t);
+      const float t = dot32(wsT[l - 1][j], hs[cur][s]);
       const float d = j < p.dims[l] ? t * fp[l - 1] : 0.0f;
       hs[cur ^ 1][s][j] = d;
       if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
@@ -194,8 +217,9 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
   auto xs = reinterpret_cast<float(*)[T][N1_KP]>(stage);
   auto wsl = reinterpret_cast<float(*)[NW][N1_KP]>(stage + 2 * T * N1_KP);
   auto zp = reinterpret_cast<float(*)[T][NW + 1]>(stage);
-  __shared__ float hs[2][T][NW + 1];                         // activations, then deltas
-  __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];    // W_2 .. W_L
+  __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];   // activations, then deltas
+  __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];  // W_2 .. W_L
+  __shared__ __attribute__((aligned(16))) float wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][NWP];
   __shared__ float bs[NARROW_MAX_LAYERS][NW];                // b_1 .. b_L
 
   const int tid = threadIdx.x;
@@ -279,7 +303,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
       zp[wave][4 * g + v][16 + r] = acc1[v];
     }
   }
-  store_small_layers(sl, tid, ws, bs);
+  store_small_layers<TRAIN>(sl, tid, ws, wsT, bs);
   __syncthreads();
 
   // z_1 of (sample tid / 32, unit tid % 32): the waves' sums in wave order
@@ -290,7 +314,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
 #pragma unroll
     for (int w = 1; w < N1_WAVES; ++w) z1 += zp[w][s][j];
   }
-  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, bs);
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, bs);
 }
 
 // ---------------------------------------------------------------------------
@@ -320,8 +344,9 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
   constexpr int NW = NARROW_WIDTH;
   __shared__ float red[T * N4_SS];                           // [sample][wave*16+block][unit]
   __shared__ float psum[4][T][NW];
-  __shared__ float hs[2][T][NW + 1];
-  __shared__ float ws[NARROW_MAX_LAYERS - 1][NW][NW + 1];
+  __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];
+  __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];
+  __shared__ __attribute__((aligned(16))) float wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][NWP];
   __shared__ float bs[NARROW_MAX_LAYERS][NW];
 
   const int tid = threadIdx.x;
@@ -391,7 +416,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
       for (int v = 0; v < 4; ++v)
         red[v * N4_SS + (wave * 16 + b) * N4_RP + 4 * ug + q] = acc[ug][v];
   }
-  store_small_layers(sl, tid, ws, bs);
+  store_small_layers<TRAIN>(sl, tid, ws, wsT, bs);
   __syncthreads();
 
   // every thread adds a quarter of the (wave, block) sums of one output, in
@@ -410,7 +435,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
     const int s = tid >> 5, j = tid & 31;
     z1 = (psum[0][s][j] + psum[1][s][j]) + (psum[2][s][j] + psum[3][s][j]);
   }
-  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, bs);
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, bs);
 }
 
 // Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the whole
