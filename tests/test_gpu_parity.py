@@ -76,6 +76,28 @@ def test_small_trajectory(dims, acts, batch, shards, eta):
     _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 3)
 
 
+# the narrow kernels' edges: batches around the 4- and 16-sample tiles and the
+# switch between them, input widths below, at and past one 64-input step and
+# one 128-input stage, and one to four layers after the input
+NARROW_EDGES = [
+    ((4, 3), ("sigmoid",), 1),
+    ((8, 32), ("tanh",), 2),
+    ((60, 7, 2), ("sigmoid", "tanh"), 3),
+    ((64, 32, 31, 1), ("gaussian", "tanh", "sigmoid"), 5),
+    ((68, 20, 20, 20, 20), ("tanh",), 17),
+    ((1028, 30, 10), ("sigmoid",), 2047),
+    ((132, 30, 10), ("sigmoid",), 2048),
+    ((256, 12, 10), ("tanh", "sigmoid"), 2049),
+    ((12, 32, 32, 32, 32), ("sigmoid",), 2064),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch", NARROW_EDGES)
+def test_narrow_edges(dims, acts, batch):
+    theta, X, Y = _problem(dims, 7 * sum(dims) + batch, batch * 2)
+    _compare_trajectory(dims, acts, theta, X, Y, batch, 1.0, 1, 2)
+
+
 RELU_SMALL = [
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 1, 0.2),
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 4, 0.2),
