@@ -163,7 +163,8 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
   hipError_t e = hipMalloc(&buf, (size_t)total * n->esz);
   if (e != hipSuccess) {
     (void)hipGetLastError();
-    return fail(NF_ENOMEM, "hipMalloc of the workspace failed: " + std::string(hipGetErrorString(e)));
+    return fail(NF_ENOMEM,
+                "hipMalloc of the workspace failed: " + std::string(hipGetErrorString(e)));
   }
   e = hipMemset(buf, 0, (size_t)total * n->esz);  // pitch padding must read as zero
   if (e != hipSuccess) {
@@ -1122,7 +1123,8 @@ nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_
                          int64_t batch, float eta, int32_t n_shards, void* stream) {
   return train_epoch<float>(net, d_x, d_y, n_samples, batch, (double)eta, n_shards, stream);
 }
-nf_status nf_train_single(nf_net* net, const float* d_x, const float* d_y, float eta, void* stream) {
+nf_status nf_train_single(nf_net* net, const float* d_x, const float* d_y, float eta,
+                          void* stream) {
   return train_batch<float>(net, d_x, d_y, 1, (double)eta, 1, stream);
 }
 nf_status nf_train_windows(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
@@ -1220,7 +1222,9 @@ nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t
     }
     clear_recs(net);
     std::sort(agg.begin(), agg.end(),
-              [](const nf_kernel_stat& a, const nf_kernel_stat& b) { return a.total_ms > b.total_ms; });
+              [](const nf_kernel_stat& a, const nf_kernel_stat& b) {
+                return a.total_ms > b.total_ms;
+              });
     const int32_t n = (int32_t)std::min<size_t>(agg.size(), (size_t)cap);
     for (int32_t i = 0; i < n; ++i) out[i] = agg[i];
     *count = n;

@@ -40,7 +40,9 @@ struct Mma<float> {
   }
   __device__ static __forceinline__ int a_row(int l) { return l & 31; }
   __device__ static __forceinline__ int k_of(int l) { return l >> 5; }
-  __device__ static __forceinline__ int row(int v, int l) { return 8 * (v >> 2) + 4 * (l >> 5) + (v & 3); }
+  __device__ static __forceinline__ int row(int v, int l) {
+    return 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+  }
   __device__ static __forceinline__ int col(int l) { return l & 31; }
 };
 
@@ -254,7 +256,8 @@ gemm_kernel(const GemmParamsT<T> p) {
       const int n = n0 + wn + j * MM::BLK + MM::col(lane);
       if (n >= p.N) continue;
       T bn = T(0);
-      if constexpr (EPI == EPI_FWD_STASH || EPI == EPI_FWD_DELTA || EPI == EPI_FWD_OUT) bn = p.bias[n];
+      if constexpr (EPI == EPI_FWD_STASH || EPI == EPI_FWD_DELTA || EPI == EPI_FWD_OUT)
+        bn = p.bias[n];
 #pragma unroll
       for (int v = 0; v < MM::NACC; ++v) {
         const int m = m0 + wm + i * MM::BLK + MM::row(v, lane);
@@ -375,7 +378,8 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
   if (tile == TILE_128x128)
     return dispatch_tile<T, 128, 128, 16, 64, WN128>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
                                                      nsplit, p, s);
-  return dispatch_tile<T, 64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p, s);
+  return dispatch_tile<T, 64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p,
+                                              s);
 }
 
 template hipError_t launch_gemm<float>(int, int, bool, bool, bool, bool, int,

@@ -13,17 +13,16 @@
 // Kernel 2, tendencies of every layer (sections 3.3-3.5): workgroup
 //   (layer, 16-column tile, 16-unit half) forms the batch sum of delta (outer)
 //   activation for its block on the matrix cores (16x16x4), its 8 waves
-//   splitting the batch and their sums added in wave order; it then stores the tendency and
-//   writes W' = W - (eta/B) G itself (into the other parameter buffer), so no
-//   workgroup waits on another.  The order of every sum is fixed, so results
-//   are reproducible bit for bit.
+//   splitting the batch and their sums added in wave order; it then stores
+//   the tendency and writes W' = W - (eta/B) G itself (into the other
+//   parameter buffer), so no workgroup waits on another.
+// The order of every sum is fixed, so results are reproducible bit for bit.
 #include "nf_act.h"
 #include "nf_internal.h"
 
 namespace nf {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 // v if c, else zeros; written per component (a conditional on the vector
 // type itself is lowered through private memory)
@@ -535,7 +534,8 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
 #pragma unroll
     for (int w = 0; w < N2_WAVES; ++w)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
+      for (int q = 0; q < 4; ++q)
+        gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
     gb[u0 + tid] = gsum;
     bias[u0 + tid] = fmaf(-p.scale, gsum, b_old);
   }
