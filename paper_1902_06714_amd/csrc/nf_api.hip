@@ -63,6 +63,7 @@ constexpr int dtype_of() {
 
 struct nf_net {
   int device = 0;
+  int ncu = 0;                 // compute units of the device
   int dtype = nf::DT_F32;
   size_t esz = sizeof(float);  // bytes per element
   std::vector<int> dims;
@@ -466,6 +467,7 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
   }
   p.dout = n->dims[L];
   p.out = out;
+  p.ncu = n->ncu;
   return p;
 }
 
@@ -497,7 +499,7 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
   narrow_fwd_work(n, batch, true, &by, &fl);
   const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, y, batch, nullptr);
   nf_status st =
-      timed(n, nf::narrow_fwd_name(true, (int)batch), by, fl, s,
+      timed(n, nf::narrow_fwd_name(true, fp), by, fl, s,
             [&] { return nf::launch_narrow_fwd(true, fp, s); });
   if (st != NF_OK) return st;
 
@@ -570,7 +572,7 @@ nf_status infer(nf_net* n, const T* x, int64_t batch, T* out, hipStream_t s) {
       double by, fl;
       narrow_fwd_work(n, batch, false, &by, &fl);
       const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
-      return timed(n, nf::narrow_fwd_name(false, (int)batch), by, fl, s,
+      return timed(n, nf::narrow_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow_fwd(false, fp, s); });
     }
   }
@@ -642,8 +644,15 @@ nf_status create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32
     (void)hipGetLastError();
     return hip_fail(e, "no usable HIP device");
   }
+  int ncu = 0;
+  e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return hip_fail(e, "hipDeviceGetAttribute");
+  }
   nf_net* n = new nf_net();
   n->device = dev;
+  n->ncu = ncu;
   n->dtype = dtype == NF_F64 ? nf::DT_F64 : nf::DT_F32;
   n->esz = dtype == NF_F64 ? sizeof(double) : sizeof(float);
   n->dims.assign(dims, dims + n_dims);

@@ -105,6 +105,7 @@ struct NarrowFwdParams {
   float* A[NARROW_MAX_LAYERS];             // f(z_l) [B][32], l = 1..L-1
   float* D[NARROW_MAX_LAYERS];             // delta_l [B][32], l = 1..L
   float* out;                              // inference: f(z_L) [B][d_L]
+  int ncu;                                 // compute units of the device
 };
 
 struct NarrowDwParams {
@@ -126,9 +127,13 @@ struct NarrowDwParams {
   float scale;
 };
 
+// The per-sample kernels: 4-sample tiles (batches up to NARROW_SMALL_BATCH),
+// 16-sample tiles, and the persistent inference kernel (larger batches).
+enum NarrowKernel : int { NK_FWD4 = 0, NK_FWD16 = 1, NK_INFER = 2 };
+NarrowKernel narrow_fwd_kernel(bool train, const NarrowFwdParams& p);
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s);
-// Name of the per-sample kernel launch_narrow_fwd picks for this batch.
-const char* narrow_fwd_name(bool train, int batch);
+// Name of the kernel launch_narrow_fwd picks for this pass.
+const char* narrow_fwd_name(bool train, const NarrowFwdParams& p);
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 
 // Adds to *count the number of rows s < n for which out[s][0..d) and

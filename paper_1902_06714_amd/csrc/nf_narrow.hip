@@ -38,10 +38,11 @@ constexpr int N1_KP = N1_KC + 4;      // padded LDS row
 constexpr int N1_PRE_TRAIN = 8;
 constexpr int N1_PRE_INFER = 4;
 
-// The weights of layers 2..L and every bias, staged in LDS by every tile
-// (the per-sample threads read them again and again).  Each thread loads its
-// share into registers before layer 1 and stores it to LDS afterwards, so the
-// loads land while layer 1 runs.
+// The weights of layers 2..L, staged in LDS by every tile (the per-sample
+// threads read them again and again), and every layer's bias for unit tid % 32
+// (the unit the thread handles in the tail, so the biases stay in registers).
+// Each thread loads its share before layer 1 and stores the weights to LDS
+// afterwards, so the loads land while layer 1 runs.
 constexpr int NSTAGE = NARROW_WIDTH * NARROW_WIDTH / (N1_WAVES * 64);
 static_assert(NARROW_WIDTH * NARROW_WIDTH % (N1_WAVES * 64) == 0, "staging split");
 
@@ -74,8 +75,7 @@ constexpr int NWP = NARROW_WIDTH + 4;
 template <bool TRANSPOSED>
 __device__ __forceinline__ void store_small_layers(const SmallLayers& r, int tid,
                                                    float (*ws)[NARROW_WIDTH][NWP],
-                                                   float (*wsT)[NARROW_WIDTH][NWP],
-                                                   float (*bs)[NARROW_WIDTH]) {
+                                                   float (*wsT)[NARROW_WIDTH][NWP]) {
   constexpr int NW = NARROW_WIDTH;
 #pragma unroll
   for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
@@ -85,10 +85,6 @@ __device__ __forceinline__ void store_small_layers(const SmallLayers& r, int tid
       ws[li][e / NW][e % NW] = r.w[li][u];
       if (TRANSPOSED) wsT[li][e % NW][e / NW] = r.w[li][u];
     }
-  if (tid < NW) {
-#pragma unroll
-    for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bs[l][tid] = r.b[l];
-  }
 }
 
 // sum over i < 32 of w[i] h[i] from two 16-byte aligned LDS rows, in four
@@ -125,12 +121,14 @@ __device__ __forceinline__ float load_target(const NarrowFwdParams& p, int s0, i
 // zeros, so every sum runs over 32), the output delta (a_L - y) f'(z_L) and
 // the hidden deltas (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with
 // f'(z_l) kept in registers.  Threads past 32 T only join the barriers.
-template <bool TRAIN, int T>
+// Inference writes f(z_L) to the output, or with STAGED to ostage[s][j] in LDS.
+template <bool TRAIN, int T, bool STAGED = false>
 __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, int tid, float z1,
                                             float ytg, float (*hs)[T][NWP],
                                             const float (*ws)[NARROW_WIDTH][NWP],
                                             const float (*wsT)[NARROW_WIDTH][NWP],
-                                            const float (*bs)[NARROW_WIDTH]) {
+                                            const float (&bias)[NARROW_MAX_LAYERS],
+                                            float (*ostage)[NARROW_WIDTH] = nullptr) {
   constexpr int NW = NARROW_WIDTH;
   const bool active = tid < T * NW;
   const int s = active ? tid >> 5 : 0, j = tid & 31;
@@ -142,12 +140,14 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
   int cur = 0;
   if (active) {
     float a = 0.0f, f = 0.0f;
-    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bs[0][j], a, f);
+    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bias[0], a, f);
     fp[0] = f;
     if (p.L == 1) {
       if (TRAIN) {
         const float d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0f;
         if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
+      } else if (STAGED) {
+        ostage[s][j] = a;
       } else if (s_ok && j < p.dims[1]) {
         p.out[(int64_t)gs * p.dims[1] + j] = a;
       }
@@ -166,13 +166,15 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
       const int dl = p.dims[l];
       const float z = dot32(ws[l - 2][j], hs[cur][s]);
       float a = 0.0f, f = 0.0f;
-      if (j < dl) act_eval(p.acts[l - 1], z + bs[l - 1][j], a, f);
+      if (j < dl) act_eval(p.acts[l - 1], z + bias[l - 1], a, f);
       fp[l - 1] = f;
       if (l == p.L) {
         if (TRAIN) {
           const float d = (j < dl && s_ok) ? (a - ytg) * f : 0.0f;
           hs[cur ^ 1][s][j] = d;
           if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+        } else if (STAGED) {
+          ostage[s][j] = a;
         } else if (s_ok && j < dl) {
           p.out[(int64_t)gs * dl + j] = a;
         }
@@ -219,7 +221,6 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
   __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];   // activations, then deltas
   __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];  // W_2 .. W_L
   __shared__ __attribute__((aligned(16))) float wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][NWP];
-  __shared__ float bs[NARROW_MAX_LAYERS][NW];                // b_1 .. b_L
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -302,7 +303,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
       zp[wave][4 * g + v][16 + r] = acc1[v];
     }
   }
-  store_small_layers<TRAIN>(sl, tid, ws, wsT, bs);
+  store_small_layers<TRAIN>(sl, tid, ws, wsT);
   __syncthreads();
 
   // z_1 of (sample tid / 32, unit tid % 32): the waves' sums in wave order
@@ -313,7 +314,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd16_kernel(const Narro
 #pragma unroll
     for (int w = 1; w < N1_WAVES; ++w) z1 += zp[w][s][j];
   }
-  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, bs);
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, sl.b);
 }
 
 // ---------------------------------------------------------------------------
@@ -346,7 +347,6 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
   __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];
   __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];
   __shared__ __attribute__((aligned(16))) float wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][NWP];
-  __shared__ float bs[NARROW_MAX_LAYERS][NW];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -415,7 +415,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
       for (int v = 0; v < 4; ++v)
         red[v * N4_SS + (wave * 16 + b) * N4_RP + 4 * ug + q] = acc[ug][v];
   }
-  store_small_layers<TRAIN>(sl, tid, ws, wsT, bs);
+  store_small_layers<TRAIN>(sl, tid, ws, wsT);
   __syncthreads();
 
   // every thread adds a quarter of the (wave, block) sums of one output, in
@@ -434,7 +434,168 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
     const int s = tid >> 5, j = tid & 31;
     z1 = (psum[0][s][j] + psum[1][s][j]) + (psum[2][s][j] + psum[3][s][j]);
   }
-  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, bs);
+  narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, sl.b);
+}
+
+// ---------------------------------------------------------------------------
+// Inference over large batches.  One persistent workgroup per CU walks a
+// contiguous run of 16-sample tiles.  W_1 stays in registers for the whole
+// launch (wave w holds the 16-wide input chunks w, w + 8, ... of all 32 units),
+// so a CU reads it once instead of once per tile, and the inputs of the tile
+// two ahead are requested before the matrix work of the current one.  The
+// inputs are read through a buffer resource: rows past the batch and inputs
+// past the width come back as zeros without touching memory, so every load is
+// unconditional.  The waves' layer-1 sums are added in wave order and the tail
+// is that of the per-sample kernels, its outputs staged in LDS and written out
+// once per round of tiles: a global store inside the tile loop would make the
+// compiler wait for every outstanding load at the next use (stores and loads
+// share one wait counter), draining the loads of the tiles ahead.
+// ---------------------------------------------------------------------------
+constexpr int NI_CH = 16;                  // inputs per chunk: a float4 per lane group
+constexpr int NI_SLOTS = 3;                // tiles of inputs held: the current one + two ahead
+constexpr int NI_ROUND = 5 * NI_SLOTS;     // tiles whose outputs are staged in LDS
+constexpr unsigned NI_OOB = 0x40000000u;   // an offset past every input range
+
+template <int MC>
+__global__ void __launch_bounds__(N1_WAVES * 64) narrow_infer_kernel(const NarrowFwdParams p) {
+  constexpr int T = NARROW_TILE;
+  constexpr int NW = NARROW_WIDTH;
+  __shared__ float zp[N1_WAVES][T][NW + 1];                   // the waves' layer-1 sums
+  __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];
+  __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];
+  __shared__ float ob[NI_ROUND * T][NW];                      // f(z_L) of a round's samples
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, g = lane >> 4;
+
+  // this workgroup's tiles [t0, t1): a contiguous, balanced share
+  const int ntiles = (p.B + T - 1) / T;
+  const int t0 = (int)((int64_t)blockIdx.x * ntiles / gridDim.x);
+  const int t1 = (int)((int64_t)(blockIdx.x + 1) * ntiles / gridDim.x);
+  const int nt = t1 - t0;
+  const int nch = (p.d0 + NI_CH - 1) / NI_CH;
+  // chunks of this wave: MC or MC - 1 (MC is the launch's ceil(nch / 8))
+  const bool last_mine = (wave + N1_WAVES * (MC - 1)) < nch;
+
+  SmallLayers sl;
+  load_small_layers(p, tid, sl);
+
+  // lane (r, g) feeds sample r and units r, 16 + r with inputs 16 c + 4 g ..
+  // 16 c + 4 g + 3 of chunk c = wave + 8 i, one per MFMA (as in the 16-sample
+  // kernel).  W_1 and the inputs are read through buffer resources.  Chunks
+  // i < MC - 1 lie wholly inside the input width (byte offset kofs + 512 i);
+  // the last one may be partial or absent, and its inputs past the width are
+  // read at an offset past the buffers.
+  const unsigned kofs = 4u * (unsigned)(wave * NI_CH + 4 * g);
+  const int klast = (wave + N1_WAVES * (MC - 1)) * NI_CH + 4 * g;
+  const unsigned kofs_last = klast < p.d0 ? 4u * (unsigned)klast : NI_OOB;
+  auto koff = [&](int i) {
+    return i < MC - 1 ? kofs + 4u * N1_WAVES * NI_CH * i : kofs_last;
+  };
+  const unsigned wrow = 4u * (unsigned)(r * p.ldw[0]);
+  const unsigned whalf = 4u * (unsigned)(16 * p.ldw[0]);
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)p.W[0], (short)0, (int)(4 * NW * p.ldw[0]), 0x00020000);
+  float4 wlo[MC], whi[MC];
+#pragma unroll
+  for (int i = 0; i < MC; ++i) {
+    wlo[i] = __builtin_bit_cast(
+        float4, __builtin_amdgcn_raw_buffer_load_b128(wres, wrow + koff(i), 0, 0));
+    whi[i] = __builtin_bit_cast(
+        float4, __builtin_amdgcn_raw_buffer_load_b128(wres, wrow + whalf + koff(i), 0, 0));
+  }
+
+  // the rows of this workgroup's tiles (fewer than NI_OOB bytes: the host
+  // picks another kernel otherwise)
+  const int row0 = t0 * T;
+  const int nrows = (p.B < t1 * T ? p.B : t1 * T) - row0;
+  const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.X + (int64_t)row0 * p.d0), (short)0, nrows * p.d0 * 4, 0x00020000);
+  auto load_tile = [&](float4(&dst)[MC], int tt) {
+    const unsigned roff = 4u * (unsigned)((tt * T + r) * p.d0);
+#pragma unroll
+    for (int i = 0; i < MC; ++i)
+      dst[i] = __builtin_bit_cast(
+          float4, __builtin_amdgcn_raw_buffer_load_b128(xres, roff + koff(i), 0, 0));
+  };
+
+  float4 x[NI_SLOTS][MC];
+  load_tile(x[0], 0);
+  load_tile(x[1], 1);
+  // every load of the prologue is issued before the first wait
+  __builtin_amdgcn_sched_barrier(0);
+  store_small_layers<false>(sl, tid, ws, ws);
+
+  // layer 1 of tile tt from its inputs xc, then the tail, whose outputs go to
+  // row block obi of the round's staging area
+  auto tile = [&](const float4(&xc)[MC], int tt, int obi) {
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < MC; ++i) {
+      if (i < MC - 1 || last_mine) {
+        const float4 v = xc[i];
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, wlo[i].x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, whi[i].x, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, wlo[i].y, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, whi[i].y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, wlo[i].z, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, whi[i].z, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, wlo[i].w, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, whi[i].w, acc1, 0, 0, 0);
+      }
+    }
+    // accumulator register v of lane (r, g): sample 4 g + v, unit r (+16)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      zp[wave][4 * g + v][r] = acc0[v];
+      zp[wave][4 * g + v][16 + r] = acc1[v];
+    }
+    __syncthreads();
+    // z_1 of (sample tid / 32, unit tid % 32): the waves' sums in wave order;
+    // the tail's first barrier comes before the next tile rewrites zp
+    const int s = tid >> 5, j = tid & 31;
+    float z1 = zp[0][s][j];
+#pragma unroll
+    for (int w = 1; w < N1_WAVES; ++w) z1 += zp[w][s][j];
+    narrow_tail<false, T, true>(p, (t0 + tt) * T, tid, z1, 0.0f, hs, ws, ws, sl.b,
+                                ob + obi * T);
+  };
+
+  // Tile tt is in slot tt % 3 (rounds are whole multiples of 3 tiles).  The
+  // loop runs whole groups of three tiles, each requesting the inputs of the
+  // tile two ahead before its matrix work (past the last tile: zeros, no
+  // traffic); the last one or two tiles follow the loop, their inputs already
+  // requested.  (With a loop exit or a guard inside the group the compiler
+  // could no longer tell which loads a use waits for, and would wait for all.)
+  for (int rb = 0; rb < nt; rb += NI_ROUND) {
+    const int rn = nt - rb < NI_ROUND ? nt - rb : NI_ROUND;
+    int tb = 0;
+    for (; tb + NI_SLOTS <= rn; tb += NI_SLOTS) {
+      load_tile(x[2], rb + tb + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      tile(x[0], rb + tb, tb);
+      load_tile(x[0], rb + tb + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      tile(x[1], rb + tb + 1, tb + 1);
+      load_tile(x[1], rb + tb + 4);
+      __builtin_amdgcn_sched_barrier(0);
+      tile(x[2], rb + tb + 2, tb + 2);
+    }
+    if (tb < rn) tile(x[0], rb + tb, tb);
+    if (tb + 1 < rn) tile(x[1], rb + tb + 1, tb + 1);
+    // the round's outputs, rows [(t0 + rb) T, ..) of out [B][d_L], contiguous;
+    // the tail ended on a barrier, and the next round's first barrier comes
+    // before ob is written again
+    const int d = p.dout;
+    const int rs = (t0 + rb) * T;
+    const int re = (t0 + rb + rn) * T < p.B ? (t0 + rb + rn) * T : p.B;
+    float* o = p.out + (int64_t)rs * d;
+    for (int e = tid; e < (re - rs) * d; e += N1_WAVES * 64) o[e] = ob[e / d][e % d];
+    // let the stores drain here, once per round, so that the loads of the
+    // next round are tracked on their own
+    __builtin_amdgcn_s_waitcnt(0);
+  }
 }
 
 // Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the whole
@@ -541,26 +702,74 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   }
 }
 
+// The per-sample kernel for this pass: inference over batches above
+// NARROW_SMALL_BATCH takes the persistent kernel when W_1 fits its registers
+// (d0 <= 8 waves x NI_MC_MAX chunks x 16 = 896; eight chunks per wave would
+// spill) and every workgroup's input rows fit below NI_OOB bytes.
+constexpr int NI_MC_MAX = 7;
+
+int narrow_infer_grid(const NarrowFwdParams& p) {
+  const int ntiles = (p.B + NARROW_TILE - 1) / NARROW_TILE;
+  return ntiles < p.ncu ? ntiles : p.ncu;
+}
+
+NarrowKernel narrow_fwd_kernel(bool train, const NarrowFwdParams& p) {
+  if (p.B <= NARROW_SMALL_BATCH) return NK_FWD4;
+  if (!train && p.ncu > 0 && p.d0 <= N1_WAVES * NI_MC_MAX * NI_CH) {
+    const int64_t ntiles = (p.B + NARROW_TILE - 1) / NARROW_TILE;
+    const int64_t grid = narrow_infer_grid(p);
+    const int64_t rows = (ntiles + grid - 1) / grid * NARROW_TILE;
+    if (rows * p.d0 * 4 < (int64_t)NI_OOB) return NK_INFER;
+  }
+  return NK_FWD16;
+}
+
 hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s) {
-  if (p.B <= NARROW_SMALL_BATCH) {
-    const dim3 grid((p.B + N4_T - 1) / N4_T);
-    if (train)
-      narrow_fwd4_kernel<true><<<grid, N1_WAVES * 64, 0, s>>>(p);
-    else
-      narrow_fwd4_kernel<false><<<grid, N1_WAVES * 64, 0, s>>>(p);
-  } else {
-    const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
-    if (train)
-      narrow_fwd16_kernel<true, N1_PRE_TRAIN><<<grid, N1_WAVES * 64, 0, s>>>(p);
-    else
-      narrow_fwd16_kernel<false, N1_PRE_INFER><<<grid, N1_WAVES * 64, 0, s>>>(p);
+  const dim3 block(N1_WAVES * 64);
+  switch (narrow_fwd_kernel(train, p)) {
+    case NK_FWD4: {
+      const dim3 grid((p.B + N4_T - 1) / N4_T);
+      if (train)
+        narrow_fwd4_kernel<true><<<grid, block, 0, s>>>(p);
+      else
+        narrow_fwd4_kernel<false><<<grid, block, 0, s>>>(p);
+      break;
+    }
+    case NK_FWD16: {
+      const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
+      if (train)
+        narrow_fwd16_kernel<true, N1_PRE_TRAIN><<<grid, block, 0, s>>>(p);
+      else
+        narrow_fwd16_kernel<false, N1_PRE_INFER><<<grid, block, 0, s>>>(p);
+      break;
+    }
+    case NK_INFER: {
+      const dim3 grid(narrow_infer_grid(p));
+      // chunks per wave
+      switch (((p.d0 + NI_CH - 1) / NI_CH + N1_WAVES - 1) / N1_WAVES) {
+        case 1: narrow_infer_kernel<1><<<grid, block, 0, s>>>(p); break;
+        case 2: narrow_infer_kernel<2><<<grid, block, 0, s>>>(p); break;
+        case 3: narrow_infer_kernel<3><<<grid, block, 0, s>>>(p); break;
+        case 4: narrow_infer_kernel<4><<<grid, block, 0, s>>>(p); break;
+        case 5: narrow_infer_kernel<5><<<grid, block, 0, s>>>(p); break;
+        case 6: narrow_infer_kernel<6><<<grid, block, 0, s>>>(p); break;
+        default: narrow_infer_kernel<NI_MC_MAX><<<grid, block, 0, s>>>(p); break;
+      }
+      break;
+    }
   }
   return hipGetLastError();
 }
 
-const char* narrow_fwd_name(bool train, int batch) {
-  if (batch <= NARROW_SMALL_BATCH) return train ? "narrow_fwd4_train" : "narrow_fwd4_infer";
-  return train ? "narrow_fwd16_train" : "narrow_fwd16_infer";
+const char* narrow_fwd_name(bool train, const NarrowFwdParams& p) {
+  switch (narrow_fwd_kernel(train, p)) {
+    case NK_FWD4:
+      return train ? "narrow_fwd4_train" : "narrow_fwd4_infer";
+    case NK_FWD16:
+      return train ? "narrow_fwd16_train" : "narrow_fwd16_infer";
+    default:
+      return "narrow_infer";
+  }
 }
 
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s) {

@@ -178,6 +178,14 @@ def test_hand_worked_networks_on_gpu():
     ((784, 30, 10), ("sigmoid",), 5001),     # 16-sample tiles, ragged last tile
     ((36, 20, 7), ("tanh", "sigmoid"), 3),
     ((5, 300, 2), ("step", "sigmoid"), 1000),
+    # narrow inference past 2048 samples: persistent workgroups holding W_1
+    ((40, 17, 9, 5), ("tanh", "sigmoid", "gaussian"), 4100),   # width 2.5 chunks
+    ((4, 3), ("tanh",), 3000),                                 # one partial chunk
+    ((896, 32), ("sigmoid",), 3000),                           # widest input held, one layer
+    ((128, 32, 32, 32, 10), ("tanh", "relu", "gaussian", "sigmoid"), 2049),  # 1-sample tail
+    ((784, 30, 10), ("sigmoid",), 65541),    # 16 or 17 tiles per workgroup: 1 or 2 after the loop
+    ((784, 30, 10), ("sigmoid",), 70001),    # 17 or 18 tiles per workgroup
+    ((900, 30, 10), ("sigmoid",), 3000),     # input too wide to hold: 16-sample tiles
 ])
 def test_inference_matches_reference(dims, acts, n):
     theta, X, _ = _problem(dims, 77, n, x_lo=-1.0)
