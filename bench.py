@@ -217,26 +217,35 @@ def main(argv=None) -> int:
         print(f"[kernel] {k['name']:<28} launches {k['launches']:>6}  avg {avg * 1e3:9.2f} us  "
               f"total {k['total_ms']:9.3f} ms  {k['bytes'] / k['launches'] / 1e6:11.6f} MB/launch  "
               f"{k['flops'] / k['launches'] / 1e9:9.4f} GFLOP/launch", file=sys.stderr)
-    dom = stats[0]
-    avg_s = dom["total_ms"] / dom["launches"] / 1e3
-    bytes_l = dom["bytes"] / dom["launches"]
-    flops_l = dom["flops"] / dom["launches"]
     sha = kernel_sources_sha()
     mfma_peak = FP64_MFMA_PEAK_TFS if f64 else FP32_MFMA_PEAK_TFS
     ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)   # flop per byte
-    if flops_l / bytes_l < ridge:
-        achieved = bytes_l / avg_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS}
-    else:
-        achieved = flops_l / avg_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
-                "unit": "TFLOP/s", "frac": achieved / mfma_peak}
-    roof["traffic"] = read_traffic(dom["name"], w.name + ("_f64" if f64 else ""), sha)
-    roof["kernel"] = dom["name"]
-    roof["avg_us"] = avg_s * 1e6
-    roof["bytes_per_launch"] = bytes_l
-    roof["flops_per_launch"] = flops_l
+
+    def roofline(k):
+        """Roofline of one timed kernel: algorithmic bytes or flops per launch
+        over its average launch time, against the resource that bounds it."""
+        avg_s = k["total_ms"] / k["launches"] / 1e3
+        bytes_l = k["bytes"] / k["launches"]
+        flops_l = k["flops"] / k["launches"]
+        if flops_l / bytes_l < ridge:
+            achieved = bytes_l / avg_s / 1e9
+            r = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                 "frac": achieved / HBM_PEAK_GBS}
+        else:
+            achieved = flops_l / avg_s / 1e12
+            r = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
+                 "unit": "TFLOP/s", "frac": achieved / mfma_peak}
+        r["traffic"] = read_traffic(k["name"], w.name + ("_f64" if f64 else ""), sha)
+        r["kernel"] = k["name"]
+        r["avg_us"] = avg_s * 1e6
+        r["launches_per_step"] = k["launches"]
+        r["bytes_per_launch"] = bytes_l
+        r["flops_per_launch"] = flops_l
+        return r
+
+    # the dominant kernel (most time per step), then every timed kernel
+    roof = roofline(stats[0])
+    kernels = [roofline(k) for k in stats]
 
     value = n_train * args.steps / (ms / 1e3)
     line = {
@@ -258,6 +267,7 @@ def main(argv=None) -> int:
                    "heldout_per_step": int(Xh.shape[0]) if Xh is not None else 0,
                    "shards": w.shards, "kernel_sources": sha},
         "roofline": roof,
+        "kernels": kernels,
         "params_finite": finite,
     }
     if args.cpu_seconds > 0:
