@@ -75,6 +75,13 @@ struct alignas(16) Vec16 {
 // KC: k is the contiguous index in memory (X[r*ld + k]), else X[k*ld + r].
 // VEC: rows are 16-byte aligned with a pitch that is a multiple of VW and the
 // pitch padding is zero, so aligned 16-byte loads are safe.
+// The loads go through a buffer resource based at the tile's first row (KC)
+// or the stage's first k (otherwise), so offsets stay small for any matrix;
+// elements outside the matrix or past the piece's k range are read at an
+// offset past the buffer, which returns zeros without a memory access.  So
+// every load is unconditional, stages past the end included.
+constexpr unsigned TILE_OOB = 0x7ffffff0u;   // the buffers' length in bytes
+
 template <class T, int R, int BK, int NT, bool KC, bool VEC>
 struct TileLoader {
   static constexpr int VW = Vec16<T>::N;
@@ -86,6 +93,10 @@ struct TileLoader {
 
   __device__ __forceinline__ void load(const T* __restrict__ X, int64_t ld, int rmax, int kend,
                                        int r0, int k0, int tid) {
+    const T* base = KC ? X + (int64_t)r0 * ld : X + (int64_t)k0 * ld;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)TILE_OOB, 0x00020000);
+    const int ldi = (int)ld;
     if constexpr (VEC) {
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
@@ -99,29 +110,29 @@ struct TileLoader {
           r = (q % (R / VW)) * VW;
         }
         const int gr = r0 + r, gk = k0 + k;
-        if (gr < rmax && gk < kend) {
-          const T* ptr = KC ? X + (int64_t)gr * ld + gk : X + (int64_t)gk * ld + gr;
-          v[i] = *reinterpret_cast<const Vec16<T>*>(ptr);
-        } else {
-#pragma unroll
-          for (int c = 0; c < VW; ++c) v[i].e[c] = T(0);
-        }
+        const int e = KC ? r * ldi + gk : k * ldi + gr;
+        const unsigned off = (gr < rmax && gk < kend) ? (unsigned)e * (unsigned)sizeof(T) : TILE_OOB;
+        v[i] = __builtin_bit_cast(Vec16<T>, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
       }
     } else {
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
-        const int e = tid + i * NT;
+        const int q = tid + i * NT;
         int r, k;
         if constexpr (KC) {
-          r = e / BK;
-          k = e % BK;
+          r = q / BK;
+          k = q % BK;
         } else {
-          k = e / R;
-          r = e % R;
+          k = q / R;
+          r = q % R;
         }
         const int gr = r0 + r, gk = k0 + k;
-        s[i] = (gr < rmax && gk < kend) ? (KC ? X[(int64_t)gr * ld + gk] : X[(int64_t)gk * ld + gr])
-                                        : T(0);
+        const int e = KC ? r * ldi + gk : k * ldi + gr;
+        const unsigned off = (gr < rmax && gk < kend) ? (unsigned)e * (unsigned)sizeof(T) : TILE_OOB;
+        if constexpr (sizeof(T) == 4)
+          s[i] = __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+        else
+          s[i] = __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
       }
     }
   }
@@ -161,8 +172,8 @@ struct TileLoader {
 // C[BM x BN] tile per workgroup; (BM/WM) x (BN/WN) waves, each owning a
 // WM x WN sub-tile made of BLK x BLK matrix-core blocks.  grid = (M tiles,
 // N tiles, pieces of the k range).
-template <class T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV,
-          int EPI>
+template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
+          bool BV, int EPI>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 gemm_kernel(const GemmParamsT<T> p) {
   using MM = Mma<T>;
@@ -191,9 +202,6 @@ gemm_kernel(const GemmParamsT<T> p) {
   }
   const bool do_bias = (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) && blockIdx.y == 0;
 
-  TileLoader<T, BM, BK, NT, AKC, AV> la;
-  TileLoader<T, BN, BK, NT, BKC, BV> lb;
-
   typename MM::acc_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -204,24 +212,28 @@ gemm_kernel(const GemmParamsT<T> p) {
   T bsum = T(0);
 
   const int ntiles = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-  if (ntiles > 0) {
-    la.load(p.A, p.lda, p.M, kend, m0, kbeg, tid);
-    lb.load(p.B, p.ldb, p.N, kend, n0, kbeg, tid);
-    la.store(As[0], tid);
-    lb.store(Bs[0], tid);
+
+  // PD register stages of the operand tiles are in flight: stage t + 1 goes
+  // to LDS while stage t is multiplied, and its registers then take stage
+  // t + 1 + PD.  Stage s is held by register set s % PD; after the prologue
+  // LDS holds stage 0, set k stage k (k >= 1) and set 0 stage PD.
+  TileLoader<T, BM, BK, NT, AKC, AV> la[PD];
+  TileLoader<T, BN, BK, NT, BKC, BV> lb[PD];
+#pragma unroll
+  for (int d = 0; d < PD; ++d) {
+    la[d].load(p.A, p.lda, p.M, kend, m0, kbeg + d * BK, tid);
+    lb[d].load(p.B, p.ldb, p.N, kend, n0, kbeg + d * BK, tid);
   }
+  la[0].store(As[0], tid);
+  lb[0].store(Bs[0], tid);
+  la[0].load(p.A, p.lda, p.M, kend, m0, kbeg + PD * BK, tid);
+  lb[0].load(p.B, p.ldb, p.N, kend, n0, kbeg + PD * BK, tid);
   __syncthreads();
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      const int kn = kbeg + (t + 1) * BK;
-      la.load(p.A, p.lda, p.M, kend, m0, kn, tid);
-      lb.load(p.B, p.ldb, p.N, kend, n0, kn, tid);
-    }
-    const T* a_s = As[buf];
-    const T* b_s = Bs[buf];
+  // the products of stage t, held in LDS buffer t & 1
+  auto multiply = [&](int t) {
+    const T* a_s = As[t & 1];
+    const T* b_s = Bs[t & 1];
 #pragma unroll
     for (int kk = 0; kk < BK; kk += MM::KS) {
       T av[TM], bv[TN];
@@ -240,11 +252,35 @@ gemm_kernel(const GemmParamsT<T> p) {
 #pragma unroll
       for (int kk = 0; kk < BK; ++kk) bsum += a_s[kk * SA + tid];
     }
-    if (more) {
-      la.store(As[buf ^ 1], tid);
-      lb.store(Bs[buf ^ 1], tid);
+  };
+
+  // Whole groups of PD stages, every load unconditional (past the last stage
+  // they read zeros): the compiler then waits for exactly the stage it needs.
+  // The last stages follow the loop; their inputs are already requested.
+  int t = 0;
+  for (; t + PD <= ntiles; t += PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      const int j = (d + 1) % PD;
+      multiply(t + d);
+      la[j].store(As[(t + d + 1) & 1], tid);
+      lb[j].store(Bs[(t + d + 1) & 1], tid);
+      la[j].load(p.A, p.lda, p.M, kend, m0, kbeg + (t + d + 1 + PD) * BK, tid);
+      lb[j].load(p.B, p.ldb, p.N, kend, n0, kbeg + (t + d + 1 + PD) * BK, tid);
+      __syncthreads();
     }
-    __syncthreads();
+  }
+#pragma unroll
+  for (int d = 0; d < PD - 1; ++d) {
+    if (t + d < ntiles) {
+      const int j = (d + 1) % PD;
+      multiply(t + d);
+      if (t + d + 1 < ntiles) {
+        la[j].store(As[(t + d + 1) & 1], tid);
+        lb[j].store(Bs[(t + d + 1) & 1], tid);
+      }
+      __syncthreads();
+    }
   }
 
   // Epilogue: accumulator register v of this lane holds row MM::row(v, lane)
@@ -335,21 +371,21 @@ __global__ void fold_sgd_kernel(const T* __restrict__ partial, int64_t pstride,
   }
 }
 
-template <class T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, bool AV, bool BV,
-          int EPI>
+template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
+          bool BV, int EPI>
 static hipError_t launch_one(int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, nsplit);
-  gemm_kernel<T, BM, BN, BK, WM, WN, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
+  gemm_kernel<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
   return hipGetLastError();
 }
 
-template <class T, int BM, int BN, int BK, int WM, int WN>
+template <class T, int BM, int BN, int BK, int WM, int WN, int PD>
 static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
                                 const GemmParamsT<T>& p, hipStream_t s) {
 #define NF_CASE(AKC, BKC, AV, BV, E)                                     \
   if (akc == AKC && bkc == BKC && av == AV && bv == BV && epi == E)      \
-    return launch_one<T, BM, BN, BK, WM, WN, AKC, BKC, AV, BV, E>(nsplit, p, s);
+    return launch_one<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, E>(nsplit, p, s);
   // forward: A = activations [m][k], B(k, n) = W[n][k]
   NF_CASE(true, true, true, true, EPI_FWD_STASH)
   NF_CASE(true, true, false, true, EPI_FWD_STASH)
@@ -373,13 +409,20 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
                        int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
   // fp64 accumulators take twice the registers: its 128 x 128 tile uses 8
-  // waves of 64 x 32 instead of 4 of 64 x 64
+  // waves of 64 x 32 instead of 4 of 64 x 64.  Stages in flight: the small
+  // tile's few products per stage need more of them to cover the memory
+  // latency.
   constexpr int WN128 = sizeof(T) == 8 ? 32 : 64;
+  constexpr int PD128 = 4;
+  constexpr int PD64 = sizeof(T) == 8 ? 4 : 8;
+  // element offsets inside one buffer-based tile stay below TILE_OOB bytes
+  if ((int64_t)128 * (p.lda > p.ldb ? p.lda : p.ldb) * (int64_t)sizeof(T) >= (int64_t)TILE_OOB)
+    return hipErrorInvalidValue;
   if (tile == TILE_128x128)
-    return dispatch_tile<T, 128, 128, 16, 64, WN128>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
-                                                     nsplit, p, s);
-  return dispatch_tile<T, 64, 64, 16, 32, 32>(epi, a_kcontig, b_kcontig, a_vec, b_vec, nsplit, p,
-                                              s);
+    return dispatch_tile<T, 128, 128, 16, 64, WN128, PD128>(epi, a_kcontig, b_kcontig, a_vec,
+                                                            b_vec, nsplit, p, s);
+  return dispatch_tile<T, 64, 64, 16, 32, 32, PD64>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
+                                                    nsplit, p, s);
 }
 
 template hipError_t launch_gemm<float>(int, int, bool, bool, bool, bool, int,
