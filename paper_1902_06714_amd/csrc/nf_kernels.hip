@@ -408,11 +408,11 @@ template <class T>
 hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec, bool b_vec,
                        int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
-  // fp64 accumulators take twice the registers: its 128 x 128 tile uses 8
-  // waves of 64 x 32 instead of 4 of 64 x 64.  Stages in flight: the small
-  // tile's few products per stage need more of them to cover the memory
-  // latency.
-  constexpr int WN128 = sizeof(T) == 8 ? 32 : 64;
+  // The 128 x 128 tile runs 8 waves of 64 x 32 (two per SIMD, so one
+  // wave's LDS reads and barrier waits overlap the other's matrix work).
+  // Stages in flight: the small tile's few products per stage need more of
+  // them to cover the memory latency.
+  constexpr int WN128 = 32;
   constexpr int PD128 = 4;
   constexpr int PD64 = sizeof(T) == 8 ? 4 : 8;
   // element offsets inside one buffer-based tile stay below TILE_OOB bytes
