@@ -88,7 +88,8 @@ struct nf_net {
   void* evalbuf = nullptr;
   int64_t eval_elems = 0;
   unsigned long long* dcount = nullptr;
-  // fp32 nets whose every layer after the input has at most NARROW_WIDTH units
+  // nets of at most NARROW_MAX_LAYERS layers whose every layer after the input
+  // has at most NARROW_WIDTH units
   bool narrow = false;
   // narrow nets: offset of a zero block (NARROW_WIDTH^2 weights, then
   // NARROW_WIDTH biases) that stands in for the layers past the last one
@@ -431,17 +432,22 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
 }
 
 // ---------------------------------------------------------------------------
-// narrow fp32 networks: the two-kernel step of csrc/nf_narrow.hip
+// narrow networks: the two-kernel step of csrc/nf_narrow.hip (fp32) and
+// csrc/nf_narrow64.hip (fp64)
 // ---------------------------------------------------------------------------
-bool narrow_ok(const nf_net* n, const float* x, int shards) {
-  return n->narrow && shards == 1 && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0]);
+// input rows must allow 16-byte loads: a width that is a multiple of
+// 16 / sizeof(T) elements and a 16-byte aligned base
+template <class T>
+bool narrow_rows_ok(const nf_net* n, const T* x) {
+  return n->narrow && n->dims[0] % (16 / (int)sizeof(T)) == 0 && vec_ok(x, n->dims[0]);
 }
 
-nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const float* y,
-                                      int64_t batch, float* out) {
-  nf::NarrowFwdParams p{};
+template <class T>
+nf::NarrowFwdParamsT<T> narrow_fwd_params(const nf_net* n, const T* x, const T* y, int64_t batch,
+                                          T* out) {
+  nf::NarrowFwdParamsT<T> p{};
   const int L = num_layers(n);
-  float* P = cur_params<float>(n);
+  T* P = cur_params<T>(n);
   p.X = x;
   p.Y = y;
   p.B = (int)batch;
@@ -456,8 +462,8 @@ nf::NarrowFwdParams narrow_fwd_params(const nf_net* n, const float* x, const flo
       p.W[l - 1] = P + ly.w_off;
       p.ldw[l - 1] = ly.ldw;
       p.bias[l - 1] = P + ly.b_off;
-      p.A[l - 1] = as<float>(n->actv[l]);
-      p.D[l - 1] = as<float>(n->dbuf[l]);
+      p.A[l - 1] = as<T>(n->actv[l]);
+      p.D[l - 1] = as<T>(n->dbuf[l]);
     } else {
       // zero weights and biases for the layers past the last one
       p.W[l - 1] = P + n->zero_off;
@@ -488,37 +494,42 @@ void narrow_fwd_work(const nf_net* n, int64_t B, bool train, double* bytes, doub
   } else {
     by += (double)B * n->dims[L];                       // outputs
   }
-  *bytes = 4.0 * by;
+  *bytes = (double)n->esz * by;
   *flops = fl;
 }
 
-nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t batch, double eta,
+template <class T>
+nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, double eta,
                             hipStream_t s) {
   const int L = num_layers(n);
   double by, fl;
   narrow_fwd_work(n, batch, true, &by, &fl);
-  const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, y, batch, nullptr);
-  nf_status st =
-      timed(n, nf::narrow_fwd_name(true, fp), by, fl, s,
-            [&] { return nf::launch_narrow_fwd(true, fp, s); });
+  const nf::NarrowFwdParamsT<T> fp = narrow_fwd_params<T>(n, x, y, batch, nullptr);
+  nf_status st;
+  if constexpr (sizeof(T) == 4)
+    st = timed(n, nf::narrow_fwd_name(true, fp), by, fl, s,
+               [&] { return nf::launch_narrow_fwd(true, fp, s); });
+  else
+    st = timed(n, "narrow64_fwd_train", by, fl, s,
+               [&] { return nf::launch_narrow64_fwd(true, fp, s); });
   if (st != NF_OK) return st;
 
-  float* P = cur_params<float>(n);
-  float* Q = next_params<float>(n);
-  float* G = as<float>(n->grads);
-  nf::NarrowDwParams dp{};
+  T* P = cur_params<T>(n);
+  T* Q = next_params<T>(n);
+  T* G = as<T>(n->grads);
+  nf::NarrowDwParamsT<T> dp{};
   dp.B = (int)batch;
   dp.L = L;
   dp.X = x;
-  dp.scale = (float)(eta / (double)batch);
+  dp.scale = (T)(eta / (double)batch);
   dp.dims[0] = n->dims[0];
   int base = 0;
   double dby = 0.0, dfl = 0.0;
   for (int l = 1; l <= L; ++l) {
     const LayerLayout& ly = n->layers[l];
     dp.dims[l] = ly.out;
-    dp.A[l - 1] = l < L ? as<float>(n->actv[l]) : nullptr;
-    dp.D[l - 1] = as<float>(n->dbuf[l]);
+    dp.A[l - 1] = l < L ? as<T>(n->actv[l]) : nullptr;
+    dp.D[l - 1] = as<T>(n->dbuf[l]);
     dp.Win[l - 1] = P + ly.w_off;
     dp.bin[l - 1] = P + ly.b_off;
     dp.W[l - 1] = Q + ly.w_off;
@@ -530,12 +541,16 @@ nf_status narrow_train_step(nf_net* n, const float* x, const float* y, int64_t b
     base += (ly.in + 15) / 16 * ((ly.out + 15) / 16);
     // deltas and previous activations read, tendencies written, parameters updated
     const double M = ly.out, N = ly.in;
-    dby += 4.0 * ((double)batch * (M + N) + 3 * M * N + 3 * M);
+    dby += (double)sizeof(T) * ((double)batch * (M + N) + 3 * M * N + 3 * M);
     dfl += 2.0 * batch * M * N;
   }
   for (int l = L; l <= nf::NARROW_MAX_LAYERS; ++l) dp.tile_base[l] = base;
   dp.ntiles = base;
-  return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
+  if constexpr (sizeof(T) == 4)
+    return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
+  else
+    return timed(n, "narrow64_dw_sgd", dby, dfl, s,
+                 [&] { return nf::launch_narrow64_dw(dp, s); });
 }
 
 // ---------------------------------------------------------------------------
@@ -545,14 +560,10 @@ template <class T>
 nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double eta, int shards,
                      hipStream_t s) {
   nf_status st;
-  bool done = false;
-  if constexpr (sizeof(T) == 4) {
-    if (narrow_ok(n, x, shards)) {
-      st = narrow_train_step(n, x, y, batch, eta, s);
-      done = true;
-    }
-  }
-  if (!done) {
+  const bool narrow = shards == 1 && narrow_rows_ok<T>(n, x);
+  if (narrow) {
+    st = narrow_train_step<T>(n, x, y, batch, eta, s);
+  } else {
     st = run_forward<T>(n, x, y, batch, nullptr, true, s);
     if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s);
   }
@@ -567,14 +578,16 @@ template <class T>
 nf_status infer(nf_net* n, const T* x, int64_t batch, T* out, hipStream_t s) {
   nf_status st = ensure_ws(n, batch);
   if (st != NF_OK) return st;
-  if constexpr (sizeof(T) == 4) {
-    if (n->narrow && n->dims[0] % 4 == 0 && vec_ok(x, n->dims[0])) {
-      double by, fl;
-      narrow_fwd_work(n, batch, false, &by, &fl);
-      const nf::NarrowFwdParams fp = narrow_fwd_params(n, x, nullptr, batch, out);
+  if (narrow_rows_ok<T>(n, x)) {
+    double by, fl;
+    narrow_fwd_work(n, batch, false, &by, &fl);
+    const nf::NarrowFwdParamsT<T> fp = narrow_fwd_params<T>(n, x, nullptr, batch, out);
+    if constexpr (sizeof(T) == 4)
       return timed(n, nf::narrow_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow_fwd(false, fp, s); });
-    }
+    else
+      return timed(n, "narrow64_fwd_infer", by, fl, s,
+                   [&] { return nf::launch_narrow64_fwd(false, fp, s); });
   }
   return run_forward<T>(n, x, nullptr, batch, out, false, s);
 }
@@ -657,7 +670,7 @@ nf_status create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32
   n->esz = dtype == NF_F64 ? sizeof(double) : sizeof(float);
   n->dims.assign(dims, dims + n_dims);
   n->layers.resize(n_dims);
-  n->narrow = n->dtype == nf::DT_F32 && n_dims - 1 <= nf::NARROW_MAX_LAYERS;
+  n->narrow = n_dims - 1 <= nf::NARROW_MAX_LAYERS;
   for (int l = 1; l < n_dims; ++l) n->narrow = n->narrow && dims[l] <= nf::NARROW_WIDTH;
   // Narrow nets pad every layer to NARROW_WIDTH rows and the layers after
   // the first to NARROW_WIDTH columns, so their kernels read whole padded

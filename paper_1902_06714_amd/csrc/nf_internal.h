@@ -92,40 +92,44 @@ constexpr int NARROW_SMALL_BATCH = 2048;
 // is [NARROW_WIDTH][NARROW_WIDTH]; biases are NARROW_WIDTH long; rows, columns
 // and entries past the layer sizes are zero.  The per-sample kernel reads the
 // layers past the last one (up to NARROW_MAX_LAYERS) from a zero block.
-struct NarrowFwdParams {
-  const float* X;                          // [B][d0], d0 % 4 == 0, 16-byte aligned
-  const float* Y;                          // [B][d_L] targets (training)
+template <class T>
+struct NarrowFwdParamsT {
+  const T* X;                              // [B][d0], d0 % (16 / sizeof(T)) == 0, 16-byte aligned
+  const T* Y;                              // [B][d_L] targets (training)
   int B, d0, L;
   int dout;                                // d_L
   int dims[NARROW_MAX_LAYERS + 1];
   int acts[NARROW_MAX_LAYERS];
-  const float* W[NARROW_MAX_LAYERS];       // W_l (index l-1), padded as above
+  const T* W[NARROW_MAX_LAYERS];           // W_l (index l-1), padded as above
   int64_t ldw[NARROW_MAX_LAYERS];
-  const float* bias[NARROW_MAX_LAYERS];
-  float* A[NARROW_MAX_LAYERS];             // f(z_l) [B][32], l = 1..L-1
-  float* D[NARROW_MAX_LAYERS];             // delta_l [B][32], l = 1..L
-  float* out;                              // inference: f(z_L) [B][d_L]
+  const T* bias[NARROW_MAX_LAYERS];
+  T* A[NARROW_MAX_LAYERS];                 // f(z_l) [B][32], l = 1..L-1
+  T* D[NARROW_MAX_LAYERS];                 // delta_l [B][32], l = 1..L
+  T* out;                                  // inference: f(z_L) [B][d_L]
   int ncu;                                 // compute units of the device
 };
+using NarrowFwdParams = NarrowFwdParamsT<float>;
 
-struct NarrowDwParams {
+template <class T>
+struct NarrowDwParamsT {
   int B, L;                                // batch, layers
   int dims[NARROW_MAX_LAYERS + 1];
-  const float* X;                          // layer-1 inputs [B][d0]
-  const float* A[NARROW_MAX_LAYERS];       // f(z_l) [B][32], l = 1..L-1
-  const float* D[NARROW_MAX_LAYERS];       // delta_l [B][32]
-  const float* Win[NARROW_MAX_LAYERS];     // parameters before the step
-  const float* bin[NARROW_MAX_LAYERS];
-  float* W[NARROW_MAX_LAYERS];             // parameters after the step
+  const T* X;                              // layer-1 inputs [B][d0]
+  const T* A[NARROW_MAX_LAYERS];           // f(z_l) [B][32], l = 1..L-1
+  const T* D[NARROW_MAX_LAYERS];           // delta_l [B][32]
+  const T* Win[NARROW_MAX_LAYERS];         // parameters before the step
+  const T* bin[NARROW_MAX_LAYERS];
+  T* W[NARROW_MAX_LAYERS];                 // parameters after the step
   int64_t ldw[NARROW_MAX_LAYERS];
-  float* bias[NARROW_MAX_LAYERS];
-  float* G[NARROW_MAX_LAYERS];             // tendencies, same layout as W / bias
-  float* gb[NARROW_MAX_LAYERS];
+  T* bias[NARROW_MAX_LAYERS];
+  T* G[NARROW_MAX_LAYERS];                 // tendencies, same layout as W / bias
+  T* gb[NARROW_MAX_LAYERS];
   int tile_base[NARROW_MAX_LAYERS + 1];    // first (16-column, 16-unit) tile of each layer;
                                            // ntiles for the layers past the last one
   int ntiles;                              // tiles of all layers
-  float scale;
+  T scale;
 };
+using NarrowDwParams = NarrowDwParamsT<float>;
 
 // The per-sample kernels: 4-sample tiles (batches up to NARROW_SMALL_BATCH),
 // 16-sample tiles, and the persistent inference kernel (larger batches).
@@ -135,6 +139,11 @@ hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s
 // Name of the kernel launch_narrow_fwd picks for this pass.
 const char* narrow_fwd_name(bool train, const NarrowFwdParams& p);
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
+
+// The fp64 counterparts (16-sample tiles for every batch; no persistent
+// inference kernel).  Input rows need an even width.
+hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hipStream_t s);
+hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s);
 
 // Adds to *count the number of rows s < n for which out[s][0..d) and
 // y[s][0..d) have their first largest entry at the same index (rows holding a

@@ -1,0 +1,334 @@
+// Training step and inference for narrow fp64 networks (the paper's real64
+// kind, section 2; every layer after the input has at most 32 units), on the
+// fp64 matrix cores (v_mfma_f64_16x16x4f64).  Two kernels per step, as in
+// fp32:
+//   per-sample pass   one workgroup of 8 waves per 16-sample tile: layer 1
+//                     with the input width split over the waves and their
+//                     sums added in wave order; layers 2..L, the output delta
+//                     (a_L - y) f'(z_L) and the hidden deltas
+//                     (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) one thread
+//                     per (sample, unit) with the small layers in LDS;
+//   tendencies + SGD  one workgroup per (layer, 16-column tile, 16-unit half)
+//                     forms the batch sum of delta (outer) activation for its
+//                     block, its waves splitting the batch and their sums
+//                     added in wave order, and writes W' = W - (eta/B) G into
+//                     the other parameter buffer (sections 3.3-3.5).
+// The fp64 matrix core takes 4 inputs per instruction with lane l supplying
+// row l % 16 and input l / 16 of A, input l / 16 and column l % 16 of B;
+// accumulator register v of lane l holds row 4 v + l / 16, column l % 16.
+// Every sum runs in a fixed order, so results are reproducible bit for bit.
+#include "nf_act.h"
+#include "nf_internal.h"
+
+namespace nf {
+
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+// v if c, else zeros, per component
+__device__ __forceinline__ double2 keep_if2(bool c, double2 v) {
+  return make_double2(c ? v.x : 0.0, c ? v.y : 0.0);
+}
+
+constexpr int D_WAVES = 8;
+constexpr int D_T = 16;                  // samples per tile
+constexpr int D_CH = 8;                  // inputs per chunk: a 16-byte pair per lane group
+constexpr int D_PRE = 4;                 // chunks per wave requested together
+constexpr int D_NWP = NARROW_WIDTH + 2;  // LDS row pitch (16-byte aligned rows)
+constexpr int D_NSTAGE = NARROW_WIDTH * NARROW_WIDTH / (D_WAVES * 64);
+
+// sum over i < 32 of w[i] h[i] from two 16-byte aligned LDS rows, in four
+// interleaved partial sums added pairwise
+__device__ __forceinline__ double dot32d(const double* w, const double* h) {
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int m = 0; m < NARROW_WIDTH / 4; ++m) {
+    const double2 a0 = *reinterpret_cast<const double2*>(w + 4 * m);
+    const double2 a1 = *reinterpret_cast<const double2*>(w + 4 * m + 2);
+    const double2 x0 = *reinterpret_cast<const double2*>(h + 4 * m);
+    const double2 x1 = *reinterpret_cast<const double2*>(h + 4 * m + 2);
+    acc[0] = fma(a0.x, x0.x, acc[0]);
+    acc[1] = fma(a0.y, x0.y, acc[1]);
+    acc[2] = fma(a1.x, x1.x, acc[2]);
+    acc[3] = fma(a1.y, x1.y, acc[3]);
+  }
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+}  // namespace
+
+template <bool TRAIN>
+__global__ void __launch_bounds__(D_WAVES * 64) narrow64_fwd_kernel(const NarrowFwdParamsT<double> p) {
+  constexpr int T = D_T;
+  constexpr int NW = NARROW_WIDTH;
+  __shared__ double zp[D_WAVES][T][NW + 1];                         // the waves' layer-1 sums
+  __shared__ __attribute__((aligned(16))) double hs[2][T][D_NWP];   // activations, then deltas
+  __shared__ __attribute__((aligned(16))) double ws[NARROW_MAX_LAYERS - 1][NW][D_NWP];
+  __shared__ __attribute__((aligned(16))) double wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][D_NWP];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int s0 = blockIdx.x * T;
+
+  // the weights of layers 2..L (padded 32 x 32 blocks, a zero block past the
+  // last layer) for LDS, and the biases of unit tid % 32 (the unit this
+  // thread takes in the tail)
+  double wsm[NARROW_MAX_LAYERS - 1][D_NSTAGE], bias[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < D_NSTAGE; ++u) wsm[li][u] = p.W[li + 1][tid + u * D_WAVES * 64];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bias[l] = p.bias[l][tid & (NW - 1)];
+  // target of (sample tid / 32, unit tid % 32), read from a clamped position
+  double ytg = 0.0;
+  if (TRAIN) {
+    const int ys = s0 + (tid >> 5), yu = tid & 31;
+    const int yr = ys < p.B ? ys : p.B - 1, yc = yu < p.dout ? yu : p.dout - 1;
+    const double v = p.Y[(int64_t)yr * p.dout + yc];
+    ytg = (ys < p.B && yu < p.dout) ? v : 0.0;
+  }
+
+  // ---- layer 1: lane (r, g) = (lane % 16, lane / 16) feeds sample r and
+  // units r, 16 + r with inputs 8 c + 2 g and 8 c + 2 g + 1 of chunk c (one
+  // per instruction); wave w takes chunks w, w + 8, ...  W_1 rows are padded
+  // to 32 with zeros; the input width is even, so a pair is wholly in or out.
+  {
+    const int r = lane & 15, g = lane >> 4;
+    const int nch = (p.d0 + D_CH - 1) / D_CH;
+    const bool xrow_ok = s0 + r < p.B;
+    const double* xsrc = p.X + (int64_t)(xrow_ok ? s0 + r : p.B - 1) * p.d0;
+    const double* wsrc0 = p.W[0] + (int64_t)r * p.ldw[0];
+    const double* wsrc1 = p.W[0] + (int64_t)(16 + r) * p.ldw[0];
+    doublex4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+    for (int c0 = wave; c0 < nch; c0 += D_WAVES * D_PRE) {
+      double2 xr[D_PRE], w0[D_PRE], w1[D_PRE];
+#pragma unroll
+      for (int u = 0; u < D_PRE; ++u) {
+        const int k = (c0 + D_WAVES * u) * D_CH + 2 * g;
+        const bool ok = k < p.d0;
+        const int kc = ok ? k : 0;
+        xr[u] = keep_if2(ok && xrow_ok, *reinterpret_cast<const double2*>(xsrc + kc));
+        w0[u] = keep_if2(ok, *reinterpret_cast<const double2*>(wsrc0 + kc));
+        w1[u] = keep_if2(ok, *reinterpret_cast<const double2*>(wsrc1 + kc));
+      }
+#pragma unroll
+      for (int u = 0; u < D_PRE; ++u) {
+        acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(xr[u].x, w0[u].x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(xr[u].x, w1[u].x, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(xr[u].y, w0[u].y, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(xr[u].y, w1[u].y, acc1, 0, 0, 0);
+      }
+    }
+    // accumulator register v of lane (r, g): sample 4 v + g, unit r (+16)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      zp[wave][4 * v + g][r] = acc0[v];
+      zp[wave][4 * v + g][16 + r] = acc1[v];
+    }
+  }
+  // the small layers to LDS: ws[l][j][i] = W(j, i) for the forward sums and,
+  // when training, wsT[l][i][j] = W(j, i) for the delta sums
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < D_NSTAGE; ++u) {
+      const int e = tid + u * D_WAVES * 64;
+      ws[li][e / NW][e % NW] = wsm[li][u];
+      if (TRAIN) wsT[li][e % NW][e / NW] = wsm[li][u];
+    }
+  __syncthreads();
+
+  // ---- thread (s, j) = (tid / 32, tid % 32): sample s of the tile, unit j
+  const int s = tid >> 5, j = tid & 31;
+  const int gs = s0 + s;
+  const bool s_ok = gs < p.B;
+  double z1 = zp[0][s][j];
+#pragma unroll
+  for (int w = 1; w < D_WAVES; ++w) z1 += zp[w][s][j];
+  double fp[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0;
+  int cur = 0;
+  {
+    double a = 0.0, f = 0.0;
+    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bias[0], a, f);
+    fp[0] = f;
+    if (p.L == 1) {
+      if (TRAIN) {
+        const double d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0;
+        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < p.dims[1]) {
+        p.out[(int64_t)gs * p.dims[1] + j] = a;
+      }
+    } else {
+      hs[0][s][j] = a;
+      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
+    }
+  }
+  __syncthreads();
+
+  // ---- layers 2..L (padded units carry zeros, so every sum runs over 32)
+#pragma unroll
+  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
+    if (l > p.L) break;
+    const int dl = p.dims[l];
+    const double z = dot32d(ws[l - 2][j], hs[cur][s]);
+    double a = 0.0, f = 0.0;
+    if (j < dl) act_eval(p.acts[l - 1], z + bias[l - 1], a, f);
+    fp[l - 1] = f;
+    if (l == p.L) {
+      if (TRAIN) {
+        const double d = (j < dl && s_ok) ? (a - ytg) * f : 0.0;
+        hs[cur ^ 1][s][j] = d;
+        if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < dl) {
+        p.out[(int64_t)gs * dl + j] = a;
+      }
+    } else {
+      hs[cur ^ 1][s][j] = a;
+      if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (!TRAIN) return;
+
+  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+#pragma unroll
+  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
+    if (l >= p.L) continue;
+    const double t = dot32d(wsT[l - 1][j], hs[cur][s]);
+    const double d = j < p.dims[l] ? t * fp[l - 1] : 0.0;
+    hs[cur ^ 1][s][j] = d;
+    if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+    cur ^= 1;
+    __syncthreads();
+  }
+}
+
+// Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the
+// whole batch: G[16 h + u][c0 + r] = sum over samples of
+// delta[s][16 h + u] a_prev[s][c0 + r].  Wave w takes every 8th group of 4
+// samples; the waves' sums are added in wave order, then the tile applies the
+// SGD step.
+namespace {
+
+template <class V>
+__device__ __forceinline__ V pick4(int l, V a0, V a1, V a2, V a3) {
+  return l == 0 ? a0 : (l == 1 ? a1 : (l == 2 ? a2 : a3));
+}
+
+constexpr int D2_WAVES = 8;
+constexpr int D2_UNROLL = 16;  // groups of 4 samples loaded before use
+
+}  // namespace
+
+__global__ void __launch_bounds__(D2_WAVES * 64) narrow64_dw_kernel(const NarrowDwParamsT<double> p) {
+  __shared__ double red[D2_WAVES][16][17];
+  __shared__ double bred[D2_WAVES][4][16];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // consecutive workgroups land on different XCDs (round robin over 8); give
+  // each XCD a contiguous run of tiles, so the two unit halves of a column
+  // tile and neighbouring column tiles share the input rows in one L2
+  const int nwg = p.ntiles;
+  const int per = (nwg + 7) / 8;
+  const int full = nwg - 8 * (per - 1);
+  const int xcd = (int)blockIdx.x & 7, slot = (int)blockIdx.x >> 3;
+  const int tile = xcd < full ? xcd * per + slot : full * per + (xcd - full) * (per - 1) + slot;
+  const int l = (tile >= p.tile_base[1]) + (tile >= p.tile_base[2]) + (tile >= p.tile_base[3]);
+  const int M = pick4(l, p.dims[1], p.dims[2], p.dims[3], p.dims[4]);
+  const int N = pick4(l, p.dims[0], p.dims[1], p.dims[2], p.dims[3]);
+  const int base = pick4(l, p.tile_base[0], p.tile_base[1], p.tile_base[2], p.tile_base[3]);
+  const int nh = (M + 15) / 16;
+  const int c = (tile - base) / nh, h = (tile - base) % nh;
+  const int c0 = c * 16, u0 = h * 16;
+  const double* xop = pick4(l, p.X, p.A[0], p.A[1], p.A[2]);
+  const int64_t ldx = l == 0 ? p.dims[0] : NARROW_WIDTH;
+  const double* dl = pick4(l, p.D[0], p.D[1], p.D[2], p.D[3]) + u0;
+  const int64_t ldw = pick4(l, p.ldw[0], p.ldw[1], p.ldw[2], p.ldw[3]);
+  double* G = pick4(l, p.G[0], p.G[1], p.G[2], p.G[3]);
+  double* W = pick4(l, p.W[0], p.W[1], p.W[2], p.W[3]);
+  const double* Win = pick4(l, p.Win[0], p.Win[1], p.Win[2], p.Win[3]);
+  double* gb = pick4(l, p.gb[0], p.gb[1], p.gb[2], p.gb[3]);
+  double* bias = pick4(l, p.bias[0], p.bias[1], p.bias[2], p.bias[3]);
+  const double* bin = pick4(l, p.bin[0], p.bin[1], p.bin[2], p.bin[3]);
+
+  // the parameters this thread updates at the end, requested now (clamped,
+  // always valid)
+  const int ui = (tid >> 4) & 15, uj = tid & 15;
+  const bool w_mine = tid < 256 && u0 + ui < M && c0 + uj < N;
+  const int64_t wo = w_mine ? (int64_t)(u0 + ui) * ldw + c0 + uj : 0;
+  const double w_old = Win[wo];
+  const bool b_mine = c == 0 && tid < 16 && u0 + tid < M;
+  const double b_old = bin[b_mine ? u0 + tid : 0];
+
+  // lane (r, g) feeds unit u0 + r and column c0 + r with sample g of each
+  // group of 4 (one instruction per group)
+  const int r = lane & 15, g = lane >> 4;
+  const bool col_ok = c0 + r < N;
+  const double* xcol = xop + (col_ok ? c0 + r : 0);
+  doublex4 acc = {0.0, 0.0, 0.0, 0.0};
+  double bsum = 0.0;
+  const int ngroups = (p.B + 3) / 4;
+  for (int g0 = wave; g0 < ngroups; g0 += D2_WAVES * D2_UNROLL) {
+    double dv[D2_UNROLL], xv[D2_UNROLL];
+#pragma unroll
+    for (int u = 0; u < D2_UNROLL; ++u) {
+      const int smp = (g0 + u * D2_WAVES) * 4 + g;
+      const int sc = smp < p.B ? smp : p.B - 1;
+      dv[u] = dl[(int64_t)sc * NARROW_WIDTH + r];
+      xv[u] = xcol[(int64_t)sc * ldx];
+    }
+#pragma unroll
+    for (int u = 0; u < D2_UNROLL; ++u) {
+      const bool ok = (g0 + u * D2_WAVES) * 4 + g < p.B;
+      const double a = ok ? dv[u] : 0.0;
+      const double b = (ok && col_ok) ? xv[u] : 0.0;
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+      bsum += a;
+    }
+  }
+  // accumulator register v of lane (r, g): unit u0 + 4 v + g, column c0 + r
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[wave][4 * v + g][r] = acc[v];
+  if (c == 0) bred[wave][g][r] = bsum;
+  __syncthreads();
+
+  if (w_mine) {
+    double gsum = red[0][ui][uj];
+#pragma unroll
+    for (int w = 1; w < D2_WAVES; ++w) gsum += red[w][ui][uj];
+    G[wo] = gsum;
+    W[wo] = fma(-p.scale, gsum, w_old);
+  }
+  if (b_mine) {
+    double gsum = 0.0;
+#pragma unroll
+    for (int w = 0; w < D2_WAVES; ++w)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        gsum = (w == 0 && q == 0) ? bred[0][0][tid] : gsum + bred[w][q][tid];
+    gb[u0 + tid] = gsum;
+    bias[u0 + tid] = fma(-p.scale, gsum, b_old);
+  }
+}
+
+hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hipStream_t s) {
+  const dim3 grid((p.B + D_T - 1) / D_T);
+  if (train)
+    narrow64_fwd_kernel<true><<<grid, D_WAVES * 64, 0, s>>>(p);
+  else
+    narrow64_fwd_kernel<false><<<grid, D_WAVES * 64, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s) {
+  narrow64_dw_kernel<<<dim3(p.ntiles), D2_WAVES * 64, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace nf

@@ -118,6 +118,46 @@ def test_f64_trajectory(dims, acts, batch, shards, eta, steps):
     assert not fails, "\n".join(fails[:20])
 
 
+# narrow fp64 networks (every layer after the input <= 32 units, even input
+# width) take the two-kernel step of csrc/nf_narrow64.hip; odd input widths and
+# split batches fall back to the contraction kernels on the same padded layout
+NARROW64 = [
+    # dims, acts, batch, shards
+    ((4, 3), ("sigmoid",), 1, 1),
+    ((8, 32), ("tanh",), 2, 1),
+    ((60, 7, 2), ("sigmoid", "tanh"), 3, 1),
+    ((64, 32, 31, 1), ("gaussian", "tanh", "sigmoid"), 17, 1),
+    ((66, 20, 20, 20, 20), ("tanh",), 33, 1),
+    ((1026, 30, 10), ("sigmoid",), 2049, 1),
+    ((12, 32, 32, 32, 32), ("relu", "tanh", "tanh", "sigmoid"), 100, 1),
+    ((7, 9, 4), ("tanh", "sigmoid"), 40, 1),          # odd input width: contraction kernels
+    ((64, 32, 10), ("sigmoid",), 96, 4),              # split batch: contraction kernels
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards", NARROW64)
+def test_f64_narrow(dims, acts, batch, shards):
+    acts_full = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+    theta, X, Y = _problem(dims, 5 * sum(dims) + batch, batch * 2, x_lo=-1.0)
+    note(f"f64 narrow dims={dims} batch={batch} shards={shards}")
+    ref = theta
+    fails = []
+    with Net64(dims, acts, theta) as net:
+        xd, yd = to_dev64(X), to_dev64(Y)
+        for t in range(2):
+            sl = slice(t * batch, (t + 1) * batch)
+            net.nf.nf_train_batch_f64(net.h, xd[sl], yd[sl], 1.0, shards)
+            ref, G = mlp.train_batch(ref, dims, acts_full, X[sl], Y[sl], 1.0, shards,
+                                     precision="f64")
+            fails += [f"step {t}: {m}" for m in _check(net.params(), ref, dims, "params")]
+            fails += [f"step {t}: {m}" for m in _check(net.grads(), G, dims, "grads")]
+        out = net.forward(xd)
+    e, i = parity.floored_rel(out, mlp.output(ref, dims, acts_full, X))
+    if e > F64_TOL:
+        fails.append(f"inference: {e:.3e} at {i}")
+    assert not fails, "\n".join(fails[:20])
+
+
 @pytest.mark.parametrize("name,steps", [("c1", 10), ("c2", 12), ("c3", 6), ("c4", 4), ("c5", 2)])
 def test_f64_workloads(name, steps):
     """Each workload's network, data and schedule in fp64, free-running from
