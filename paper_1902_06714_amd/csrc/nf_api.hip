@@ -343,6 +343,61 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
   const int L = num_layers(n);
   const T scale = (T)(eta / (double)batch);
   const int64_t shard_len = batch / shards;
+  T* P = cur_params<T>(n);
+  T* Q = next_params<T>(n);
+  T* G = as<T>(n->grads);
+
+  // Tendencies of layer l: G = delta_l^T A_{l-1}, g = sum of delta_l rows.
+  // A batch in one piece takes the kernel with the SGD step fused in; split
+  // batches (shards, or sub-pieces when the tile grid alone would leave most
+  // compute units idle) write per-piece sums, which are folded in piece order
+  // after every layer's pieces are in.  Each layer's pieces get their own
+  // region of the workspace, so the piece kernels of several layers share a
+  // launch and one fold serves them all.
+  struct Piece {
+    int l, nsub;
+    int64_t pstride, off;                  // weights' pitch per piece, region offset
+  };
+  std::vector<Piece> pieces;
+  int64_t total = 0;
+  for (int l = L; l >= 1; --l) {
+    const LayerLayout& ly = n->layers[l];
+    const int64_t M = ly.out, N = ly.in;
+    int nsub = 1;
+    const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    while (tiles * shards * nsub < 256 && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
+           (int64_t)shards * nsub * 2 <= 65535)
+      nsub *= 2;
+    if (shards * nsub == 1) continue;
+    const int64_t pstride = round_up(M * ly.ldw, kAlign);
+    const int64_t nsplit = (int64_t)shards * nsub;
+    pieces.push_back({l, nsub, pstride, total});
+    total += round_up(nsplit * (pstride + round_up(M, kAlign)), kAlign);
+  }
+  if (total > 0) {
+    nf_status st = ensure_partial(n, total);
+    if (st != NF_OK) return st;
+  }
+  auto piece_of = [&](int l) -> const Piece* {
+    for (const Piece& pc : pieces)
+      if (pc.l == l) return &pc;
+    return nullptr;
+  };
+  auto dw_params = [&](int l) {
+    const LayerLayout& ly = n->layers[l];
+    nf::GemmParamsT<T> p{};
+    p.A = as<T>(n->dbuf[l]);
+    p.lda = ly.lda;
+    p.B = l == 1 ? x : as<T>(n->actv[l - 1]);
+    p.ldb = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
+    p.M = ly.out;
+    p.N = ly.in;
+    p.K = (int)batch;
+    p.shard_len = (int)shard_len;
+    p.scale = scale;
+    return p;
+  };
+
   for (int l = L; l >= 1; --l) {
     const LayerLayout& ly = n->layers[l];
     if (l > 1) {
@@ -351,7 +406,7 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
       nf::GemmParamsT<T> p{};
       p.A = as<T>(n->dbuf[l]);
       p.lda = ly.lda;
-      p.B = cur_params<T>(n) + ly.w_off;
+      p.B = P + ly.w_off;
       p.ldb = ly.ldw;
       p.M = (int)batch;
       p.N = lp.out;
@@ -364,39 +419,11 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
       nf_status st = launch<T>(n, nf::EPI_BWD, true, false, true, true, 1, p, s);
       if (st != NF_OK) return st;
     }
-    // tendencies of layer l: G = delta_l^T A_{l-1}, g = sum of delta_l rows
-    const T* aprev = l == 1 ? x : as<T>(n->actv[l - 1]);
-    const int64_t ldprev = l == 1 ? n->dims[0] : n->layers[l - 1].lda;
-    const bool bv = l == 1 ? vec_ok(x, n->dims[0]) : true;
-    const int64_t M = ly.out, N = ly.in;
-    // pieces: every shard is cut into nsub sub-pieces when the tile grid alone
-    // would leave most compute units idle
-    int nsub = 1;
-    {
-      const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-      const int64_t want = 256;
-      while (tiles * shards * nsub < want && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
-             (int64_t)shards * nsub * 2 <= 65535)
-        nsub *= 2;
-    }
-    const int64_t sub_len = (shard_len + nsub - 1) / nsub;
-    const int nsplit = shards * nsub;
-    T* P = cur_params<T>(n);
-    T* Q = next_params<T>(n);
-    T* G = as<T>(n->grads);
-    nf::GemmParamsT<T> p{};
-    p.A = as<T>(n->dbuf[l]);
-    p.lda = ly.lda;
-    p.B = aprev;
-    p.ldb = ldprev;
-    p.M = (int)M;
-    p.N = (int)N;
-    p.K = (int)batch;
-    p.nsub = nsub;
-    p.shard_len = (int)shard_len;
-    p.sub_len = (int)sub_len;
-    p.scale = scale;
-    if (nsplit == 1) {
+    if (!piece_of(l)) {
+      const bool bv = l == 1 ? vec_ok(x, n->dims[0]) : true;
+      nf::GemmParamsT<T> p = dw_params(l);
+      p.nsub = 1;
+      p.sub_len = (int)shard_len;
       p.out0 = G + ly.w_off;
       p.ld0 = ly.ldw;
       p.W = Q + ly.w_off;
@@ -407,26 +434,80 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
       p.gbias = G + ly.b_off;
       nf_status st = launch<T>(n, nf::EPI_DW_SGD, false, false, true, bv, 1, p, s);
       if (st != NF_OK) return st;
-    } else {
-      const int64_t pstride = round_up(M * ly.ldw, kAlign);
-      nf_status st = ensure_partial(n, (int64_t)nsplit * (pstride + round_up(M, kAlign)));
-      if (st != NF_OK) return st;
-      p.partial = as<T>(n->partial);
-      p.pstride = pstride;
-      p.ld0 = ly.ldw;
-      p.pbias = p.partial + (int64_t)nsplit * pstride;
-      st = launch<T>(n, nf::EPI_DW_PARTIAL, false, false, true, bv, nsplit, p, s);
-      if (st != NF_OK) return st;
-      const double elems = (double)M * N + M;
-      st = timed(n, sizeof(T) == 8 ? "fold64_sgd" : "fold_sgd",
-                 (double)sizeof(T) * elems * (nsplit + 3), elems * (nsplit + 1), s, [&] {
-                   return nf::launch_fold_sgd<T>(p.partial, pstride, p.pbias, shards, nsub, (int)M,
-                                                 (int)N, ly.ldw, G + ly.w_off, G + ly.b_off,
-                                                 P + ly.w_off, P + ly.b_off, Q + ly.w_off,
-                                                 Q + ly.b_off, scale, s);
-                 });
-      if (st != NF_OK) return st;
     }
+  }
+  if (pieces.empty()) return NF_OK;
+
+  // the piece kernels, grouped by tile shape and B-row vector loads (layer
+  // order within a group), up to GEMM_GROUP_MAX layers per launch
+  const int dtype = dtype_of<T>();
+  std::vector<bool> done(pieces.size(), false);
+  for (size_t i = 0; i < pieces.size(); ++i) {
+    if (done[i]) continue;
+    const Piece& pi = pieces[i];
+    const LayerLayout& li = n->layers[pi.l];
+    const int tile = pick_tile(li.out, li.in, (int64_t)shards * pi.nsub);
+    const bool bv = pi.l == 1 ? vec_ok(x, n->dims[0]) : true;
+    nf::GemmGroupT<T> g{};
+    int nsplit[nf::GEMM_GROUP_MAX];
+    double bytes = 0.0, flops = 0.0;
+    for (size_t j = i; j < pieces.size() && g.n < nf::GEMM_GROUP_MAX; ++j) {
+      if (done[j]) continue;
+      const Piece& pj = pieces[j];
+      const LayerLayout& lj = n->layers[pj.l];
+      const int tj = pick_tile(lj.out, lj.in, (int64_t)shards * pj.nsub);
+      const bool bvj = pj.l == 1 ? vec_ok(x, n->dims[0]) : true;
+      if (tj != tile || bvj != bv) continue;
+      nf::GemmParamsT<T> p = dw_params(pj.l);
+      p.nsub = pj.nsub;
+      p.sub_len = (int)((shard_len + pj.nsub - 1) / pj.nsub);
+      p.partial = as<T>(n->partial) + pj.off;
+      p.pstride = pj.pstride;
+      p.ld0 = lj.ldw;
+      p.pbias = p.partial + (int64_t)shards * pj.nsub * pj.pstride;
+      nsplit[g.n] = shards * pj.nsub;
+      g.p[g.n++] = p;
+      bytes += gemm_bytes(nf::EPI_DW_PARTIAL, p.M, p.N, p.K, nsplit[g.n - 1], (double)sizeof(T));
+      flops += 2.0 * p.M * (double)p.N * p.K;
+      done[j] = true;
+    }
+    nf_status st = timed(n, nf::gemm_name(nf::EPI_DW_PARTIAL, tile, dtype), bytes, flops, s, [&] {
+      return nf::launch_dw_partial_group<T>(tile, bv, g, nsplit, s);
+    });
+    if (st != NF_OK) return st;
+  }
+
+  // one fold for up to FOLD_GROUP_MAX layers
+  for (size_t i = 0; i < pieces.size(); i += nf::FOLD_GROUP_MAX) {
+    nf::FoldGroupT<T> f{};
+    f.nshards = shards;
+    f.scale = scale;
+    double bytes = 0.0, flops = 0.0;
+    for (size_t j = i; j < pieces.size() && f.n < nf::FOLD_GROUP_MAX; ++j) {
+      const Piece& pc = pieces[j];
+      const LayerLayout& ly = n->layers[pc.l];
+      const int64_t nsplit = (int64_t)shards * pc.nsub;
+      nf::FoldLayerT<T>& fl = f.l[f.n++];
+      fl.partial = as<T>(n->partial) + pc.off;
+      fl.pstride = pc.pstride;
+      fl.pbias = fl.partial + nsplit * pc.pstride;
+      fl.nsub = pc.nsub;
+      fl.M = ly.out;
+      fl.N = ly.in;
+      fl.ldw = ly.ldw;
+      fl.G = G + ly.w_off;
+      fl.gbias = G + ly.b_off;
+      fl.Win = P + ly.w_off;
+      fl.bin = P + ly.b_off;
+      fl.W = Q + ly.w_off;
+      fl.b = Q + ly.b_off;
+      const double elems = (double)ly.out * ly.in + ly.out;
+      bytes += (double)sizeof(T) * elems * (nsplit + 3);
+      flops += elems * (nsplit + 1);
+    }
+    nf_status st = timed(n, sizeof(T) == 8 ? "fold64_sgd" : "fold_sgd", bytes, flops, s,
+                         [&] { return nf::launch_fold_sgd<T>(f, s); });
+    if (st != NF_OK) return st;
   }
   return NF_OK;
 }

@@ -66,13 +66,52 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
 // Name of the kernel instance launch_gemm picks for these arguments.
 const char* gemm_name(int epi, int tile, int dtype);
 
-// Fold the per-piece tendencies of one layer in piece order, store the sum as
-// the tendency, and write the SGD step W = Win - scale * G, b = bin - scale * g
-// (W [M][ldw], b [M]).
+// The tendency pieces of up to GEMM_GROUP_MAX layers in one launch
+// (EPI_DW_PARTIAL; both operands mn-contiguous, A rows vectorisable, B rows as
+// b_vec says), problem q split into nsplit[q] pieces.  The workgroup table is
+// filled by the launcher.
+constexpr int GEMM_GROUP_MAX = 4;
 template <class T>
-hipError_t launch_fold_sgd(const T* partial, int64_t pstride, const T* pbias, int nshards,
-                           int nsub, int M, int N, int64_t ldw, T* G, T* gbias, const T* Win,
-                           const T* bin, T* W, T* b, T scale, hipStream_t s);
+struct GemmGroupT {
+  GemmParamsT<T> p[GEMM_GROUP_MAX];
+  int start[GEMM_GROUP_MAX + 1];           // first workgroup of each problem
+  int n;                                   // problems
+};
+template <class T>
+hipError_t launch_dw_partial_group(int tile, bool b_vec, const GemmGroupT<T>& g,
+                                   const int* nsplit, hipStream_t s);
+
+// Fold the per-piece tendencies of up to FOLD_GROUP_MAX layers in piece order,
+// store each sum as the tendency, and write the SGD step W = Win - scale * G,
+// b = bin - scale * g (W [M][ldw], b [M]).  Layer q's pieces: nshards shards
+// of nsub sub-pieces, weights at partial + piece * pstride, biases at
+// pbias + piece * M.  The workgroup table is filled by the launcher.
+constexpr int FOLD_GROUP_MAX = 8;
+constexpr int FOLD_THREADS = 256;
+template <class T>
+struct FoldLayerT {
+  const T* partial;
+  int64_t pstride;
+  const T* pbias;
+  int nsub, M, N;
+  int64_t ldw;
+  T* G;
+  T* gbias;
+  const T* Win;
+  const T* bin;
+  T* W;
+  T* b;
+};
+template <class T>
+struct FoldGroupT {
+  FoldLayerT<T> l[FOLD_GROUP_MAX];
+  int start[FOLD_GROUP_MAX + 1];           // first workgroup of each layer
+  int n;                                   // layers
+  int nshards;
+  T scale;
+};
+template <class T>
+hipError_t launch_fold_sgd(FoldGroupT<T> g, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Narrow networks: every layer after the input has at most NARROW_WIDTH units

@@ -174,8 +174,7 @@ struct TileLoader {
 // N tiles, pieces of the k range).
 template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
           bool BV, int EPI>
-__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
-gemm_kernel(const GemmParamsT<T> p) {
+__device__ __forceinline__ void gemm_tile(const GemmParamsT<T>& p, int bx, int by, int bz) {
   using MM = Mma<T>;
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   constexpr int TM = WM / MM::BLK, TN = WN / MM::BLK;
@@ -188,19 +187,19 @@ gemm_kernel(const GemmParamsT<T> p) {
   const int wave = tid >> 6;
   const int wm = (wave % (BM / WM)) * WM;
   const int wn = (wave / (BM / WM)) * WN;
-  const int m0 = blockIdx.x * BM;
-  const int n0 = blockIdx.y * BN;
+  const int m0 = bx * BM;
+  const int n0 = by * BN;
 
   // k range of this piece
   int kbeg = 0, kend = p.K;
   if constexpr (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) {
-    const int z = blockIdx.z;
+    const int z = bz;
     const int shard = z / p.nsub, sub = z % p.nsub;
     const int sb = shard * p.shard_len;
     kbeg = sb + sub * p.sub_len;
     kend = min(kbeg + p.sub_len, sb + p.shard_len);
   }
-  const bool do_bias = (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) && blockIdx.y == 0;
+  const bool do_bias = (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) && by == 0;
 
   typename MM::acc_t acc[TM][TN];
 #pragma unroll
@@ -319,7 +318,7 @@ gemm_kernel(const GemmParamsT<T> p) {
           p.out0[o] = c;
           p.W[o] = fma_t(-p.scale, c, p.Win[o]);
         } else {  // EPI_DW_PARTIAL
-          p.partial[(int64_t)blockIdx.z * p.pstride + (int64_t)m * p.ld0 + n] = c;
+          p.partial[(int64_t)bz * p.pstride + (int64_t)m * p.ld0 + n] = c;
         }
       }
     }
@@ -331,43 +330,74 @@ gemm_kernel(const GemmParamsT<T> p) {
         p.gbias[m] = bsum;
         p.bvec[m] = fma_t(-p.scale, bsum, p.bin[m]);
       } else if constexpr (EPI == EPI_DW_PARTIAL) {
-        p.pbias[(int64_t)blockIdx.z * p.M + m] = bsum;
+        p.pbias[(int64_t)bz * p.M + m] = bsum;
       }
     }
   }
 }
 
+
+// One launch of one contraction: grid = (M tiles, N tiles, pieces of the k range).
+template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
+          bool BV, int EPI>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_kernel(const GemmParamsT<T> p) {
+  gemm_tile<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, EPI>(p, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// One launch of several contractions of the same shape class (the tendency
+// pieces of several layers): workgroup b belongs to the problem q with
+// start[q] <= b < start[q + 1] and takes its tiles in the order of the
+// single-problem grid (M tiles fastest, then N tiles, then pieces).
+template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
+          bool BV, int EPI>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_group_kernel(const GemmGroupT<T> g) {
+  const int b = blockIdx.x;
+  int q = 0;
+#pragma unroll
+  for (int i = 1; i < GEMM_GROUP_MAX; ++i) q += (i < g.n && b >= g.start[i]);
+  const int r = b - g.start[q];
+  const int mt = (g.p[q].M + BM - 1) / BM, nt = (g.p[q].N + BN - 1) / BN;
+  const int z = r / (mt * nt), rem = r % (mt * nt);
+  gemm_tile<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, EPI>(g.p[q], rem % mt, rem / mt, z);
+}
+
 // Sum of the per-piece tendencies in piece order, then the SGD step (from the
-// parameters before the step into the other parameter buffer).
+// parameters before the step into the other parameter buffer), for up to
+// FOLD_GROUP_MAX layers per launch; workgroup b belongs to layer q with
+// start[q] <= b < start[q + 1].
 template <class T>
-__global__ void fold_sgd_kernel(const T* __restrict__ partial, int64_t pstride,
-                                const T* __restrict__ pbias, int nshards, int nsub, int M, int N,
-                                int64_t ldw, T* __restrict__ G, T* __restrict__ gbias,
-                                const T* __restrict__ Win, const T* __restrict__ bin,
-                                T* __restrict__ W, T* __restrict__ b, T scale) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nw = (int64_t)M * N;
+__global__ void fold_sgd_kernel(const FoldGroupT<T> g) {
+  const int b = blockIdx.x;
+  int q = 0;
+#pragma unroll
+  for (int i = 1; i < FOLD_GROUP_MAX; ++i) q += (i < g.n && b >= g.start[i]);
+  const FoldLayerT<T>& f = g.l[q];
+  const int64_t idx = (int64_t)(b - g.start[q]) * blockDim.x + threadIdx.x;
+  const int64_t nw = (int64_t)f.M * f.N;
+  const int nshards = g.nshards, nsub = f.nsub;
   if (idx < nw) {
-    const int m = (int)(idx / N), n = (int)(idx % N);
-    const int64_t o = (int64_t)m * ldw + n;
+    const int m = (int)(idx / f.N), n = (int)(idx % f.N);
+    const int64_t o = (int64_t)m * f.ldw + n;
     T tot = T(0);
     for (int s = 0; s < nshards; ++s) {
-      T piece = partial[(int64_t)(s * nsub) * pstride + o];
-      for (int q = 1; q < nsub; ++q) piece += partial[(int64_t)(s * nsub + q) * pstride + o];
+      T piece = f.partial[(int64_t)(s * nsub) * f.pstride + o];
+      for (int u = 1; u < nsub; ++u) piece += f.partial[(int64_t)(s * nsub + u) * f.pstride + o];
       tot = s == 0 ? piece : tot + piece;
     }
-    G[o] = tot;
-    W[o] = fma_t(-scale, tot, Win[o]);
-  } else if (idx < nw + M) {
+    f.G[o] = tot;
+    f.W[o] = fma_t(-g.scale, tot, f.Win[o]);
+  } else if (idx < nw + f.M) {
     const int m = (int)(idx - nw);
     T tot = T(0);
     for (int s = 0; s < nshards; ++s) {
-      T piece = pbias[(int64_t)(s * nsub) * M + m];
-      for (int q = 1; q < nsub; ++q) piece += pbias[(int64_t)(s * nsub + q) * M + m];
+      T piece = f.pbias[(int64_t)(s * nsub) * f.M + m];
+      for (int u = 1; u < nsub; ++u) piece += f.pbias[(int64_t)(s * nsub + u) * f.M + m];
       tot = s == 0 ? piece : tot + piece;
     }
-    gbias[m] = tot;
-    b[m] = fma_t(-scale, tot, bin[m]);
+    f.gbias[m] = tot;
+    f.b[m] = fma_t(-g.scale, tot, f.bin[m]);
   }
 }
 
@@ -445,23 +475,57 @@ const char* gemm_name(int epi, int tile, int dtype) {
 }
 
 template <class T>
-hipError_t launch_fold_sgd(const T* partial, int64_t pstride, const T* pbias, int nshards,
-                           int nsub, int M, int N, int64_t ldw, T* G, T* gbias, const T* Win,
-                           const T* bin, T* W, T* b, T scale, hipStream_t s) {
-  const int64_t total = (int64_t)M * N + M;
-  const int threads = 256;
-  const int64_t blocks = (total + threads - 1) / threads;
-  fold_sgd_kernel<T><<<dim3((unsigned)blocks), threads, 0, s>>>(partial, pstride, pbias, nshards,
-                                                              nsub, M, N, ldw, G, gbias, Win, bin,
-                                                              W, b, scale);
+hipError_t launch_fold_sgd(FoldGroupT<T> g, hipStream_t s) {
+  if (g.n < 1 || g.n > FOLD_GROUP_MAX) return hipErrorInvalidValue;
+  const int threads = FOLD_THREADS;
+  g.start[0] = 0;
+  for (int q = 0; q < g.n; ++q) {
+    const int64_t elems = (int64_t)g.l[q].M * g.l[q].N + g.l[q].M;
+    g.start[q + 1] = g.start[q] + (int)((elems + threads - 1) / threads);
+  }
+  for (int q = g.n + 1; q <= FOLD_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
+  fold_sgd_kernel<T><<<dim3((unsigned)g.start[g.n]), threads, 0, s>>>(g);
   return hipGetLastError();
 }
 
-template hipError_t launch_fold_sgd<float>(const float*, int64_t, const float*, int, int, int, int,
-                                           int64_t, float*, float*, const float*, const float*,
-                                           float*, float*, float, hipStream_t);
-template hipError_t launch_fold_sgd<double>(const double*, int64_t, const double*, int, int, int,
-                                            int, int64_t, double*, double*, const double*,
-                                            const double*, double*, double*, double, hipStream_t);
+template hipError_t launch_fold_sgd<float>(FoldGroupT<float>, hipStream_t);
+template hipError_t launch_fold_sgd<double>(FoldGroupT<double>, hipStream_t);
+
+template <class T, int BM, int BN, int WM, int WN, int PD, bool BV>
+static hipError_t launch_group(GemmGroupT<T> g, const int* nsplit, hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  g.start[0] = 0;
+  for (int q = 0; q < g.n; ++q) {
+    const int mt = (g.p[q].M + BM - 1) / BM, nt = (g.p[q].N + BN - 1) / BN;
+    g.start[q + 1] = g.start[q] + mt * nt * nsplit[q];
+  }
+  for (int q = g.n + 1; q <= GEMM_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
+  gemm_group_kernel<T, BM, BN, 16, WM, WN, PD, false, false, true, BV, EPI_DW_PARTIAL>
+      <<<dim3((unsigned)g.start[g.n]), NT, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_dw_partial_group(int tile, bool b_vec, const GemmGroupT<T>& g,
+                                   const int* nsplit, hipStream_t s) {
+  if (g.n < 1 || g.n > GEMM_GROUP_MAX) return hipErrorInvalidValue;
+  for (int q = 0; q < g.n; ++q) {
+    if (g.p[q].M <= 0 || g.p[q].N <= 0 || nsplit[q] <= 0) return hipErrorInvalidValue;
+    const int64_t ld = g.p[q].lda > g.p[q].ldb ? g.p[q].lda : g.p[q].ldb;
+    if ((int64_t)128 * ld * (int64_t)sizeof(T) >= (int64_t)TILE_OOB) return hipErrorInvalidValue;
+  }
+  // the tiles and stage depths of launch_gemm
+  constexpr int PD64 = sizeof(T) == 8 ? 4 : 8;
+  if (tile == TILE_128x128)
+    return b_vec ? launch_group<T, 128, 128, 64, 32, 4, true>(g, nsplit, s)
+                 : launch_group<T, 128, 128, 64, 32, 4, false>(g, nsplit, s);
+  return b_vec ? launch_group<T, 64, 64, 32, 32, PD64, true>(g, nsplit, s)
+               : launch_group<T, 64, 64, 32, 32, PD64, false>(g, nsplit, s);
+}
+
+template hipError_t launch_dw_partial_group<float>(int, bool, const GemmGroupT<float>&, const int*,
+                                                   hipStream_t);
+template hipError_t launch_dw_partial_group<double>(int, bool, const GemmGroupT<double>&,
+                                                    const int*, hipStream_t);
 
 }  // namespace nf
