@@ -269,14 +269,16 @@ double gemm_bytes(int epi, int M_, int N_, int K_, int nsplit, double esz) {
     case nf::EPI_FWD_OUT: return esz * (M * K + N * K + N + M * N);
     case nf::EPI_BWD: return esz * (M * K + K * N + 2 * M * N);
     case nf::EPI_DW_SGD: return esz * (K * M + K * N + 3 * M * N + 3 * M);
+    case nf::EPI_FWD_PIECE: return esz * (M * K + N * K + nsplit * M * N);
     default: return esz * (K * M + K * N + nsplit * (M * N + M));
   }
 }
 
+// tile_override: a TileShape, or -1 to pick one from the grid size
 template <class T>
 nf_status launch(nf_net* n, int epi, bool akc, bool bkc, bool av, bool bv, int nsplit,
-                 const nf::GemmParamsT<T>& p, hipStream_t s) {
-  const int tile = pick_tile(p.M, p.N, nsplit);
+                 const nf::GemmParamsT<T>& p, hipStream_t s, int tile_override = -1) {
+  const int tile = tile_override >= 0 ? tile_override : pick_tile(p.M, p.N, nsplit);
   return timed(n, nf::gemm_name(epi, tile, dtype_of<T>()),
                gemm_bytes(epi, p.M, p.N, p.K, nsplit, (double)sizeof(T)),
                2.0 * p.M * (double)p.N * p.K, s,
@@ -329,7 +331,58 @@ nf_status run_forward(nf_net* n, const T* x, const T* y, int64_t batch, T* out, 
         p.ld0 = ly.out;
       }
     }
-    nf_status st = launch<T>(n, epi, true, true, av, true, 1, p, s);
+    // A contraction with too few 64 x 64 tiles to fill the chip and a long k
+    // range is split over the k range; a fold adds the pieces in order and
+    // applies the epilogue.
+    const int64_t tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
+    const int64_t want = 2 * (int64_t)(n->ncu > 0 ? n->ncu : 256);
+    int nsplit = 1;
+    if (pick_tile(p.M, p.N, 1) == nf::TILE_64x64 && tiles < want && p.K >= 256) {
+      nsplit = (int)std::min<int64_t>({(want + tiles - 1) / tiles, p.K / 128, 16});
+    }
+    nf_status st;
+    if (nsplit <= 1) {
+      st = launch<T>(n, epi, true, true, av, true, 1, p, s);
+    } else {
+      // pieces start on whole 16-input stages, so a vector load never
+      // reaches into the next piece and every piece start stays 16-byte
+      // aligned
+      const int sub_len = (int)round_up((p.K + nsplit - 1) / nsplit, 16);
+      nsplit = (p.K + sub_len - 1) / sub_len;
+      const int64_t ldp = round_up(p.N, 4);
+      const int64_t pstride = round_up((int64_t)p.M * ldp, kAlign);
+      st = ensure_partial(n, nsplit * pstride);
+      if (st != NF_OK) return st;
+      nf::GemmParamsT<T> q = p;
+      q.shard_len = p.K;
+      q.nsub = nsplit;
+      q.sub_len = sub_len;
+      q.partial = as<T>(n->partial);
+      q.pstride = pstride;
+      q.ld0 = ldp;
+      st = launch<T>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, q, s, nf::TILE_64x64);
+      if (st != NF_OK) return st;
+      nf::FwdFoldParamsT<T> f{};
+      f.partial = q.partial;
+      f.pstride = pstride;
+      f.ldp = ldp;
+      f.nsplit = nsplit;
+      f.M = p.M;
+      f.N = p.N;
+      f.bias = p.bias;
+      f.act = p.act;
+      f.out0 = p.out0;
+      f.ld0 = p.ld0;
+      f.out1 = p.out1;
+      f.ld1 = p.ld1;
+      f.aux = p.aux;
+      f.ldaux = p.ldaux;
+      const double mn = (double)p.M * p.N;
+      const double outs = epi == nf::EPI_FWD_STASH ? 2.0 : (epi == nf::EPI_FWD_DELTA ? 2.0 : 1.0);
+      st = timed(n, sizeof(T) == 8 ? "fwd64_fold" : "fwd_fold",
+                 (double)sizeof(T) * (mn * (nsplit + outs) + p.N), mn * (nsplit + 1), s,
+                 [&] { return nf::launch_fwd_fold<T>(epi, f, s); });
+    }
     if (st != NF_OK) return st;
   }
   return NF_OK;

@@ -13,7 +13,8 @@ enum Epilogue : int {
   EPI_FWD_OUT = 2,    // z = C + b[n]; out0 = f(z)              (inference)
   EPI_BWD = 3,        // out0 = C * aux                          (hidden delta)
   EPI_DW_SGD = 4,     // G = C; W -= scale * C; bias sums and update
-  EPI_DW_PARTIAL = 5  // partial[split] = C; bias partial sums
+  EPI_DW_PARTIAL = 5, // partial[split] = C; bias partial sums
+  EPI_FWD_PIECE = 6   // forward operands, partial[piece] = C over a piece of the k range
 };
 
 // Element types of a network's parameters and per-sample buffers.
@@ -65,6 +66,26 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
 
 // Name of the kernel instance launch_gemm picks for these arguments.
 const char* gemm_name(int epi, int tile, int dtype);
+
+// Forward contractions split over the k range (EPI_FWD_PIECE) finish here:
+// z = sum of the pieces in piece order + b[n], then the forward epilogue
+// `epi` (EPI_FWD_STASH, EPI_FWD_DELTA or EPI_FWD_OUT) on z.
+template <class T>
+struct FwdFoldParamsT {
+  const T* partial;                        // [nsplit][M][ldp]
+  int64_t pstride, ldp;
+  int nsplit, M, N;
+  const T* bias;                           // [N]
+  int act;
+  T* out0;                                 // [M][ld0]
+  int64_t ld0;
+  T* out1;                                 // EPI_FWD_STASH: f'(z) [M][ld1]
+  int64_t ld1;
+  const T* aux;                            // EPI_FWD_DELTA: y [M][ldaux]
+  int64_t ldaux;
+};
+template <class T>
+hipError_t launch_fwd_fold(int epi, const FwdFoldParamsT<T>& f, hipStream_t s);
 
 // The tendency pieces of up to GEMM_GROUP_MAX layers in one launch
 // (EPI_DW_PARTIAL; both operands mn-contiguous, A rows vectorisable, B rows as

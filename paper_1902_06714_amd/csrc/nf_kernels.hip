@@ -192,7 +192,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParamsT<T>& p, int bx, int b
 
   // k range of this piece
   int kbeg = 0, kend = p.K;
-  if constexpr (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL) {
+  if constexpr (EPI == EPI_DW_SGD || EPI == EPI_DW_PARTIAL || EPI == EPI_FWD_PIECE) {
     const int z = bz;
     const int shard = z / p.nsub, sub = z % p.nsub;
     const int sb = shard * p.shard_len;
@@ -317,7 +317,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParamsT<T>& p, int bx, int b
           const int64_t o = (int64_t)m * p.ldw + n;
           p.out0[o] = c;
           p.W[o] = fma_t(-p.scale, c, p.Win[o]);
-        } else {  // EPI_DW_PARTIAL
+        } else {  // EPI_DW_PARTIAL, EPI_FWD_PIECE
           p.partial[(int64_t)bz * p.pstride + (int64_t)m * p.ld0 + n] = c;
         }
       }
@@ -423,6 +423,8 @@ static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, i
   NF_CASE(true, true, false, true, EPI_FWD_DELTA)
   NF_CASE(true, true, true, true, EPI_FWD_OUT)
   NF_CASE(true, true, false, true, EPI_FWD_OUT)
+  NF_CASE(true, true, true, true, EPI_FWD_PIECE)
+  NF_CASE(true, true, false, true, EPI_FWD_PIECE)
   // backward: A = delta [m][k], B(k, n) = W[k][n]
   NF_CASE(true, false, true, true, EPI_BWD)
   // tendencies: A(m, k) = delta[k][m], B(k, n) = activations[k][n]
@@ -461,18 +463,62 @@ template hipError_t launch_gemm<double>(int, int, bool, bool, bool, bool, int,
                                         const GemmParamsT<double>&, hipStream_t);
 
 const char* gemm_name(int epi, int tile, int dtype) {
-  static const char* names[2][2][6] = {
+  static const char* names[2][2][7] = {
       {{"gemm_fwd_stash_128x128", "gemm_fwd_delta_128x128", "gemm_fwd_out_128x128",
-        "gemm_bwd_128x128", "gemm_dw_sgd_128x128", "gemm_dw_partial_128x128"},
+        "gemm_bwd_128x128", "gemm_dw_sgd_128x128", "gemm_dw_partial_128x128",
+        "gemm_fwd_piece_128x128"},
        {"gemm_fwd_stash_64x64", "gemm_fwd_delta_64x64", "gemm_fwd_out_64x64", "gemm_bwd_64x64",
-        "gemm_dw_sgd_64x64", "gemm_dw_partial_64x64"}},
+        "gemm_dw_sgd_64x64", "gemm_dw_partial_64x64", "gemm_fwd_piece_64x64"}},
       {{"gemm64_fwd_stash_128x128", "gemm64_fwd_delta_128x128", "gemm64_fwd_out_128x128",
-        "gemm64_bwd_128x128", "gemm64_dw_sgd_128x128", "gemm64_dw_partial_128x128"},
+        "gemm64_bwd_128x128", "gemm64_dw_sgd_128x128", "gemm64_dw_partial_128x128",
+        "gemm64_fwd_piece_128x128"},
        {"gemm64_fwd_stash_64x64", "gemm64_fwd_delta_64x64", "gemm64_fwd_out_64x64",
-        "gemm64_bwd_64x64", "gemm64_dw_sgd_64x64", "gemm64_dw_partial_64x64"}}};
-  if (epi < 0 || epi > 5 || tile < 0 || tile > 1 || dtype < 0 || dtype > 1) return "gemm";
+        "gemm64_bwd_64x64", "gemm64_dw_sgd_64x64", "gemm64_dw_partial_64x64",
+        "gemm64_fwd_piece_64x64"}}};
+  if (epi < 0 || epi > 6 || tile < 0 || tile > 1 || dtype < 0 || dtype > 1) return "gemm";
   return names[dtype][tile][epi];
 }
+
+// The forward epilogue on the sum of a split contraction's pieces (piece
+// order), one thread per (m, n), n fastest.
+template <class T, int EPI>
+__global__ void fwd_fold_kernel(const FwdFoldParamsT<T> f) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)f.M * f.N) return;
+  const int m = (int)(idx / f.N), n = (int)(idx % f.N);
+  const int64_t o = (int64_t)m * f.ldp + n;
+  T z = f.partial[o];
+  for (int q = 1; q < f.nsplit; ++q) z += f.partial[(int64_t)q * f.pstride + o];
+  T a, fp;
+  act_eval(f.act, z + f.bias[n], a, fp);
+  if constexpr (EPI == EPI_FWD_STASH) {
+    f.out0[(int64_t)m * f.ld0 + n] = a;
+    f.out1[(int64_t)m * f.ld1 + n] = fp;
+  } else if constexpr (EPI == EPI_FWD_DELTA) {
+    f.out0[(int64_t)m * f.ld0 + n] = (a - f.aux[(int64_t)m * f.ldaux + n]) * fp;
+  } else {
+    f.out0[(int64_t)m * f.ld0 + n] = a;
+  }
+}
+
+template <class T>
+hipError_t launch_fwd_fold(int epi, const FwdFoldParamsT<T>& f, hipStream_t s) {
+  const int64_t total = (int64_t)f.M * f.N;
+  if (total <= 0 || f.nsplit < 1) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (epi == EPI_FWD_STASH)
+    fwd_fold_kernel<T, EPI_FWD_STASH><<<grid, 256, 0, s>>>(f);
+  else if (epi == EPI_FWD_DELTA)
+    fwd_fold_kernel<T, EPI_FWD_DELTA><<<grid, 256, 0, s>>>(f);
+  else if (epi == EPI_FWD_OUT)
+    fwd_fold_kernel<T, EPI_FWD_OUT><<<grid, 256, 0, s>>>(f);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template hipError_t launch_fwd_fold<float>(int, const FwdFoldParamsT<float>&, hipStream_t);
+template hipError_t launch_fwd_fold<double>(int, const FwdFoldParamsT<double>&, hipStream_t);
 
 template <class T>
 hipError_t launch_fold_sgd(FoldGroupT<T> g, hipStream_t s) {

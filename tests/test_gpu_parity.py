@@ -131,7 +131,11 @@ def test_small_relu_elementwise(dims, acts, batch, shards, eta):
 
 def test_narrow_and_general_paths_agree():
     """A narrow network trained with one shard (its own two-kernel path) and
-    with two shards (the general contraction path) differs only by rounding."""
+    with two shards (the general contraction path) differs only by rounding.
+    The two paths add the 784 products of a layer-1 sum in different orders
+    (the general path in k pieces), which moves a sum by about sqrt(784) *
+    2^-24 = 1.7e-6 of its magnitude; the gate is 1e-5 for parameters and
+    tendencies alike."""
     dims = (784, 30, 10)
     theta, X, Y = _problem(dims, 21, 1000)
     res = []
@@ -140,7 +144,7 @@ def test_narrow_and_general_paths_agree():
         with GpuNet(dims, ("sigmoid",), theta) as net:
             net.train_batch(to_dev(X), to_dev(Y), 3.0, shards)
             res.append((net.params(), net.grads()))
-    assert not parity.check_params(res[0][0], res[1][0], dims, tol=1e-6)
+    assert not parity.check_params(res[0][0], res[1][0], dims, tol=1e-5)
     assert not parity.check_params(res[0][1], res[1][1], dims, tol=1e-5, what="grads")
 
 
