@@ -64,6 +64,14 @@ SMALL = [
     ((8, 3), ("sigmoid",), 77, 1, 1.0),
     ((20, 32), ("tanh",), 129, 1, 0.5),
     ((1024, 32, 16, 10), ("tanh", "gaussian", "sigmoid"), 2048, 1, 0.5),
+    # forward contractions split over k (few tiles, k >= 256): odd input width
+    # (scalar loads), and a k range of 257 (the output layers of the
+    # 12-300-300-5 network above and of the wide workloads are split too)
+    ((301, 40, 10), ("tanh", "sigmoid"), 200, 1, 0.5),
+    ((300, 257, 129, 10), ("tanh", "relu", "sigmoid"), 500, 4, 0.5),
+    # ten layers with split batches: three launches of tendency pieces
+    # (at most four layers each) and two folds (at most eight layers each)
+    ((16, 12, 14, 10, 12, 9, 11, 8, 10, 7, 5), ("tanh",), 64, 2, 0.5),
     # narrow networks past 2048 samples take 16-sample tiles (ragged last tile)
     ((784, 30, 10), ("sigmoid",), 2049, 1, 3.0),
     ((40, 17, 9, 5), ("tanh", "sigmoid", "gaussian"), 4100, 1, 0.5),
