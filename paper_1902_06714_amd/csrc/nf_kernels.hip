@@ -427,11 +427,10 @@ static hipError_t dispatch_tile(int epi, bool akc, bool bkc, bool av, bool bv, i
   NF_CASE(true, true, false, true, EPI_FWD_PIECE)
   // backward: A = delta [m][k], B(k, n) = W[k][n]
   NF_CASE(true, false, true, true, EPI_BWD)
-  // tendencies: A(m, k) = delta[k][m], B(k, n) = activations[k][n]
+  // tendencies: A(m, k) = delta[k][m], B(k, n) = activations[k][n] (the
+  // tendency pieces go through launch_dw_partial_group)
   NF_CASE(false, false, true, true, EPI_DW_SGD)
   NF_CASE(false, false, true, false, EPI_DW_SGD)
-  NF_CASE(false, false, true, true, EPI_DW_PARTIAL)
-  NF_CASE(false, false, true, false, EPI_DW_PARTIAL)
 #undef NF_CASE
   return hipErrorInvalidValue;
 }
