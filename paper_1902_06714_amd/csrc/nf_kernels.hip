@@ -401,6 +401,13 @@ __global__ void fold_sgd_kernel(const FoldGroupT<T> g) {
   }
 }
 
+// Operand stages in flight per tile shape (measured).  The 128 x 128 tile
+// runs one workgroup per CU on large problems and needs the depth; the
+// 64 x 64 tile serves small grids, where extra stages cost registers and so
+// workgroups per CU, which hide the memory latency better.
+constexpr int PD_128 = 4;
+constexpr int PD_64 = 2;
+
 template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, bool BKC, bool AV,
           bool BV, int EPI>
 static hipError_t launch_one(int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
@@ -441,18 +448,14 @@ hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a
   if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
   // The 128 x 128 tile runs 8 waves of 64 x 32 (two per SIMD, so one
   // wave's LDS reads and barrier waits overlap the other's matrix work).
-  // Stages in flight: the small tile's few products per stage need more of
-  // them to cover the memory latency.
   constexpr int WN128 = 32;
-  constexpr int PD128 = 4;
-  constexpr int PD64 = sizeof(T) == 8 ? 4 : 8;
   // element offsets inside one buffer-based tile stay below TILE_OOB bytes
   if ((int64_t)128 * (p.lda > p.ldb ? p.lda : p.ldb) * (int64_t)sizeof(T) >= (int64_t)TILE_OOB)
     return hipErrorInvalidValue;
   if (tile == TILE_128x128)
-    return dispatch_tile<T, 128, 128, 16, 64, WN128, PD128>(epi, a_kcontig, b_kcontig, a_vec,
+    return dispatch_tile<T, 128, 128, 16, 64, WN128, PD_128>(epi, a_kcontig, b_kcontig, a_vec,
                                                             b_vec, nsplit, p, s);
-  return dispatch_tile<T, 64, 64, 16, 32, 32, PD64>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
+  return dispatch_tile<T, 64, 64, 16, 32, 32, PD_64>(epi, a_kcontig, b_kcontig, a_vec, b_vec,
                                                     nsplit, p, s);
 }
 
@@ -560,12 +563,11 @@ hipError_t launch_dw_partial_group(int tile, bool b_vec, const GemmGroupT<T>& g,
     if ((int64_t)128 * ld * (int64_t)sizeof(T) >= (int64_t)TILE_OOB) return hipErrorInvalidValue;
   }
   // the tiles and stage depths of launch_gemm
-  constexpr int PD64 = sizeof(T) == 8 ? 4 : 8;
   if (tile == TILE_128x128)
-    return b_vec ? launch_group<T, 128, 128, 64, 32, 4, true>(g, nsplit, s)
-                 : launch_group<T, 128, 128, 64, 32, 4, false>(g, nsplit, s);
-  return b_vec ? launch_group<T, 64, 64, 32, 32, PD64, true>(g, nsplit, s)
-               : launch_group<T, 64, 64, 32, 32, PD64, false>(g, nsplit, s);
+    return b_vec ? launch_group<T, 128, 128, 64, 32, PD_128, true>(g, nsplit, s)
+                 : launch_group<T, 128, 128, 64, 32, PD_128, false>(g, nsplit, s);
+  return b_vec ? launch_group<T, 64, 64, 32, 32, PD_64, true>(g, nsplit, s)
+               : launch_group<T, 64, 64, 32, 32, PD_64, false>(g, nsplit, s);
 }
 
 template hipError_t launch_dw_partial_group<float>(int, bool, const GemmGroupT<float>&, const int*,
