@@ -23,7 +23,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnf.so")
-SOURCES = ["nf_api.hip", "nf_kernels.hip", "nf_narrow.hip", "nf_narrow64.hip", "nf_eval.hip"]
+SOURCES = ["nf_api.hip", "nf_kernels.hip", "nf_narrow.hip", "nf_narrow64.hip", "nf_medium.hip",
+           "nf_eval.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -392,7 +392,7 @@ nf_status run_forward(nf_net* n, const T* x, const T* y, int64_t batch, T* out, 
 // updated only after delta_{l-1}, which reads them, has been formed.
 template <class T>
 nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, int shards,
-                              hipStream_t s) {
+                              hipStream_t s, bool deltas_done = false) {
   const int L = num_layers(n);
   const T scale = (T)(eta / (double)batch);
   const int64_t shard_len = batch / shards;
@@ -453,7 +453,7 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
 
   for (int l = L; l >= 1; --l) {
     const LayerLayout& ly = n->layers[l];
-    if (l > 1) {
+    if (l > 1 && !deltas_done) {
       // delta_{l-1} = (delta_l W_l) * f'(z_{l-1}), with this step's W_l
       const LayerLayout& lp = n->layers[l - 1];
       nf::GemmParamsT<T> p{};
@@ -688,6 +688,95 @@ nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, do
 }
 
 // ---------------------------------------------------------------------------
+// medium fp32 networks: layer 1's contraction in k pieces, then the
+// per-sample kernel of csrc/nf_medium.hip for the rest of the forward pass and
+// every delta
+// ---------------------------------------------------------------------------
+// LDS placement of W_l, l >= 2 (see MediumParams); false when the net or the
+// batch does not qualify: every per-sample buffer of the pass (at most 16
+// pieces of [batch][<= 128] values) must span fewer than MEDIUM_OOB bytes
+bool medium_layout(const nf_net* n, int64_t batch, nf::MediumParams* p) {
+  const int L = num_layers(n);
+  if (n->dtype != nf::DT_F32 || L < 2 || L > nf::MEDIUM_MAX_LAYERS) return false;
+  if (batch * 16 * (nf::MEDIUM_WIDTH + 4) * 4 >= (int64_t)nf::MEDIUM_OOB) return false;
+  for (int l = 1; l <= L; ++l)
+    if (n->dims[l] > nf::MEDIUM_WIDTH) return false;
+  int off = 0;
+  for (int l = 2; l <= L; ++l) {
+    const int rows = (int)round_up(n->dims[l], 16), wp = (int)round_up(n->dims[l - 1], 16) + 4;
+    p->woff[l - 1] = off;
+    p->wrows[l - 1] = rows;
+    p->wp[l - 1] = wp;
+    off += rows * wp;
+  }
+  return off <= nf::MEDIUM_LDS_WEIGHTS;
+}
+
+nf_status medium_forward_deltas(nf_net* n, const float* x, const float* y, int64_t batch,
+                                hipStream_t s) {
+  nf::MediumParams mp{};
+  if (!medium_layout(n, batch, &mp)) return fail(NF_EINVAL, "internal: not a medium net");
+  const int L = num_layers(n);
+  const LayerLayout& l1 = n->layers[1];
+  float* P = cur_params<float>(n);
+
+  // layer 1: z_1 in k pieces (one piece when the tile grid fills the chip)
+  nf::GemmParamsT<float> p{};
+  p.A = x;
+  p.lda = n->dims[0];
+  p.B = P + l1.w_off;
+  p.ldb = l1.ldw;
+  p.M = (int)batch;
+  p.N = l1.out;
+  p.K = l1.in;
+  const int64_t tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
+  const int64_t want = 2 * (int64_t)(n->ncu > 0 ? n->ncu : 256);
+  int nsplit = 1;
+  if (tiles < want && p.K >= 256)
+    nsplit = (int)std::min<int64_t>({(want + tiles - 1) / tiles, p.K / 128, 16});
+  // pieces start on whole 16-input stages (see run_forward)
+  const int sub_len = (int)round_up((p.K + nsplit - 1) / nsplit, 16);
+  nsplit = (p.K + sub_len - 1) / sub_len;
+  const int64_t ldz = round_up(p.N, 4);
+  const int64_t zstride = round_up((int64_t)p.M * ldz, kAlign);
+  nf_status st = ensure_partial(n, nsplit * zstride);
+  if (st != NF_OK) return st;
+  p.shard_len = p.K;
+  p.nsub = nsplit;
+  p.sub_len = sub_len;
+  p.partial = as<float>(n->partial);
+  p.pstride = zstride;
+  p.ld0 = ldz;
+  const bool av = vec_ok(x, n->dims[0]);
+  st = launch<float>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, p, s, nf::TILE_64x64);
+  if (st != NF_OK) return st;
+
+  mp.B = (int)batch;
+  mp.L = L;
+  for (int l = 0; l <= L; ++l) mp.dims[l] = n->dims[l];
+  mp.zp = p.partial;
+  mp.zstride = zstride;
+  mp.ldz = ldz;
+  mp.np = nsplit;
+  mp.Y = y;
+  double by = 4.0 * ((double)nsplit * batch * p.N + (double)batch * n->dims[L]), fl = 0.0;
+  for (int l = 1; l <= L; ++l) {
+    const LayerLayout& ly = n->layers[l];
+    mp.acts[l - 1] = ly.act;
+    mp.W[l - 1] = P + ly.w_off;
+    mp.ldw[l - 1] = ly.ldw;
+    mp.bias[l - 1] = P + ly.b_off;
+    mp.A[l - 1] = as<float>(n->actv[l]);
+    mp.D[l - 1] = as<float>(n->dbuf[l]);
+    mp.lda[l - 1] = ly.lda;
+    by += 4.0 * ((double)batch * ly.out * (l < L ? 2 : 1) + (l >= 2 ? (double)ly.out * ly.in : 0));
+    if (l >= 2) fl += 4.0 * batch * (double)ly.out * ly.in;   // forward and delta products
+  }
+  return timed(n, "medium_fwd_deltas", by, fl, s,
+               [&] { return nf::launch_medium(mp, n->ncu > 0 ? n->ncu : 256, s); });
+}
+
+// ---------------------------------------------------------------------------
 // the step and inference in element type T
 // ---------------------------------------------------------------------------
 template <class T>
@@ -695,8 +784,14 @@ nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double et
                      hipStream_t s) {
   nf_status st;
   const bool narrow = shards == 1 && narrow_rows_ok<T>(n, x);
+  nf::MediumParams mp{};
   if (narrow) {
     st = narrow_train_step<T>(n, x, y, batch, eta, s);
+  } else if (sizeof(T) == 4 && medium_layout(n, batch, &mp)) {
+    if constexpr (sizeof(T) == 4) {
+      st = medium_forward_deltas(n, x, y, batch, s);
+      if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s, true);
+    }
   } else {
     st = run_forward<T>(n, x, y, batch, nullptr, true, s);
     if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s);

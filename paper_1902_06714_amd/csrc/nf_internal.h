@@ -205,6 +205,41 @@ hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hipStream_t s);
 hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// Medium networks (fp32): 2..MEDIUM_MAX_LAYERS layers, every layer after the
+// input at most MEDIUM_WIDTH units, the weights of layers 2..L within
+// MEDIUM_LDS_WEIGHTS floats of LDS as padded below.  Layer 1's contraction
+// writes its k pieces; one per-sample kernel does the rest of the forward
+// pass and every delta.
+// ---------------------------------------------------------------------------
+constexpr int MEDIUM_MAX_LAYERS = 4;
+constexpr int MEDIUM_WIDTH = 128;
+constexpr int MEDIUM_LDS_WEIGHTS = 24576;
+// every per-sample buffer the medium pass reads or writes ([np][B][ldz],
+// [B][d_L], [B][lda_l]) spans fewer bytes than this: offsets at or past it
+// address nothing, so lanes off the tile load zeros and drop their stores
+constexpr unsigned MEDIUM_OOB = 0x7fff0000u;
+
+struct MediumParams {
+  int B, L;
+  int dims[MEDIUM_MAX_LAYERS + 1];
+  int acts[MEDIUM_MAX_LAYERS];
+  const float* zp;                         // layer 1's pieces [np][B][ldz]
+  int64_t zstride, ldz;
+  int np;
+  const float* W[MEDIUM_MAX_LAYERS];       // W_l (index l-1), device layout
+  int64_t ldw[MEDIUM_MAX_LAYERS];
+  const float* bias[MEDIUM_MAX_LAYERS];
+  const float* Y;                          // targets [B][d_L]
+  float* A[MEDIUM_MAX_LAYERS];             // f(z_l) [B][lda_l], l = 1..L-1
+  float* D[MEDIUM_MAX_LAYERS];             // delta_l [B][lda_l], l = 1..L
+  int64_t lda[MEDIUM_MAX_LAYERS];
+  // W_l, l >= 2, in LDS at woff[l-1] as wrows[l-1] = round_up(d_l, 16) rows
+  // of wp[l-1] = round_up(d_{l-1}, 16) + 4 floats, zero past the layer sizes
+  int woff[MEDIUM_MAX_LAYERS], wrows[MEDIUM_MAX_LAYERS], wp[MEDIUM_MAX_LAYERS];
+};
+hipError_t launch_medium(const MediumParams& p, int ncu, hipStream_t s);
+
 // Adds to *count the number of rows s < n for which out[s][0..d) and
 // y[s][0..d) have their first largest entry at the same index (rows holding a
 // NaN never count).  Row pitches ldo and ldy in elements.

@@ -1,0 +1,402 @@
+// Per-sample pass for fp32 networks whose layers after the input have at most
+// 128 units (e.g. 784-100-100-10).  Layer 1's contraction runs before it
+// (its k pieces in the piece buffer); then each workgroup of 12 waves, for
+// tiles of 16 NSB samples,
+//   folds layer 1's pieces in piece order, adds b_1 and applies f_1;
+//   runs layers 2..L with the weights of layers 2..L staged in LDS;
+//   forms the output delta (a_L - y) f'(z_L) and the hidden deltas
+//   (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with the weights of this
+//   step;
+// and stores the activations and deltas the tendency kernels read.  Every
+// product is on the 16x16x4 fp32 matrix cores.  The work of a layer is split
+// into jobs of 16 units x 16 samples, handed to the waves round robin; a
+// layer's forward product and its delta use the same jobs, so the lane that
+// formed f'(z_l) for a (sample, unit) forms that delta and keeps f' in
+// registers.  Sums run in a fixed order, so results are reproducible bit for
+// bit.
+//
+// Workgroups are persistent (one per CU): the weights are staged once, and
+// the layer-1 pieces and targets of a workgroup's next tile are loaded while
+// it works on the current one.  Per-sample loads and stores go through buffer
+// resources, with lanes off the tile given an offset past the end, so every
+// lane issues the same memory instructions and a wait for a prefetched value
+// never waits for the stores issued after it.  A lane's offsets are 32-bit:
+// its place in the tile in the vector offset, the tile's in the scalar one.
+#include <type_traits>
+
+#include "nf_act.h"
+#include "nf_internal.h"
+
+namespace nf {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+constexpr int M_WAVES = 12;
+constexpr int M_THREADS = M_WAVES * 64;
+constexpr int M_HP = MEDIUM_WIDTH + 4;  // LDS row pitch of activations and deltas
+constexpr int M_PF = 2;                 // layer-1 pieces loaded ahead per tile
+constexpr int M_SROWS = M_THREADS / 32; // weight rows per load: 32 lanes x 16 bytes a row
+constexpr int M_STAGE = 8;              // weight loads in flight per thread
+
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)MEDIUM_OOB,
+                                           0x00020000);
+}
+__device__ inline float bload(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+__device__ inline void bstore(float v, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)voff, (int)soff,
+                                        0);
+}
+
+// calls f with the activation as a compile-time constant, so the code of one
+// phase holds one activation's arithmetic, not a switch per element
+template <class F>
+__device__ __forceinline__ void with_act(int act, F&& f) {
+  switch (act) {
+    case ACT_SIGMOID: f(std::integral_constant<int, ACT_SIGMOID>{}); break;
+    case ACT_TANH: f(std::integral_constant<int, ACT_TANH>{}); break;
+    case ACT_RELU: f(std::integral_constant<int, ACT_RELU>{}); break;
+    case ACT_GAUSSIAN: f(std::integral_constant<int, ACT_GAUSSIAN>{}); break;
+    default: f(std::integral_constant<int, ACT_STEP>{}); break;
+  }
+}
+
+}  // namespace
+
+template <int NSB, int L>
+__global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p) {
+  constexpr int TS = 16 * NSB;                       // samples per tile
+  constexpr int NJ = (8 * NSB + M_WAVES - 1) / M_WAVES;  // jobs per wave at most
+  __shared__ __attribute__((aligned(16))) float wl[MEDIUM_LDS_WEIGHTS];  // W_2 .. W_L, padded
+  __shared__ float hs[2][TS][M_HP];                                      // activations, deltas
+  __shared__ float bl[L][MEDIUM_WIDTH];                                  // b_1 .. b_L
+  __shared__ float4 spare;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, g = lane >> 4;
+  const int ntiles = (p.B + TS - 1) / TS;
+  const int d1 = p.dims[1], dL = p.dims[L];
+  const int ldz = (int)p.ldz;
+
+  // job jj of this wave in a layer of d units: job = wave + 12 jj, unit block
+  // job / NSB, sample block job % NSB; lane (r, g) holds unit 16 ub + r and,
+  // in accumulator register v, tile row 16 sb + 4 g + v
+  auto has_job = [&](int jj, int d) { return wave + M_WAVES * jj < ((d + 15) >> 4) * NSB; };
+  auto unit = [&](int jj) { return 16 * ((wave + M_WAVES * jj) / NSB) + r; };
+  auto row = [&](int jj) { return 16 * ((wave + M_WAVES * jj) % NSB) + 4 * g; };
+
+  const __amdgpu_buffer_rsrc_t zres = rsrc(p.zp), yres = rsrc(p.Y);
+
+  // layer-1 pieces 0 .. M_PF-1 and the targets of tile tt (a tile past the
+  // last loads nothing: every row is past the batch, and its scalar offsets
+  // are the last tile's)
+  float pz[M_PF][NJ][4], py[NJ][4];
+  auto load_z = [&](int tt) {
+    const int rem = p.B - tt * TS, tc = tt < ntiles ? tt : ntiles - 1;
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+      if (!has_job(jj, d1)) break;
+      const int u = unit(jj), rw = row(jj);
+      const unsigned vb = 4u * (unsigned)(rw * ldz + u);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const bool ok = u < d1 && rw + v < rem;
+#pragma unroll
+        for (int q = 0; q < M_PF; ++q) {
+          const int qq = q < p.np ? q : 0;
+          pz[q][jj][v] = bload(zres, ok ? vb : MEDIUM_OOB,
+                               4u * (unsigned)((tc * TS + v) * ldz + qq * (int)p.zstride));
+        }
+      }
+    }
+  };
+  auto load_y = [&](int tt) {
+    const int rem = p.B - tt * TS, tc = tt < ntiles ? tt : ntiles - 1;
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+      if (!has_job(jj, dL)) break;
+      const int u = unit(jj), rw = row(jj);
+      const unsigned vb = 4u * (unsigned)(rw * dL + u);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const bool ok = u < dL && rw + v < rem;
+        py[jj][v] = bload(yres, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((tc * TS + v) * dL));
+      }
+    }
+  };
+  load_z(blockIdx.x);
+  load_y(blockIdx.x);
+
+  // b_l into LDS, zero past d_l (128 threads, two whole waves, per layer)
+  if (tid < L * MEDIUM_WIDTH) {
+    const int l = __builtin_amdgcn_readfirstlane(tid / MEDIUM_WIDTH) + 1, u = tid % MEDIUM_WIDTH;
+    const bool ok = u < p.dims[l];
+    const float b = p.bias[l - 1][ok ? u : 0];
+    bl[l - 1][u] = ok ? b : 0.0f;
+  }
+
+  // the weights of layers 2..L into LDS: 32 lanes per row, 16 bytes each.
+  // Staged row R (over the layers' padded rows in order) is row j of layer l;
+  // rows of the device layout are 16-byte aligned with a zero-filled pitch,
+  // and rows past d_l and columns past that pitch are stored as zeros, so
+  // every product below runs over whole 16-unit blocks (the 4 columns of
+  // bank padding at the end of each LDS row are never read)
+  {
+    int rend[L];  // staged rows of layers 2..l
+    rend[1] = p.wrows[1];
+#pragma unroll
+    for (int l = 3; l <= L; ++l) rend[l - 1] = rend[l - 2] + p.wrows[l - 1];
+    const int rtot = rend[L - 1];
+    const int c = 4 * (lane & 31);
+    for (int R0 = tid >> 5; R0 < rtot; R0 += M_SROWS * M_STAGE) {
+      float4 v[M_STAGE];
+      int dst[M_STAGE];
+#pragma unroll
+      for (int i = 0; i < M_STAGE; ++i) {
+        const int R = R0 + i * M_SROWS;
+        int li = 1, r0 = 0;
+#pragma unroll
+        for (int l = 3; l <= L; ++l)
+          if (R >= rend[l - 2]) li = l - 1, r0 = rend[l - 2];
+        const int j = R - r0;
+        // the layer's figures by selects (li differs between lanes)
+        auto pick = [&](auto a1, auto a2, auto a3) { return li == 1 ? a1 : li == 2 ? a2 : a3; };
+        const int wp = pick(p.wp[1], p.wp[2], p.wp[3]);
+        const int ldw = (int)pick(p.ldw[1], p.ldw[2], p.ldw[3]);
+        const int dl = pick(p.dims[2], p.dims[3], p.dims[4]);
+        const float* W = pick(p.W[1], p.W[2], p.W[3]);
+        const bool in = R < rtot && c < wp - 4;
+        const bool ok = in && j < dl && c < ldw;
+        const float4 x = *reinterpret_cast<const float4*>(ok ? W + (int64_t)j * ldw + c : p.W[1]);
+        v[i] = ok ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+        dst[i] = in ? pick(p.woff[1], p.woff[2], p.woff[3]) + j * wp + c : -1;
+      }
+      // rows past the last layer and columns past the padded width go to a
+      // spare slot, so no load is tied to a branch
+#pragma unroll
+      for (int i = 0; i < M_STAGE; ++i)
+        *(dst[i] >= 0 ? reinterpret_cast<float4*>(wl + dst[i]) : &spare) = v[i];
+    }
+  }
+  __syncthreads();  // weights and biases in LDS
+
+  float fp[L - 1][NJ][4];  // f'(z_l), l < L
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int s0 = t * TS, rem = p.B - s0;
+
+    // ---- layer 1: the pieces of z_1 in piece order, + b_1, f_1
+    {
+      float zs[NJ][4];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          zs[jj][v] = pz[0][jj][v];
+#pragma unroll
+          for (int q = 1; q < M_PF; ++q)
+            if (q < p.np) zs[jj][v] += pz[q][jj][v];
+        }
+      // pieces past those loaded ahead (small batches cut into many pieces)
+      for (int q = M_PF; q < p.np; ++q) {
+        float tq[NJ][4];
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, d1)) break;
+          const int u = unit(jj), rw = row(jj);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const bool ok = u < d1 && rw + v < rem;
+            tq[jj][v] = bload(zres, ok ? 4u * (unsigned)(rw * ldz + u) : MEDIUM_OOB,
+                              4u * (unsigned)((s0 + v) * ldz + q * (int)p.zstride));
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) zs[jj][v] += tq[jj][v];
+      }
+      load_z(t + gridDim.x);
+      const __amdgpu_buffer_rsrc_t ares = rsrc(p.A[0]);
+      const int lda = (int)p.lda[0];
+      with_act(p.acts[0], [&](auto act) {
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, d1)) break;
+          const int u = unit(jj), rw = row(jj);
+          const unsigned vb = 4u * (unsigned)(rw * lda + u);
+          const float b = bl[0][u];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const bool ok = u < d1 && rw + v < rem;
+            float a, f;
+            act_eval(decltype(act)::value, zs[jj][v] + b, a, f);
+            a = ok ? a : 0.0f;
+            bstore(a, ares, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((s0 + v) * lda));
+            hs[0][rw + v][u] = a;
+            fp[0][jj][v] = f;
+          }
+        }
+      });
+    }
+    __syncthreads();
+
+    // ---- layers 2..L: z_l = W_l a_{l-1} + b_l; at l = L the output delta
+    int cur = 0;
+#pragma unroll
+    for (int l = 2; l <= L; ++l) {
+      const int N = p.dims[l], Kp = (p.dims[l - 1] + 15) & ~15;
+      const int wp = p.wp[l - 1];
+      const float* w = wl + p.woff[l - 1];
+      floatx4 acc[NJ];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) acc[jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+      // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with input
+      // k0 + 4 i + g; inputs past d_{l-1} are zero on both sides up to the
+      // next multiple of 16
+      for (int k0 = 0; k0 < Kp; k0 += 16) {
+        float xa[NJ][4], wb[NJ][4];
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, N)) break;
+          const int xr = row(jj) - 4 * g + r;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            wb[jj][i] = w[unit(jj) * wp + k0 + 4 * i + g];
+            xa[jj][i] = hs[cur][xr][k0 + 4 * i + g];
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, N)) break;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[jj][i], wb[jj][i], acc[jj], 0, 0, 0);
+        }
+      }
+      const __amdgpu_buffer_rsrc_t ores = rsrc(l < L ? p.A[l - 1] : p.D[l - 1]);
+      const int lda = (int)p.lda[l - 1];
+      with_act(p.acts[l - 1], [&](auto act) {
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, N)) break;
+          const int u = unit(jj), rw = row(jj);
+          const unsigned vb = 4u * (unsigned)(rw * lda + u);
+          const float b = bl[l - 1][u];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const bool ok = u < N && rw + v < rem;
+            const unsigned so = 4u * (unsigned)((s0 + v) * lda);
+            float a, f;
+            act_eval(decltype(act)::value, acc[jj][v] + b, a, f);
+            if (l < L) {
+              a = ok ? a : 0.0f;
+              bstore(a, ores, ok ? vb : MEDIUM_OOB, so);
+              hs[cur ^ 1][rw + v][u] = a;
+              fp[l - 1][jj][v] = f;
+            } else {
+              const float d = ok ? (a - py[jj][v]) * f : 0.0f;
+              bstore(d, ores, ok ? vb : MEDIUM_OOB, so);
+              hs[cur ^ 1][rw + v][u] = d;
+            }
+          }
+        }
+      });
+      if (l == L) load_y(t + gridDim.x);
+      cur ^= 1;
+      __syncthreads();
+    }
+
+    // ---- hidden deltas, l = L-1 .. 1: (W_{l+1}^T delta_{l+1}) * f'(z_l).
+    // Phases so far flipped the LDS buffers 2L - 3 times, so layer 1's delta
+    // reads buffer 1 and the next tile's layer 1 may write buffer 0 without
+    // another barrier.
+#pragma unroll
+    for (int l = L - 1; l >= 1; --l) {
+      const int N = p.dims[l], Kp = (p.dims[l + 1] + 15) & ~15;
+      const int wp = p.wp[l];
+      const float* w = wl + p.woff[l];
+      floatx4 acc[NJ];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) acc[jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+      // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with unit
+      // k0 + 4 i + g of layer l + 1 (zero on both sides past d_{l+1})
+      for (int k0 = 0; k0 < Kp; k0 += 16) {
+        float xa[NJ][4], wb[NJ][4];
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, N)) break;
+          const int xr = row(jj) - 4 * g + r;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            wb[jj][i] = w[(k0 + 4 * i + g) * wp + unit(jj)];
+            xa[jj][i] = hs[cur][xr][k0 + 4 * i + g];
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+          if (!has_job(jj, N)) break;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[jj][i], wb[jj][i], acc[jj], 0, 0, 0);
+        }
+      }
+      const __amdgpu_buffer_rsrc_t dres = rsrc(p.D[l - 1]);
+      const int lda = (int)p.lda[l - 1];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) {
+        if (!has_job(jj, N)) break;
+        const int u = unit(jj), rw = row(jj);
+        const unsigned vb = 4u * (unsigned)(rw * lda + u);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool ok = u < N && rw + v < rem;
+          const float d = ok ? acc[jj][v] * fp[l - 1][jj][v] : 0.0f;
+          bstore(d, dres, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((s0 + v) * lda));
+          if (l > 1) hs[cur ^ 1][rw + v][u] = d;
+        }
+      }
+      cur ^= 1;
+      if (l > 1) __syncthreads();
+    }
+  }
+}
+
+// 16-sample blocks per tile: enough for one tile per CU where that takes at
+// most 3 (3 blocks of 128 padded units fill LDS beside the largest weights);
+// bigger batches run several rounds of tiles
+static int medium_tile_blocks(int B, int ncu) {
+  const int blocks = (B + 15) / 16;
+  const int nsb = (blocks + ncu - 1) / ncu;
+  return nsb < 1 ? 1 : nsb > 3 ? 3 : nsb;
+}
+
+template <int NSB>
+static void launch_nsb(const MediumParams& p, dim3 grid, hipStream_t s) {
+  switch (p.L) {
+    case 2: medium_kernel<NSB, 2><<<grid, M_THREADS, 0, s>>>(p); break;
+    case 3: medium_kernel<NSB, 3><<<grid, M_THREADS, 0, s>>>(p); break;
+    default: medium_kernel<NSB, 4><<<grid, M_THREADS, 0, s>>>(p); break;
+  }
+}
+
+hipError_t launch_medium(const MediumParams& p, int ncu, hipStream_t s) {
+  if (p.L < 2 || p.L > MEDIUM_MAX_LAYERS) return hipErrorInvalidValue;
+  const int nsb = medium_tile_blocks(p.B, ncu);
+  const int ntiles = (p.B + 16 * nsb - 1) / (16 * nsb);
+  const dim3 grid(ntiles < ncu ? ntiles : ncu);
+  switch (nsb) {
+    case 1: launch_nsb<1>(p, grid, s); break;
+    case 2: launch_nsb<2>(p, grid, s); break;
+    default: launch_nsb<3>(p, grid, s); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nf

@@ -106,6 +106,29 @@ def test_narrow_edges(dims, acts, batch):
     _compare_trajectory(dims, acts, theta, X, Y, batch, 1.0, 1, 2)
 
 
+# the per-sample pass for fp32 networks of 2 to 4 layers up to 128 units
+# wide: tiles of one, two and three 16-sample blocks (the tile grows with the
+# batch: over 4096 and over 8192 samples), several rounds of tiles per
+# workgroup (past 12288 samples), more layer-1 pieces than are loaded ahead
+# (small batches), widths that are not multiples of 16, one-unit layers, and
+# weights of layers 2..L near the LDS limit
+MEDIUM_EDGES = [
+    ((784, 100, 100, 10), ("tanh", "tanh", "sigmoid"), 100, 4, 1.0),
+    ((300, 120, 10), ("sigmoid",), 5, 1, 2.0),
+    ((50, 128, 128, 10), ("tanh", "gaussian", "sigmoid"), 4098, 3, 0.5),
+    ((33, 128, 1), ("sigmoid",), 8200, 1, 2.0),
+    ((20, 17, 31, 45, 7), ("tanh", "sigmoid", "gaussian", "sigmoid"), 13000, 2, 0.5),
+    ((40, 128, 96, 64, 32), ("gaussian", "tanh", "sigmoid", "tanh"), 700, 1, 0.5),
+    ((1, 1, 1), ("tanh",), 300, 1, 0.5),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards,eta", MEDIUM_EDGES)
+def test_medium_edges(dims, acts, batch, shards, eta):
+    theta, X, Y = _problem(dims, 3 * sum(dims) + batch, batch * 3)
+    _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 3)
+
+
 RELU_SMALL = [
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 1, 0.2),
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 4, 0.2),
@@ -139,9 +162,9 @@ def test_small_relu_elementwise(dims, acts, batch, shards, eta):
 
 def test_narrow_and_general_paths_agree():
     """A narrow network trained with one shard (its own two-kernel path) and
-    with two shards (the general contraction path) differs only by rounding.
-    The two paths add the 784 products of a layer-1 sum in different orders
-    (the general path in k pieces), which moves a sum by about sqrt(784) *
+    with two shards (layer 1's contraction in k pieces, then the per-sample
+    pass) differs only by rounding.  The two paths add the 784 products of a
+    layer-1 sum in different orders, which moves a sum by about sqrt(784) *
     2^-24 = 1.7e-6 of its magnitude; the gate is 1e-5 for parameters and
     tendencies alike."""
     dims = (784, 30, 10)
