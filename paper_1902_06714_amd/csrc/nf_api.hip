@@ -573,7 +573,8 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
 // 16 / sizeof(T) elements and a 16-byte aligned base
 template <class T>
 bool narrow_rows_ok(const nf_net* n, const T* x) {
-  return n->narrow && n->dims[0] % (16 / (int)sizeof(T)) == 0 && vec_ok(x, n->dims[0]);
+  return n->narrow && n->dims[0] % (16 / (int)sizeof(T)) == 0 && vec_ok(x, n->dims[0]) &&
+         (int64_t)n->dims[0] * nf::NARROW_WIDTH * (int64_t)sizeof(T) < (int64_t)nf::NARROW_OOB;
 }
 
 template <class T>

@@ -147,6 +147,10 @@ constexpr int NARROW_TILE = 16;       // samples per workgroup of the per-sample
 // batches up to this size take 4-sample workgroups (enough of them to fill
 // the chip); larger ones take NARROW_TILE-sample workgroups
 constexpr int NARROW_SMALL_BATCH = 2048;
+// the narrow kernels read W_1 and input rows through buffer resources; the
+// host keeps those ranges (at most NARROW_WIDTH rows of d_0 values) below
+// this many bytes, and offsets at or past it read as zeros
+constexpr unsigned NARROW_OOB = 0x40000000u;
 
 // Parameter layout of narrow nets: W_1 is [NARROW_WIDTH][ldw_1] and W_l, l >= 2,
 // is [NARROW_WIDTH][NARROW_WIDTH]; biases are NARROW_WIDTH long; rows, columns

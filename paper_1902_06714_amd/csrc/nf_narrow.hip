@@ -30,6 +30,10 @@ __device__ __forceinline__ float4 keep_if(bool c, float4 v) {
   return make_float4(c ? v.x : 0.0f, c ? v.y : 0.0f, c ? v.z : 0.0f, c ? v.w : 0.0f);
 }
 
+// A buffer offset past every range the narrow kernels read through buffer
+// resources: a load there returns zeros without touching memory.
+constexpr unsigned NB_OOB = NARROW_OOB;
+
 constexpr int N1_WAVES = 8;
 constexpr int N1_KC = 16 * N1_WAVES;  // inputs per LDS stage: one 16-wide group per wave
 constexpr int N1_KP = N1_KC + 4;      // padded LDS row
@@ -359,12 +363,16 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
 
   {
     const int b = lane >> 2, q = lane & 3;
-    const bool xrow_ok = s0 + q < p.B;
-    const float* xsrc = p.X + (int64_t)(xrow_ok ? s0 + q : p.B - 1) * p.d0;
-    // W_1 rows are padded to 32 with zeros
-    const float* wsrc[N4_UG];
-#pragma unroll
-    for (int ug = 0; ug < N4_UG; ++ug) wsrc[ug] = p.W[0] + (int64_t)(4 * ug + q) * p.ldw[0];
+    // the tile's input rows and W_1's d_1 rows through buffer resources that
+    // end at the last row: rows past the batch, W_1's padding rows and inputs
+    // past the width (given an offset past the end) read as zeros without a
+    // memory access, so no bytes go to loads whose values are not used
+    const int nrows = p.B - s0 < T ? p.B - s0 : T;
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.X + (int64_t)s0 * p.d0), (short)0, nrows * p.d0 * 4, 0x00020000);
+    const int ldw1 = (int)p.ldw[0];
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)p.W[0], (short)0, p.dims[1] * ldw1 * 4, 0x00020000);
     floatx4 acc[N4_UG];
 #pragma unroll
     for (int ug = 0; ug < N4_UG; ++ug) acc[ug] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -385,12 +393,16 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
         if (t < nsteps) t = t + rot < nsteps ? t + rot : t + rot - nsteps;
         const int k = t * N4_KS + 4 * b;
         const bool ok = k < p.d0;
-        const int kc = ok ? k : 0;
-        xr[u] = keep_if(ok && xrow_ok, *reinterpret_cast<const float4*>(xsrc + kc));
+        xr[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               xres, ok ? 4 * (q * p.d0 + k) : (int)NB_OOB, 0, 0));
 #pragma unroll
         for (int ug = 0; ug < N4_UG; ++ug)
-          wr[u][ug] = keep_if(ok, *reinterpret_cast<const float4*>(wsrc[ug] + kc));
+          wr[u][ug] = __builtin_bit_cast(
+              float4, __builtin_amdgcn_raw_buffer_load_b128(
+                          wres, ok ? 4 * ((4 * ug + q) * ldw1 + k) : (int)NB_OOB, 0, 0));
       }
+      // keep every load of the block ahead of the first matrix instruction
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < N4_PRE; ++u) {
 #pragma unroll
@@ -454,7 +466,7 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
 constexpr int NI_CH = 16;                  // inputs per chunk: a float4 per lane group
 constexpr int NI_SLOTS = 3;                // tiles of inputs held: the current one + two ahead
 constexpr int NI_ROUND = 5 * NI_SLOTS;     // tiles whose outputs are staged in LDS
-constexpr unsigned NI_OOB = 0x40000000u;   // an offset past every input range
+constexpr unsigned NI_OOB = NB_OOB;
 
 template <int MC>
 __global__ void __launch_bounds__(N1_WAVES * 64) narrow_infer_kernel(const NarrowFwdParams p) {
