@@ -207,6 +207,30 @@ def test_hand_worked_networks_on_gpu():
                 np.testing.assert_allclose(p, want_p, rtol=1e-6, atol=1e-7)
 
 
+@pytest.mark.parametrize("act", ["tanh", "sigmoid"])
+@pytest.mark.parametrize("d0", [1, 4])   # the contraction kernels; the narrow kernels
+def test_activation_ulp(act, d0):
+    """f(z) of the fp32 kernels against the fp64 closed forms, in ulp of the
+    fp32 value, over z in [-20, 20] and densely near 0, where tanh switches
+    from its series to the exponential form at |z| = 1/2. The network
+    d0-1 with W_1 = (1, 0, ...) and b_1 = 0 gives z = x exactly."""
+    z = np.concatenate([np.linspace(-20, 20, 20001), np.geomspace(1e-6, 1, 2001),
+                        -np.geomspace(1e-6, 1, 2001), [0.0, 0.5, -0.5]]).astype(np.float32)
+    theta = np.zeros(d0 + 1, np.float32)
+    theta[0] = 1.0
+    X = np.zeros((len(z), d0), np.float32)
+    X[:, 0] = z
+    note(f"activation ulp act={act} d0={d0}")
+    with GpuNet((d0, 1), (act,), theta) as net:
+        out = net.forward(to_dev(X))[:, 0].astype(np.float64)
+    zz = z.astype(np.float64)
+    ref = np.tanh(zz) if act == "tanh" else 1.0 / (1.0 + np.exp(-zz))
+    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    err = np.abs(out - ref) / ulp
+    i = int(np.argmax(err))
+    assert err[i] <= 4.0, (act, float(err[i]), float(z[i]))
+
+
 @pytest.mark.parametrize("dims,acts,n", [
     ((37, 133, 65, 7), ("tanh", "relu", "gaussian"), 1000),
     ((784, 30, 10), ("sigmoid",), 1000),
