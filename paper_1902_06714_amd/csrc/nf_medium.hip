@@ -134,13 +134,17 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
   load_z(blockIdx.x);
   load_y(blockIdx.x);
 
-  // b_l into LDS, zero past d_l (128 threads, two whole waves, per layer)
-  if (tid < L * MEDIUM_WIDTH) {
-    const int l = __builtin_amdgcn_readfirstlane(tid / MEDIUM_WIDTH) + 1, u = tid % MEDIUM_WIDTH;
-    const bool ok = u < p.dims[l];
-    const float b = p.bias[l - 1][ok ? u : 0];
-    bl[l - 1][u] = ok ? b : 0.0f;
-  }
+  // b_l for LDS, zero past d_l (128 threads, two whole waves, per layer).  The
+  // load issues here, with the others; the value goes to LDS after the weight
+  // loads have issued, so the prologue waits for memory once.
+  const int bl_u = tid % MEDIUM_WIDTH;
+  const bool bl_mine = tid < L * MEDIUM_WIDTH;
+  // MEDIUM_WIDTH threads are whole waves: the layer is uniform in a wave, so
+  // its size and bias pointer come from scalar loads
+  const int bl_w = __builtin_amdgcn_readfirstlane(tid / MEDIUM_WIDTH) + 1;
+  const int bl_l = bl_w < L ? bl_w : L;
+  const bool bl_ok = bl_mine && bl_u < p.dims[bl_l];
+  const float bl_v = p.bias[bl_l - 1][bl_ok ? bl_u : 0];
 
   // the weights of layers 2..L into LDS: 32 lanes per row, 16 bytes each.
   // Staged row R (over the layers' padded rows in order) is row j of layer l;
@@ -185,6 +189,7 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         *(dst[i] >= 0 ? reinterpret_cast<float4*>(wl + dst[i]) : &spare) = v[i];
     }
   }
+  if (bl_mine) bl[bl_l - 1][bl_u] = bl_ok ? bl_v : 0.0f;
   __syncthreads();  // weights and biases in LDS
 
   float fp[L - 1][NJ][4];  // f'(z_l), l < L

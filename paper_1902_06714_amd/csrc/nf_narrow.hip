@@ -193,17 +193,18 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
   if (!TRAIN) return;
 
   // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+  // (layer 1's delta is read by no later phase: no LDS copy, no barrier)
 #pragma unroll
   for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
     if (l >= p.L) continue;
     if (active) {
       const float t = dot32(wsT[l - 1][j], hs[cur][s]);
       const float d = j < p.dims[l] ? t * fp[l - 1] : 0.0f;
-      hs[cur ^ 1][s][j] = d;
+      if (l > 1) hs[cur ^ 1][s][j] = d;
       if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
     }
     cur ^= 1;
-    __syncthreads();
+    if (l > 1) __syncthreads();
   }
 }
 

@@ -197,15 +197,16 @@ __global__ void __launch_bounds__(D_WAVES * 64) narrow64_fwd_kernel(const Narrow
   if (!TRAIN) return;
 
   // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+  // (layer 1's delta is read by no later phase: no LDS copy, no barrier)
 #pragma unroll
   for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
     if (l >= p.L) continue;
     const double t = dot32d(wsT[l - 1][j], hs[cur][s]);
     const double d = j < p.dims[l] ? t * fp[l - 1] : 0.0;
-    hs[cur ^ 1][s][j] = d;
+    if (l > 1) hs[cur ^ 1][s][j] = d;
     if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
     cur ^= 1;
-    __syncthreads();
+    if (l > 1) __syncthreads();
   }
 }
 
