@@ -71,7 +71,12 @@ struct alignas(16) Vec16 {
 
 // Global -> register -> LDS staging of one R x BK operand tile X(r, k),
 // r in [r0, r0 + R), k in [k0, k0 + BK).  In LDS the tile is k-major,
-// lds[k * (R + 4) + r], which is the order the MFMA operand reads want.
+// lds[k * SR + r], which is the order the MFMA operand reads want.  The row
+// pitch SR is R + 4 when the tile arrives mn-contiguous (16-byte stores stay
+// aligned) and R + 2 when it arrives k-contiguous: each thread then scatters
+// a 16-byte load over 4 consecutive k rows, and with R + 2 the four row groups
+// a wave writes at once fall in different banks (R + 4 put rows k and k + 8
+// in the same ones).
 // KC: k is the contiguous index in memory (X[r*ld + k]), else X[k*ld + r].
 // VEC: rows are 16-byte aligned with a pitch that is a multiple of VW and the
 // pitch padding is zero, so aligned 16-byte loads are safe.
@@ -85,7 +90,7 @@ constexpr unsigned TILE_OOB = 0x7ffffff0u;   // the buffers' length in bytes
 template <class T, int R, int BK, int NT, bool KC, bool VEC>
 struct TileLoader {
   static constexpr int VW = Vec16<T>::N;
-  static constexpr int SR = R + 4;
+  static constexpr int SR = R + (KC ? 2 : 4);
   static constexpr int NV = VEC ? (R * BK / VW) / NT : (R * BK) / NT;
   static_assert(VEC ? (R * BK / VW) % NT == 0 : (R * BK) % NT == 0, "tile not divisible");
   Vec16<T> v[VEC ? NV : 1];
@@ -178,7 +183,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParamsT<T>& p, int bx, int b
   using MM = Mma<T>;
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   constexpr int TM = WM / MM::BLK, TN = WN / MM::BLK;
-  constexpr int SA = BM + 4, SB = BN + 4;
+  // LDS row pitches, as in TileLoader
+  constexpr int SA = BM + (AKC ? 2 : 4), SB = BN + (BKC ? 2 : 4);
   __shared__ __attribute__((aligned(16))) T As[2][BK * SA];
   __shared__ __attribute__((aligned(16))) T Bs[2][BK * SB];
 
