@@ -704,7 +704,10 @@ bool medium_layout(const nf_net* n, int64_t batch, nf::MediumParams* p) {
     if (n->dims[l] > nf::MEDIUM_WIDTH) return false;
   int off = 0;
   for (int l = 2; l <= L; ++l) {
-    const int rows = (int)round_up(n->dims[l], 16), wp = (int)round_up(n->dims[l - 1], 16) + 4;
+    // pitch 18 mod 32 floats: both the row-wise (forward) and the
+    // column-wise (delta) operand reads of a half-wave hit distinct banks
+    const int cw = (int)round_up(n->dims[l - 1], 16);
+    const int rows = (int)round_up(n->dims[l], 16), wp = cw + (cw % 32 == 0 ? 18 : 2);
     p->woff[l - 1] = off;
     p->wrows[l - 1] = rows;
     p->wp[l - 1] = wp;

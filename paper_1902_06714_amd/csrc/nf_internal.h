@@ -239,7 +239,8 @@ struct MediumParams {
   float* D[MEDIUM_MAX_LAYERS];             // delta_l [B][lda_l], l = 1..L
   int64_t lda[MEDIUM_MAX_LAYERS];
   // W_l, l >= 2, in LDS at woff[l-1] as wrows[l-1] = round_up(d_l, 16) rows
-  // of wp[l-1] = round_up(d_{l-1}, 16) + 4 floats, zero past the layer sizes
+  // of wp[l-1] floats (round_up(d_{l-1}, 16) plus bank padding, 18 mod 32),
+  // zero past the layer sizes
   int woff[MEDIUM_MAX_LAYERS], wrows[MEDIUM_MAX_LAYERS], wp[MEDIUM_MAX_LAYERS];
 };
 hipError_t launch_medium(const MediumParams& p, int ncu, hipStream_t s);

@@ -35,7 +35,10 @@ namespace {
 
 constexpr int M_WAVES = 12;
 constexpr int M_THREADS = M_WAVES * 64;
-constexpr int M_HP = MEDIUM_WIDTH + 4;  // LDS row pitch of activations and deltas
+// LDS row pitch of activations and deltas.  The matrix-core operand reads
+// take 16 rows x 2 columns per half-wave; a pitch of 2 mod 32 (in 4-byte
+// banks) puts them in 32 different banks.
+constexpr int M_HP = MEDIUM_WIDTH + 2;
 constexpr int M_PF = 2;                 // layer-1 pieces loaded ahead per tile
 constexpr int M_SROWS = M_THREADS / 32; // weight rows per load: 32 lanes x 16 bytes a row
 constexpr int M_STAGE = 8;              // weight loads in flight per thread
@@ -150,8 +153,10 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
   // Staged row R (over the layers' padded rows in order) is row j of layer l;
   // rows of the device layout are 16-byte aligned with a zero-filled pitch,
   // and rows past d_l and columns past that pitch are stored as zeros, so
-  // every product below runs over whole 16-unit blocks (the 4 columns of
-  // bank padding at the end of each LDS row are never read)
+  // every product below runs over whole 16-unit blocks (the bank padding at
+  // the end of each LDS row is never read).  The LDS pitch is 18 mod 32
+  // floats, so rows are 8-byte aligned: each 16-byte load is stored as two
+  // 8-byte halves.
   {
     int rend[L];  // staged rows of layers 2..l
     rend[1] = p.wrows[1];
@@ -173,10 +178,11 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         // the layer's figures by selects (li differs between lanes)
         auto pick = [&](auto a1, auto a2, auto a3) { return li == 1 ? a1 : li == 2 ? a2 : a3; };
         const int wp = pick(p.wp[1], p.wp[2], p.wp[3]);
+        const int cw = (pick(p.dims[1], p.dims[2], p.dims[3]) + 15) & ~15;  // padded width
         const int ldw = (int)pick(p.ldw[1], p.ldw[2], p.ldw[3]);
         const int dl = pick(p.dims[2], p.dims[3], p.dims[4]);
         const float* W = pick(p.W[1], p.W[2], p.W[3]);
-        const bool in = R < rtot && c < wp - 4;
+        const bool in = R < rtot && c < cw;
         const bool ok = in && j < dl && c < ldw;
         const float4 x = *reinterpret_cast<const float4*>(ok ? W + (int64_t)j * ldw + c : p.W[1]);
         v[i] = ok ? x : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -185,8 +191,12 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
       // rows past the last layer and columns past the padded width go to a
       // spare slot, so no load is tied to a branch
 #pragma unroll
-      for (int i = 0; i < M_STAGE; ++i)
-        *(dst[i] >= 0 ? reinterpret_cast<float4*>(wl + dst[i]) : &spare) = v[i];
+      for (int i = 0; i < M_STAGE; ++i) {
+        float2* d = dst[i] >= 0 ? reinterpret_cast<float2*>(wl + dst[i])
+                                : reinterpret_cast<float2*>(&spare);
+        d[0] = make_float2(v[i].x, v[i].y);
+        d[1] = make_float2(v[i].z, v[i].w);
+      }
     }
   }
   if (bl_mine) bl[bl_l - 1][bl_u] = bl_ok ? bl_v : 0.0f;
