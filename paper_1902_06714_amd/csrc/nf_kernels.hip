@@ -373,6 +373,50 @@ gemm_group_kernel(const GemmGroupT<T> g) {
 // parameters before the step into the other parameter buffer), for up to
 // FOLD_GROUP_MAX layers per launch; workgroup b belongs to layer q with
 // start[q] <= b < start[q + 1].
+// The shard fold of one value: pieces q = s nsub + u (shard s, sub-piece u)
+// in order, piece_s = ((p_{s,0} + p_{s,1}) + ...), total = ((piece_0 +
+// piece_1) + ...).  The loads of a batch of NB pieces issue together before
+// any is added (past the last piece a batch re-reads the last one and drops
+// it), so a fold of up to NB pieces waits for memory once, not once per
+// piece.  NB is the smallest of 4, 8, 16 that holds every piece, so folds of
+// few pieces (bandwidth-bound on large layers) read no extra bytes.
+template <int NB, class T, class Get>
+__device__ __forceinline__ T fold_pieces_nb(int nsub, int P, Get get) {
+  T tot = T(0), piece = T(0);
+  int u = 0;           // sub-piece within the current shard
+  bool first = true;   // no shard added to the total yet
+  auto batch = [&](int q0) {
+    T v[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) v[i] = get(q0 + i < P ? q0 + i : P - 1);
+    __builtin_amdgcn_sched_barrier(0);  // every load of the batch before the first add
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (q0 + i < P) {
+        piece = u == 0 ? v[i] : piece + v[i];
+        if (++u == nsub) {
+          tot = first ? piece : tot + piece;
+          first = false;
+          u = 0;
+        }
+      }
+    }
+  };
+  // the first batch outside the loop (P >= 1): a loop head would wait for
+  // the loads issued before it
+  batch(0);
+  for (int q0 = NB; q0 < P; q0 += NB) batch(q0);
+  return tot;
+}
+
+template <class T, class Get>
+__device__ __forceinline__ T fold_pieces(int nshards, int nsub, Get get) {
+  const int P = nshards * nsub;
+  if (P <= 4) return fold_pieces_nb<4, T>(nsub, P, get);
+  if (P <= 8) return fold_pieces_nb<8, T>(nsub, P, get);
+  return fold_pieces_nb<16, T>(nsub, P, get);
+}
+
 template <class T>
 __global__ void fold_sgd_kernel(const FoldGroupT<T> g) {
   const int b = blockIdx.x;
@@ -386,24 +430,18 @@ __global__ void fold_sgd_kernel(const FoldGroupT<T> g) {
   if (idx < nw) {
     const int m = (int)(idx / f.N), n = (int)(idx % f.N);
     const int64_t o = (int64_t)m * f.ldw + n;
-    T tot = T(0);
-    for (int s = 0; s < nshards; ++s) {
-      T piece = f.partial[(int64_t)(s * nsub) * f.pstride + o];
-      for (int u = 1; u < nsub; ++u) piece += f.partial[(int64_t)(s * nsub + u) * f.pstride + o];
-      tot = s == 0 ? piece : tot + piece;
-    }
+    const T w_old = f.Win[o];
+    const T tot = fold_pieces<T>(nshards, nsub,
+                                 [&](int q) { return f.partial[(int64_t)q * f.pstride + o]; });
     f.G[o] = tot;
-    f.W[o] = fma_t(-g.scale, tot, f.Win[o]);
+    f.W[o] = fma_t(-g.scale, tot, w_old);
   } else if (idx < nw + f.M) {
     const int m = (int)(idx - nw);
-    T tot = T(0);
-    for (int s = 0; s < nshards; ++s) {
-      T piece = f.pbias[(int64_t)(s * nsub) * f.M + m];
-      for (int u = 1; u < nsub; ++u) piece += f.pbias[(int64_t)(s * nsub + u) * f.M + m];
-      tot = s == 0 ? piece : tot + piece;
-    }
+    const T b_old = f.bin[m];
+    const T tot = fold_pieces<T>(nshards, nsub,
+                                 [&](int q) { return f.pbias[(int64_t)q * f.M + m]; });
     f.gbias[m] = tot;
-    f.b[m] = fma_t(-g.scale, tot, f.bin[m]);
+    f.b[m] = fma_t(-g.scale, tot, b_old);
   }
 }
 
