@@ -533,15 +533,18 @@ __global__ void fwd_fold_kernel(const FwdFoldParamsT<T> f) {
   if (idx >= (int64_t)f.M * f.N) return;
   const int m = (int)(idx / f.N), n = (int)(idx % f.N);
   const int64_t o = (int64_t)m * f.ldp + n;
-  T z = f.partial[o];
-  for (int q = 1; q < f.nsplit; ++q) z += f.partial[(int64_t)q * f.pstride + o];
+  // the bias and the target requested with the pieces, all before the first use
+  const T bias = f.bias[n];
+  const T y = EPI == EPI_FWD_DELTA ? f.aux[(int64_t)m * f.ldaux + n] : T(0);
+  const T z = fold_pieces<T>(f.nsplit, 1,
+                             [&](int q) { return f.partial[(int64_t)q * f.pstride + o]; });
   T a, fp;
-  act_eval(f.act, z + f.bias[n], a, fp);
+  act_eval(f.act, z + bias, a, fp);
   if constexpr (EPI == EPI_FWD_STASH) {
     f.out0[(int64_t)m * f.ld0 + n] = a;
     f.out1[(int64_t)m * f.ld1 + n] = fp;
   } else if constexpr (EPI == EPI_FWD_DELTA) {
-    f.out0[(int64_t)m * f.ld0 + n] = (a - f.aux[(int64_t)m * f.ldaux + n]) * fp;
+    f.out0[(int64_t)m * f.ld0 + n] = (a - y) * fp;
   } else {
     f.out0[(int64_t)m * f.ld0 + n] = a;
   }
