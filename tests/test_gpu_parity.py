@@ -129,6 +129,36 @@ def test_medium_edges(dims, acts, batch, shards, eta):
     _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 3)
 
 
+def _random_cases(n=24, seed=20260):
+    """Seeded network shapes across the narrow, medium and contraction paths:
+    1 to 4 layers, widths 1 to 200 (narrow nets need every layer after the
+    input <= 32 and an input width that is a multiple of 4; medium nets need
+    2 to 4 layers <= 128 wide), batches 1 to 1500 split into shards that
+    divide them, smooth activations (unique gradients everywhere)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        L = int(rng.integers(1, 5))
+        kind = i % 3   # narrow-sized, medium-sized, wide
+        top = (32, 128, 200)[kind]
+        d0 = int(rng.integers(1, 300))
+        if kind == 0 and rng.random() < 0.7:
+            d0 = 4 * max(1, d0 // 4)
+        dims = [d0] + [int(rng.integers(1, top + 1)) for _ in range(L)]
+        batch = int(rng.integers(1, 1501))
+        divisors = [k for k in (1, 2, 3, 4, 5, 8, 16) if batch % k == 0]
+        shards = int(rng.choice(divisors))
+        acts = tuple(str(a) for a in rng.choice(["sigmoid", "tanh", "gaussian"], size=L))
+        cases.append((tuple(dims), acts, batch, shards))
+    return cases
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards", _random_cases())
+def test_random_shapes(dims, acts, batch, shards):
+    theta, X, Y = _problem(dims, 11 * sum(dims) + batch, batch * 2, init_scale=None)
+    _compare_trajectory(dims, acts, theta, X, Y, batch, 0.5, shards, 2)
+
+
 RELU_SMALL = [
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 1, 0.2),
     ((40, 96, 72, 6), ("relu", "relu", "sigmoid"), 128, 4, 0.2),
