@@ -696,15 +696,17 @@ nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, do
 // LDS placement of W_l, l >= 2 (see MediumParams); false when the net or the
 // batch does not qualify: every per-sample buffer of the pass (at most 16
 // pieces of [batch][<= 128] values) must span fewer than MEDIUM_OOB bytes
-bool medium_layout(const nf_net* n, int64_t batch, nf::MediumParams* p) {
+template <class T>
+bool medium_layout(const nf_net* n, int64_t batch, nf::MediumParamsT<T>* p) {
   const int L = num_layers(n);
-  if (n->dtype != nf::DT_F32 || L < 2 || L > nf::MEDIUM_MAX_LAYERS) return false;
-  if (batch * 16 * (nf::MEDIUM_WIDTH + 4) * 4 >= (int64_t)nf::MEDIUM_OOB) return false;
+  if (n->dtype != dtype_of<T>() || L < 2 || L > nf::MEDIUM_MAX_LAYERS) return false;
+  if (batch * 16 * (nf::MEDIUM_WIDTH + 4) * (int64_t)sizeof(T) >= (int64_t)nf::MEDIUM_OOB)
+    return false;
   for (int l = 1; l <= L; ++l)
     if (n->dims[l] > nf::MEDIUM_WIDTH) return false;
   int off = 0;
   for (int l = 2; l <= L; ++l) {
-    // pitch 18 mod 32 floats: both the row-wise (forward) and the
+    // pitch 18 mod 32 elements: both the row-wise (forward) and the
     // column-wise (delta) operand reads of a half-wave hit distinct banks
     const int cw = (int)round_up(n->dims[l - 1], 16);
     const int rows = (int)round_up(n->dims[l], 16), wp = cw + (cw % 32 == 0 ? 18 : 2);
@@ -713,19 +715,20 @@ bool medium_layout(const nf_net* n, int64_t batch, nf::MediumParams* p) {
     p->wp[l - 1] = wp;
     off += rows * wp;
   }
-  return off <= nf::MEDIUM_LDS_WEIGHTS;
+  return off <= (sizeof(T) == 4 ? nf::MEDIUM_LDS_WEIGHTS : nf::MEDIUM64_LDS_WEIGHTS);
 }
 
-nf_status medium_forward_deltas(nf_net* n, const float* x, const float* y, int64_t batch,
+template <class T>
+nf_status medium_forward_deltas(nf_net* n, const T* x, const T* y, int64_t batch,
                                 hipStream_t s) {
-  nf::MediumParams mp{};
-  if (!medium_layout(n, batch, &mp)) return fail(NF_EINVAL, "internal: not a medium net");
+  nf::MediumParamsT<T> mp{};
+  if (!medium_layout<T>(n, batch, &mp)) return fail(NF_EINVAL, "internal: not a medium net");
   const int L = num_layers(n);
   const LayerLayout& l1 = n->layers[1];
-  float* P = cur_params<float>(n);
+  T* P = cur_params<T>(n);
 
   // layer 1: z_1 in k pieces (one piece when the tile grid fills the chip)
-  nf::GemmParamsT<float> p{};
+  nf::GemmParamsT<T> p{};
   p.A = x;
   p.lda = n->dims[0];
   p.B = P + l1.w_off;
@@ -748,11 +751,11 @@ nf_status medium_forward_deltas(nf_net* n, const float* x, const float* y, int64
   p.shard_len = p.K;
   p.nsub = nsplit;
   p.sub_len = sub_len;
-  p.partial = as<float>(n->partial);
+  p.partial = as<T>(n->partial);
   p.pstride = zstride;
   p.ld0 = ldz;
   const bool av = vec_ok(x, n->dims[0]);
-  st = launch<float>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, p, s, nf::TILE_64x64);
+  st = launch<T>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, p, s, nf::TILE_64x64);
   if (st != NF_OK) return st;
 
   mp.B = (int)batch;
@@ -763,20 +766,21 @@ nf_status medium_forward_deltas(nf_net* n, const float* x, const float* y, int64
   mp.ldz = ldz;
   mp.np = nsplit;
   mp.Y = y;
-  double by = 4.0 * ((double)nsplit * batch * p.N + (double)batch * n->dims[L]), fl = 0.0;
+  const double es = (double)sizeof(T);
+  double by = es * ((double)nsplit * batch * p.N + (double)batch * n->dims[L]), fl = 0.0;
   for (int l = 1; l <= L; ++l) {
     const LayerLayout& ly = n->layers[l];
     mp.acts[l - 1] = ly.act;
     mp.W[l - 1] = P + ly.w_off;
     mp.ldw[l - 1] = ly.ldw;
     mp.bias[l - 1] = P + ly.b_off;
-    mp.A[l - 1] = as<float>(n->actv[l]);
-    mp.D[l - 1] = as<float>(n->dbuf[l]);
+    mp.A[l - 1] = as<T>(n->actv[l]);
+    mp.D[l - 1] = as<T>(n->dbuf[l]);
     mp.lda[l - 1] = ly.lda;
-    by += 4.0 * ((double)batch * ly.out * (l < L ? 2 : 1) + (l >= 2 ? (double)ly.out * ly.in : 0));
+    by += es * ((double)batch * ly.out * (l < L ? 2 : 1) + (l >= 2 ? (double)ly.out * ly.in : 0));
     if (l >= 2) fl += 4.0 * batch * (double)ly.out * ly.in;   // forward and delta products
   }
-  return timed(n, "medium_fwd_deltas", by, fl, s,
+  return timed(n, sizeof(T) == 4 ? "medium_fwd_deltas" : "medium64_fwd_deltas", by, fl, s,
                [&] { return nf::launch_medium(mp, n->ncu > 0 ? n->ncu : 256, s); });
 }
 
@@ -788,14 +792,12 @@ nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double et
                      hipStream_t s) {
   nf_status st;
   const bool narrow = shards == 1 && narrow_rows_ok<T>(n, x);
-  nf::MediumParams mp{};
+  nf::MediumParamsT<T> mp{};
   if (narrow) {
     st = narrow_train_step<T>(n, x, y, batch, eta, s);
-  } else if (sizeof(T) == 4 && medium_layout(n, batch, &mp)) {
-    if constexpr (sizeof(T) == 4) {
-      st = medium_forward_deltas(n, x, y, batch, s);
-      if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s, true);
-    }
+  } else if (medium_layout<T>(n, batch, &mp)) {
+    st = medium_forward_deltas<T>(n, x, y, batch, s);
+    if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s, true);
   } else {
     st = run_forward<T>(n, x, y, batch, nullptr, true, s);
     if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s);

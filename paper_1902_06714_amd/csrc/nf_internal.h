@@ -210,7 +210,7 @@ hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hi
 hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s);
 
 // ---------------------------------------------------------------------------
-// Medium networks (fp32): 2..MEDIUM_MAX_LAYERS layers, every layer after the
+// Medium networks (fp32 and fp64): 2..MEDIUM_MAX_LAYERS layers, every layer after the
 // input at most MEDIUM_WIDTH units, the weights of layers 2..L within
 // MEDIUM_LDS_WEIGHTS floats of LDS as padded below.  Layer 1's contraction
 // writes its k pieces; one per-sample kernel does the rest of the forward
@@ -224,26 +224,33 @@ constexpr int MEDIUM_LDS_WEIGHTS = 24576;
 // address nothing, so lanes off the tile load zeros and drop their stores
 constexpr unsigned MEDIUM_OOB = 0x7fff0000u;
 
-struct MediumParams {
+template <class T>
+struct MediumParamsT {
   int B, L;
   int dims[MEDIUM_MAX_LAYERS + 1];
   int acts[MEDIUM_MAX_LAYERS];
-  const float* zp;                         // layer 1's pieces [np][B][ldz]
+  const T* zp;                             // layer 1's pieces [np][B][ldz]
   int64_t zstride, ldz;
   int np;
-  const float* W[MEDIUM_MAX_LAYERS];       // W_l (index l-1), device layout
+  const T* W[MEDIUM_MAX_LAYERS];           // W_l (index l-1), device layout
   int64_t ldw[MEDIUM_MAX_LAYERS];
-  const float* bias[MEDIUM_MAX_LAYERS];
-  const float* Y;                          // targets [B][d_L]
-  float* A[MEDIUM_MAX_LAYERS];             // f(z_l) [B][lda_l], l = 1..L-1
-  float* D[MEDIUM_MAX_LAYERS];             // delta_l [B][lda_l], l = 1..L
+  const T* bias[MEDIUM_MAX_LAYERS];
+  const T* Y;                              // targets [B][d_L]
+  T* A[MEDIUM_MAX_LAYERS];                 // f(z_l) [B][lda_l], l = 1..L-1
+  T* D[MEDIUM_MAX_LAYERS];                 // delta_l [B][lda_l], l = 1..L
   int64_t lda[MEDIUM_MAX_LAYERS];
   // W_l, l >= 2, in LDS at woff[l-1] as wrows[l-1] = round_up(d_l, 16) rows
-  // of wp[l-1] floats (round_up(d_{l-1}, 16) plus bank padding, 18 mod 32),
+  // of wp[l-1] elements (round_up(d_{l-1}, 16) plus bank padding, 18 mod 32),
   // zero past the layer sizes
   int woff[MEDIUM_MAX_LAYERS], wrows[MEDIUM_MAX_LAYERS], wp[MEDIUM_MAX_LAYERS];
 };
-hipError_t launch_medium(const MediumParams& p, int ncu, hipStream_t s);
+using MediumParams = MediumParamsT<float>;
+using MediumParams64 = MediumParamsT<double>;
+// fp64 nets: the staged weights in at most this many doubles (the tile is
+// then one 16-sample block, so the weights and the tile fit in LDS together)
+constexpr int MEDIUM64_LDS_WEIGHTS = 15360;
+template <class T>
+hipError_t launch_medium(const MediumParamsT<T>& p, int ncu, hipStream_t s);
 
 // Adds to *count the number of rows s < n for which out[s][0..d) and
 // y[s][0..d) have their first largest entry at the same index (rows holding a

@@ -1,5 +1,5 @@
-// Per-sample pass for fp32 networks whose layers after the input have at most
-// 128 units (e.g. 784-100-100-10).  Layer 1's contraction runs before it
+// Per-sample pass for networks whose layers after the input have at most 128
+// units (e.g. 784-100-100-10), in fp32 and fp64.  Layer 1's contraction runs before it
 // (its k pieces in the piece buffer); then each workgroup of 12 waves, for
 // tiles of 16 NSB samples,
 //   folds layer 1's pieces in piece order, adds b_1 and applies f_1;
@@ -8,7 +8,10 @@
 //   (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with the weights of this
 //   step;
 // and stores the activations and deltas the tendency kernels read.  Every
-// product is on the 16x16x4 fp32 matrix cores.  The work of a layer is split
+// product is on the 16x16x4 matrix cores of the element type (fp32 or fp64;
+// both take lane (r, g)'s inputs as row r / column r and input g, and differ
+// in where accumulator register v lands: row 4 g + v in fp32, 4 v + g in
+// fp64).  The work of a layer is split
 // into jobs of 16 units x 16 samples, handed to the waves round robin; a
 // layer's forward product and its delta use the same jobs, so the lane that
 // formed f'(z_l) for a (sample, unit) forms that delta and keeps f' in
@@ -30,6 +33,7 @@
 namespace nf {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
@@ -40,21 +44,51 @@ constexpr int M_THREADS = M_WAVES * 64;
 // banks) puts them in 32 different banks.
 constexpr int M_HP = MEDIUM_WIDTH + 2;
 constexpr int M_PF = 2;                 // layer-1 pieces loaded ahead per tile
-constexpr int M_SROWS = M_THREADS / 32; // weight rows per load: 32 lanes x 16 bytes a row
 constexpr int M_STAGE = 8;              // weight loads in flight per thread
 
 __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)MEDIUM_OOB,
                                            0x00020000);
 }
-__device__ inline float bload(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-  return __builtin_bit_cast(float,
-                            __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
-}
-__device__ inline void bstore(float v, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)voff, (int)soff,
-                                        0);
-}
+// the element type's matrix instruction, accumulator and layout
+template <class T>
+struct MedT;
+template <>
+struct MedT<float> {
+  using acc_t = floatx4;
+  using vec16 = float4;
+  static constexpr int RS = 1, GS = 4;  // tile row of register v of lane group g: GS g + RS v
+  static constexpr int WLDS = MEDIUM_LDS_WEIGHTS;
+  __device__ static acc_t mma(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static float load(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    return __builtin_bit_cast(float,
+                              __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+  }
+  __device__ static void store(float v, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)voff,
+                                          (int)soff, 0);
+  }
+};
+template <>
+struct MedT<double> {
+  using acc_t = doublex4;
+  using vec16 = double2;
+  static constexpr int RS = 4, GS = 1;
+  static constexpr int WLDS = MEDIUM64_LDS_WEIGHTS;
+  __device__ static acc_t mma(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  __device__ static double load(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    return __builtin_bit_cast(double,
+                              __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0));
+  }
+  __device__ static void store(double v, __amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), r, (int)voff, (int)soff, 0);
+  }
+};
 
 // calls f with the activation as a compile-time constant, so the code of one
 // phase holds one activation's arithmetic, not a switch per element
@@ -71,13 +105,18 @@ __device__ __forceinline__ void with_act(int act, F&& f) {
 
 }  // namespace
 
-template <int NSB, int L>
-__global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p) {
+template <class T, int NSB, int L>
+__global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T> p) {
+  using M = MedT<T>;
   constexpr int TS = 16 * NSB;                       // samples per tile
   constexpr int NJ = (8 * NSB + M_WAVES - 1) / M_WAVES;  // jobs per wave at most
-  __shared__ __attribute__((aligned(16))) float wl[MEDIUM_LDS_WEIGHTS];  // W_2 .. W_L, padded
-  __shared__ float hs[2][TS][M_HP];                                      // activations, deltas
-  __shared__ float bl[L][MEDIUM_WIDTH];                                  // b_1 .. b_L
+  constexpr unsigned SZ = sizeof(T);
+  constexpr int VW = 16 / sizeof(T);                  // elements per 16-byte load
+  constexpr int LPR = MEDIUM_WIDTH / VW;              // lanes per staged weight row
+  constexpr int SROWS = M_THREADS / LPR;              // weight rows per load
+  __shared__ __attribute__((aligned(16))) T wl[M::WLDS];  // W_2 .. W_L, padded
+  __shared__ T hs[2][TS][M_HP];                           // activations, deltas
+  __shared__ T bl[L][MEDIUM_WIDTH];                       // b_1 .. b_L
   __shared__ float4 spare;
 
   const int tid = threadIdx.x;
@@ -90,32 +129,35 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
 
   // job jj of this wave in a layer of d units: job = wave + 12 jj, unit block
   // job / NSB, sample block job % NSB; lane (r, g) holds unit 16 ub + r and,
-  // in accumulator register v, tile row 16 sb + 4 g + v
+  // in accumulator register v, tile row row(jj) + RS v (16 sb + 4 g + v in
+  // fp32, 16 sb + g + 4 v in fp64)
   auto has_job = [&](int jj, int d) { return wave + M_WAVES * jj < ((d + 15) >> 4) * NSB; };
   auto unit = [&](int jj) { return 16 * ((wave + M_WAVES * jj) / NSB) + r; };
-  auto row = [&](int jj) { return 16 * ((wave + M_WAVES * jj) % NSB) + 4 * g; };
+  auto sblk = [&](int jj) { return 16 * ((wave + M_WAVES * jj) % NSB); };
+  auto row = [&](int jj) { return sblk(jj) + M::GS * g; };
+  constexpr int RS = M::RS;
 
   const __amdgpu_buffer_rsrc_t zres = rsrc(p.zp), yres = rsrc(p.Y);
 
   // layer-1 pieces 0 .. M_PF-1 and the targets of tile tt (a tile past the
   // last loads nothing: every row is past the batch, and its scalar offsets
   // are the last tile's)
-  float pz[M_PF][NJ][4], py[NJ][4];
+  T pz[M_PF][NJ][4], py[NJ][4];
   auto load_z = [&](int tt) {
     const int rem = p.B - tt * TS, tc = tt < ntiles ? tt : ntiles - 1;
 #pragma unroll
     for (int jj = 0; jj < NJ; ++jj) {
       if (!has_job(jj, d1)) break;
       const int u = unit(jj), rw = row(jj);
-      const unsigned vb = 4u * (unsigned)(rw * ldz + u);
+      const unsigned vb = SZ * (unsigned)(rw * ldz + u);
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const bool ok = u < d1 && rw + v < rem;
+        const bool ok = u < d1 && rw + RS * v < rem;
 #pragma unroll
         for (int q = 0; q < M_PF; ++q) {
           const int qq = q < p.np ? q : 0;
-          pz[q][jj][v] = bload(zres, ok ? vb : MEDIUM_OOB,
-                               4u * (unsigned)((tc * TS + v) * ldz + qq * (int)p.zstride));
+          pz[q][jj][v] = M::load(zres, ok ? vb : MEDIUM_OOB,
+                                 SZ * (unsigned)((tc * TS + RS * v) * ldz + qq * (int)p.zstride));
         }
       }
     }
@@ -126,11 +168,11 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
     for (int jj = 0; jj < NJ; ++jj) {
       if (!has_job(jj, dL)) break;
       const int u = unit(jj), rw = row(jj);
-      const unsigned vb = 4u * (unsigned)(rw * dL + u);
+      const unsigned vb = SZ * (unsigned)(rw * dL + u);
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const bool ok = u < dL && rw + v < rem;
-        py[jj][v] = bload(yres, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((tc * TS + v) * dL));
+        const bool ok = u < dL && rw + RS * v < rem;
+        py[jj][v] = M::load(yres, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((tc * TS + RS * v) * dL));
       }
     }
   };
@@ -147,29 +189,30 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
   const int bl_w = __builtin_amdgcn_readfirstlane(tid / MEDIUM_WIDTH) + 1;
   const int bl_l = bl_w < L ? bl_w : L;
   const bool bl_ok = bl_mine && bl_u < p.dims[bl_l];
-  const float bl_v = p.bias[bl_l - 1][bl_ok ? bl_u : 0];
+  const T bl_v = p.bias[bl_l - 1][bl_ok ? bl_u : 0];
 
-  // the weights of layers 2..L into LDS: 32 lanes per row, 16 bytes each.
+  // the weights of layers 2..L into LDS: a row is 128 elements, 16 bytes a lane
+  // (32 lanes in fp32, 64 in fp64).
   // Staged row R (over the layers' padded rows in order) is row j of layer l;
   // rows of the device layout are 16-byte aligned with a zero-filled pitch,
   // and rows past d_l and columns past that pitch are stored as zeros, so
   // every product below runs over whole 16-unit blocks (the bank padding at
   // the end of each LDS row is never read).  The LDS pitch is 18 mod 32
-  // floats, so rows are 8-byte aligned: each 16-byte load is stored as two
-  // 8-byte halves.
+  // elements, so fp32 rows are 8-byte aligned: each 16-byte load is stored as
+  // two 8-byte halves.
   {
     int rend[L];  // staged rows of layers 2..l
     rend[1] = p.wrows[1];
 #pragma unroll
     for (int l = 3; l <= L; ++l) rend[l - 1] = rend[l - 2] + p.wrows[l - 1];
     const int rtot = rend[L - 1];
-    const int c = 4 * (lane & 31);
-    for (int R0 = tid >> 5; R0 < rtot; R0 += M_SROWS * M_STAGE) {
-      float4 v[M_STAGE];
+    const int c = VW * (tid % LPR);
+    for (int R0 = tid / LPR; R0 < rtot; R0 += SROWS * M_STAGE) {
+      typename M::vec16 v[M_STAGE];
       int dst[M_STAGE];
 #pragma unroll
       for (int i = 0; i < M_STAGE; ++i) {
-        const int R = R0 + i * M_SROWS;
+        const int R = R0 + i * SROWS;
         int li = 1, r0 = 0;
 #pragma unroll
         for (int l = 3; l <= L; ++l)
@@ -181,34 +224,40 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         const int cw = (pick(p.dims[1], p.dims[2], p.dims[3]) + 15) & ~15;  // padded width
         const int ldw = (int)pick(p.ldw[1], p.ldw[2], p.ldw[3]);
         const int dl = pick(p.dims[2], p.dims[3], p.dims[4]);
-        const float* W = pick(p.W[1], p.W[2], p.W[3]);
+        const T* W = pick(p.W[1], p.W[2], p.W[3]);
         const bool in = R < rtot && c < cw;
         const bool ok = in && j < dl && c < ldw;
-        const float4 x = *reinterpret_cast<const float4*>(ok ? W + (int64_t)j * ldw + c : p.W[1]);
-        v[i] = ok ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+        const typename M::vec16 x =
+            *reinterpret_cast<const typename M::vec16*>(ok ? W + (int64_t)j * ldw + c : p.W[1]);
+        v[i] = ok ? x : typename M::vec16{};
         dst[i] = in ? pick(p.woff[1], p.woff[2], p.woff[3]) + j * wp + c : -1;
       }
       // rows past the last layer and columns past the padded width go to a
       // spare slot, so no load is tied to a branch
 #pragma unroll
       for (int i = 0; i < M_STAGE; ++i) {
-        float2* d = dst[i] >= 0 ? reinterpret_cast<float2*>(wl + dst[i])
-                                : reinterpret_cast<float2*>(&spare);
-        d[0] = make_float2(v[i].x, v[i].y);
-        d[1] = make_float2(v[i].z, v[i].w);
+        if constexpr (sizeof(T) == 4) {
+          float2* d = dst[i] >= 0 ? reinterpret_cast<float2*>(wl + dst[i])
+                                  : reinterpret_cast<float2*>(&spare);
+          d[0] = make_float2(v[i].x, v[i].y);
+          d[1] = make_float2(v[i].z, v[i].w);
+        } else {
+          *(dst[i] >= 0 ? reinterpret_cast<double2*>(wl + dst[i])
+                        : reinterpret_cast<double2*>(&spare)) = v[i];
+        }
       }
     }
   }
-  if (bl_mine) bl[bl_l - 1][bl_u] = bl_ok ? bl_v : 0.0f;
+  if (bl_mine) bl[bl_l - 1][bl_u] = bl_ok ? bl_v : T(0);
   __syncthreads();  // weights and biases in LDS
 
-  float fp[L - 1][NJ][4];  // f'(z_l), l < L
+  T fp[L - 1][NJ][4];  // f'(z_l), l < L
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int s0 = t * TS, rem = p.B - s0;
 
     // ---- layer 1: the pieces of z_1 in piece order, + b_1, f_1
     {
-      float zs[NJ][4];
+      T zs[NJ][4];
 #pragma unroll
       for (int jj = 0; jj < NJ; ++jj)
 #pragma unroll
@@ -220,16 +269,16 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         }
       // pieces past those loaded ahead (small batches cut into many pieces)
       for (int q = M_PF; q < p.np; ++q) {
-        float tq[NJ][4];
+        T tq[NJ][4];
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, d1)) break;
           const int u = unit(jj), rw = row(jj);
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const bool ok = u < d1 && rw + v < rem;
-            tq[jj][v] = bload(zres, ok ? 4u * (unsigned)(rw * ldz + u) : MEDIUM_OOB,
-                              4u * (unsigned)((s0 + v) * ldz + q * (int)p.zstride));
+            const bool ok = u < d1 && rw + RS * v < rem;
+            tq[jj][v] = M::load(zres, ok ? SZ * (unsigned)(rw * ldz + u) : MEDIUM_OOB,
+                                SZ * (unsigned)((s0 + RS * v) * ldz + q * (int)p.zstride));
           }
         }
 #pragma unroll
@@ -245,16 +294,16 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, d1)) break;
           const int u = unit(jj), rw = row(jj);
-          const unsigned vb = 4u * (unsigned)(rw * lda + u);
-          const float b = bl[0][u];
+          const unsigned vb = SZ * (unsigned)(rw * lda + u);
+          const T b = bl[0][u];
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const bool ok = u < d1 && rw + v < rem;
-            float a, f;
+            const bool ok = u < d1 && rw + RS * v < rem;
+            T a, f;
             act_eval(decltype(act)::value, zs[jj][v] + b, a, f);
-            a = ok ? a : 0.0f;
-            bstore(a, ares, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((s0 + v) * lda));
-            hs[0][rw + v][u] = a;
+            a = ok ? a : T(0);
+            M::store(a, ares, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((s0 + RS * v) * lda));
+            hs[0][rw + RS * v][u] = a;
             fp[0][jj][v] = f;
           }
         }
@@ -268,19 +317,19 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
     for (int l = 2; l <= L; ++l) {
       const int N = p.dims[l], Kp = (p.dims[l - 1] + 15) & ~15;
       const int wp = p.wp[l - 1];
-      const float* w = wl + p.woff[l - 1];
-      floatx4 acc[NJ];
+      const T* w = wl + p.woff[l - 1];
+      typename M::acc_t acc[NJ];
 #pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) acc[jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int jj = 0; jj < NJ; ++jj) acc[jj] = typename M::acc_t{};
       // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with input
       // k0 + 4 i + g; inputs past d_{l-1} are zero on both sides up to the
       // next multiple of 16
       for (int k0 = 0; k0 < Kp; k0 += 16) {
-        float xa[NJ][4], wb[NJ][4];
+        T xa[NJ][4], wb[NJ][4];
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, N)) break;
-          const int xr = row(jj) - 4 * g + r;
+          const int xr = sblk(jj) + r;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             wb[jj][i] = w[unit(jj) * wp + k0 + 4 * i + g];
@@ -292,7 +341,7 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
           if (!has_job(jj, N)) break;
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[jj][i], wb[jj][i], acc[jj], 0, 0, 0);
+            acc[jj] = M::mma(xa[jj][i], wb[jj][i], acc[jj]);
         }
       }
       const __amdgpu_buffer_rsrc_t ores = rsrc(l < L ? p.A[l - 1] : p.D[l - 1]);
@@ -302,23 +351,23 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, N)) break;
           const int u = unit(jj), rw = row(jj);
-          const unsigned vb = 4u * (unsigned)(rw * lda + u);
-          const float b = bl[l - 1][u];
+          const unsigned vb = SZ * (unsigned)(rw * lda + u);
+          const T b = bl[l - 1][u];
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const bool ok = u < N && rw + v < rem;
-            const unsigned so = 4u * (unsigned)((s0 + v) * lda);
-            float a, f;
+            const bool ok = u < N && rw + RS * v < rem;
+            const unsigned so = SZ * (unsigned)((s0 + RS * v) * lda);
+            T a, f;
             act_eval(decltype(act)::value, acc[jj][v] + b, a, f);
             if (l < L) {
-              a = ok ? a : 0.0f;
-              bstore(a, ores, ok ? vb : MEDIUM_OOB, so);
-              hs[cur ^ 1][rw + v][u] = a;
+              a = ok ? a : T(0);
+              M::store(a, ores, ok ? vb : MEDIUM_OOB, so);
+              hs[cur ^ 1][rw + RS * v][u] = a;
               fp[l - 1][jj][v] = f;
             } else {
-              const float d = ok ? (a - py[jj][v]) * f : 0.0f;
-              bstore(d, ores, ok ? vb : MEDIUM_OOB, so);
-              hs[cur ^ 1][rw + v][u] = d;
+              const T d = ok ? (a - py[jj][v]) * f : T(0);
+              M::store(d, ores, ok ? vb : MEDIUM_OOB, so);
+              hs[cur ^ 1][rw + RS * v][u] = d;
             }
           }
         }
@@ -336,18 +385,18 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
     for (int l = L - 1; l >= 1; --l) {
       const int N = p.dims[l], Kp = (p.dims[l + 1] + 15) & ~15;
       const int wp = p.wp[l];
-      const float* w = wl + p.woff[l];
-      floatx4 acc[NJ];
+      const T* w = wl + p.woff[l];
+      typename M::acc_t acc[NJ];
 #pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) acc[jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int jj = 0; jj < NJ; ++jj) acc[jj] = typename M::acc_t{};
       // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with unit
       // k0 + 4 i + g of layer l + 1 (zero on both sides past d_{l+1})
       for (int k0 = 0; k0 < Kp; k0 += 16) {
-        float xa[NJ][4], wb[NJ][4];
+        T xa[NJ][4], wb[NJ][4];
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, N)) break;
-          const int xr = row(jj) - 4 * g + r;
+          const int xr = sblk(jj) + r;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             wb[jj][i] = w[(k0 + 4 * i + g) * wp + unit(jj)];
@@ -359,7 +408,7 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
           if (!has_job(jj, N)) break;
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[jj][i], wb[jj][i], acc[jj], 0, 0, 0);
+            acc[jj] = M::mma(xa[jj][i], wb[jj][i], acc[jj]);
         }
       }
       const __amdgpu_buffer_rsrc_t dres = rsrc(p.D[l - 1]);
@@ -368,13 +417,13 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
       for (int jj = 0; jj < NJ; ++jj) {
         if (!has_job(jj, N)) break;
         const int u = unit(jj), rw = row(jj);
-        const unsigned vb = 4u * (unsigned)(rw * lda + u);
+        const unsigned vb = SZ * (unsigned)(rw * lda + u);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const bool ok = u < N && rw + v < rem;
-          const float d = ok ? acc[jj][v] * fp[l - 1][jj][v] : 0.0f;
-          bstore(d, dres, ok ? vb : MEDIUM_OOB, 4u * (unsigned)((s0 + v) * lda));
-          if (l > 1) hs[cur ^ 1][rw + v][u] = d;
+          const bool ok = u < N && rw + RS * v < rem;
+          const T d = ok ? acc[jj][v] * fp[l - 1][jj][v] : T(0);
+          M::store(d, dres, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((s0 + RS * v) * lda));
+          if (l > 1) hs[cur ^ 1][rw + RS * v][u] = d;
         }
       }
       cur ^= 1;
@@ -385,33 +434,43 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParams p)
 
 // 16-sample blocks per tile: enough for one tile per CU where that takes at
 // most 3 (3 blocks of 128 padded units fill LDS beside the largest weights);
-// bigger batches run several rounds of tiles
-static int medium_tile_blocks(int B, int ncu) {
+// bigger batches run several rounds of tiles.  fp64 tiles are one block (the
+// fp64 weights leave room for no more).
+static int medium_tile_blocks(int B, int ncu, int esz) {
+  if (esz == 8) return 1;
   const int blocks = (B + 15) / 16;
   const int nsb = (blocks + ncu - 1) / ncu;
   return nsb < 1 ? 1 : nsb > 3 ? 3 : nsb;
 }
 
-template <int NSB>
-static void launch_nsb(const MediumParams& p, dim3 grid, hipStream_t s) {
+template <class T, int NSB>
+static void launch_nsb(const MediumParamsT<T>& p, dim3 grid, hipStream_t s) {
   switch (p.L) {
-    case 2: medium_kernel<NSB, 2><<<grid, M_THREADS, 0, s>>>(p); break;
-    case 3: medium_kernel<NSB, 3><<<grid, M_THREADS, 0, s>>>(p); break;
-    default: medium_kernel<NSB, 4><<<grid, M_THREADS, 0, s>>>(p); break;
+    case 2: medium_kernel<T, NSB, 2><<<grid, M_THREADS, 0, s>>>(p); break;
+    case 3: medium_kernel<T, NSB, 3><<<grid, M_THREADS, 0, s>>>(p); break;
+    default: medium_kernel<T, NSB, 4><<<grid, M_THREADS, 0, s>>>(p); break;
   }
 }
 
-hipError_t launch_medium(const MediumParams& p, int ncu, hipStream_t s) {
+template <class T>
+hipError_t launch_medium(const MediumParamsT<T>& p, int ncu, hipStream_t s) {
   if (p.L < 2 || p.L > MEDIUM_MAX_LAYERS) return hipErrorInvalidValue;
-  const int nsb = medium_tile_blocks(p.B, ncu);
+  const int nsb = medium_tile_blocks(p.B, ncu, (int)sizeof(T));
   const int ntiles = (p.B + 16 * nsb - 1) / (16 * nsb);
   const dim3 grid(ntiles < ncu ? ntiles : ncu);
-  switch (nsb) {
-    case 1: launch_nsb<1>(p, grid, s); break;
-    case 2: launch_nsb<2>(p, grid, s); break;
-    default: launch_nsb<3>(p, grid, s); break;
+  if constexpr (sizeof(T) == 8) {
+    launch_nsb<T, 1>(p, grid, s);
+  } else {
+    switch (nsb) {
+      case 1: launch_nsb<T, 1>(p, grid, s); break;
+      case 2: launch_nsb<T, 2>(p, grid, s); break;
+      default: launch_nsb<T, 3>(p, grid, s); break;
+    }
   }
   return hipGetLastError();
 }
+
+template hipError_t launch_medium<float>(const MediumParamsT<float>&, int, hipStream_t);
+template hipError_t launch_medium<double>(const MediumParamsT<double>&, int, hipStream_t);
 
 }  // namespace nf

@@ -120,7 +120,7 @@ def test_f64_trajectory(dims, acts, batch, shards, eta, steps):
 
 # narrow fp64 networks (every layer after the input <= 32 units, even input
 # width) take the two-kernel step of csrc/nf_narrow64.hip; odd input widths and
-# split batches fall back to the contraction kernels on the same padded layout
+# split batches take the medium per-sample kernel on the same padded layout
 NARROW64 = [
     # dims, acts, batch, shards
     ((4, 3), ("sigmoid",), 1, 1),
@@ -130,9 +130,43 @@ NARROW64 = [
     ((66, 20, 20, 20, 20), ("tanh",), 33, 1),
     ((1026, 30, 10), ("sigmoid",), 2049, 1),
     ((12, 32, 32, 32, 32), ("relu", "tanh", "tanh", "sigmoid"), 100, 1),
-    ((7, 9, 4), ("tanh", "sigmoid"), 40, 1),          # odd input width: contraction kernels
-    ((64, 32, 10), ("sigmoid",), 96, 4),              # split batch: contraction kernels
+    ((7, 9, 4), ("tanh", "sigmoid"), 40, 1),          # odd input width: medium kernel
+    ((64, 32, 10), ("sigmoid",), 96, 4),              # split batch: medium kernel
 ]
+
+
+# the fp64 per-sample kernel (csrc/nf_medium.hip, 16-sample tiles): more
+# layer-1 pieces than are loaded ahead, 2 to 4 layers with ragged widths,
+# several rounds of tiles per workgroup, weights near the fp64 LDS limit, and
+# one network just past it (the contraction kernels)
+MEDIUM64 = [
+    # dims, acts, batch, shards
+    ((300, 120, 10), ("sigmoid",), 5, 1),
+    ((784, 100, 100, 10), ("tanh", "tanh", "sigmoid"), 100, 4),
+    ((20, 17, 31, 45, 7), ("tanh", "sigmoid", "gaussian", "sigmoid"), 5000, 2),
+    ((40, 96, 64, 48, 16), ("gaussian", "tanh", "sigmoid", "tanh"), 700, 1),
+    ((50, 128, 100, 10), ("tanh", "sigmoid", "sigmoid"), 300, 3),   # past the LDS limit
+    ((1, 1, 1), ("tanh",), 33, 1),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards", MEDIUM64)
+def test_f64_medium(dims, acts, batch, shards):
+    acts_full = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+    theta, X, Y = _problem(dims, 3 * sum(dims) + batch, batch * 2)
+    note(f"f64 medium dims={dims} batch={batch} shards={shards}")
+    ref = theta
+    fails = []
+    with Net64(dims, acts, theta) as net:
+        xd, yd = to_dev64(X), to_dev64(Y)
+        for t in range(2):
+            sl = slice(t * batch, (t + 1) * batch)
+            net.nf.nf_train_batch_f64(net.h, xd[sl], yd[sl], 0.5, shards)
+            ref, G = mlp.train_batch(ref, dims, acts_full, X[sl], Y[sl], 0.5, shards,
+                                     precision="f64")
+            fails += [f"step {t}: {m}" for m in _check(net.params(), ref, dims, "params")]
+            fails += [f"step {t}: {m}" for m in _check(net.grads(), G, dims, "grads")]
+    assert not fails, "\n".join(fails[:20])
 
 
 @pytest.mark.parametrize("dims,acts,batch,shards", NARROW64)
