@@ -645,7 +645,7 @@ nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, do
     st = timed(n, nf::narrow_fwd_name(true, fp), by, fl, s,
                [&] { return nf::launch_narrow_fwd(true, fp, s); });
   else
-    st = timed(n, "narrow64_fwd_train", by, fl, s,
+    st = timed(n, nf::narrow64_fwd_name(true, fp), by, fl, s,
                [&] { return nf::launch_narrow64_fwd(true, fp, s); });
   if (st != NF_OK) return st;
 
@@ -821,7 +821,7 @@ nf_status infer(nf_net* n, const T* x, int64_t batch, T* out, hipStream_t s) {
       return timed(n, nf::narrow_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow_fwd(false, fp, s); });
     else
-      return timed(n, "narrow64_fwd_infer", by, fl, s,
+      return timed(n, nf::narrow64_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow64_fwd(false, fp, s); });
   }
   return run_forward<T>(n, x, nullptr, batch, out, false, s);

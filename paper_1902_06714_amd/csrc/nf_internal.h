@@ -207,6 +207,7 @@ hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
 // The fp64 counterparts (16-sample tiles for every batch; no persistent
 // inference kernel).  Input rows need an even width.
 hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hipStream_t s);
+const char* narrow64_fwd_name(bool train, const NarrowFwdParamsT<double>& p);
 hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s);
 
 // ---------------------------------------------------------------------------

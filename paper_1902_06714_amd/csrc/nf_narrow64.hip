@@ -37,6 +37,8 @@ constexpr int D_CH = 8;                  // inputs per chunk: a 16-byte pair per
 constexpr int D_PRE = 4;                 // chunks per wave requested together
 constexpr int D_NWP = NARROW_WIDTH + 2;  // LDS row pitch (16-byte aligned rows)
 constexpr int D_NSTAGE = NARROW_WIDTH * NARROW_WIDTH / (D_WAVES * 64);
+// an offset past every range read through a buffer resource: zeros, no access
+constexpr unsigned D_OOB = NARROW_OOB;
 
 // sum over i < 32 of w[i] h[i] from two 16-byte aligned LDS rows, in four
 // interleaved partial sums added pairwise
@@ -56,6 +58,148 @@ __device__ __forceinline__ double dot32d(const double* w, const double* h) {
   return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
+// The weights of layers 2..L (padded 32 x 32 blocks, a zero block past the
+// last layer) for LDS, and every layer's bias of unit tid % 32 (the unit the
+// thread takes in the tail).  Loaded before layer 1, stored to LDS after it,
+// so the loads land while layer 1 runs.
+struct Small64 {
+  double w[NARROW_MAX_LAYERS - 1][D_NSTAGE];
+  double b[NARROW_MAX_LAYERS];
+};
+
+__device__ __forceinline__ void load_small64(const NarrowFwdParamsT<double>& p, int tid,
+                                             Small64& r) {
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < D_NSTAGE; ++u) r.w[li][u] = p.W[li + 1][tid + u * D_WAVES * 64];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) r.b[l] = p.bias[l][tid & (NARROW_WIDTH - 1)];
+}
+
+// ws[l][j][i] = W(j, i) for the forward sums and, when training,
+// wsT[l][i][j] = W(j, i) for the delta sums
+template <bool TRANSPOSED>
+__device__ __forceinline__ void store_small64(const Small64& r, int tid,
+                                              double (*ws)[NARROW_WIDTH][D_NWP],
+                                              double (*wsT)[NARROW_WIDTH][D_NWP]) {
+  constexpr int NW = NARROW_WIDTH;
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < D_NSTAGE; ++u) {
+      const int e = tid + u * D_WAVES * 64;
+      ws[li][e / NW][e % NW] = r.w[li][u];
+      if (TRANSPOSED) wsT[li][e % NW][e / NW] = r.w[li][u];
+    }
+}
+
+// target of (sample tid / 32, unit tid % 32) of a T-sample tile, read from a
+// clamped position so the load carries no branch
+template <int T>
+__device__ __forceinline__ double load_target64(const NarrowFwdParamsT<double>& p, int s0,
+                                                int tid) {
+  const int ys = s0 + (tid >> 5), yu = tid & 31;
+  const bool ok = tid < T * NARROW_WIDTH && ys < p.B && yu < p.dout;
+  const int yr = ys < p.B ? ys : p.B - 1, yc = yu < p.dout ? yu : p.dout - 1;
+  const double v = p.Y[(int64_t)yr * p.dout + yc];
+  return ok ? v : 0.0;
+}
+
+// Everything after the layer-1 sums, for thread (s, j) = (tid / 32, tid % 32):
+// sample s of the T-sample tile, unit j.  Layer 1's activation, layers 2..L
+// with the previous layer in LDS (padded units carry zeros, so every sum runs
+// over 32), the output delta (a_L - y) f'(z_L) and the hidden deltas
+// (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with f'(z_l) kept in
+// registers.  Threads past 32 T only join the barriers.
+template <bool TRAIN, int T>
+__device__ __forceinline__ void narrow64_tail(const NarrowFwdParamsT<double>& p, int s0, int tid,
+                                              double z1, double ytg, double (*hs)[T][D_NWP],
+                                              const double (*ws)[NARROW_WIDTH][D_NWP],
+                                              const double (*wsT)[NARROW_WIDTH][D_NWP],
+                                              const double (&bias)[NARROW_MAX_LAYERS]) {
+  constexpr int NW = NARROW_WIDTH;
+  const bool active = T * NW >= D_WAVES * 64 || tid < T * NW;
+  const int s = active ? tid >> 5 : 0, j = tid & 31;
+  const int gs = s0 + s;
+  const bool s_ok = active && gs < p.B;
+  double fp[NARROW_MAX_LAYERS];
+#pragma unroll
+  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0;
+  int cur = 0;
+  if (active) {
+    double a = 0.0, f = 0.0;
+    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bias[0], a, f);
+    fp[0] = f;
+    if (p.L == 1) {
+      if (TRAIN) {
+        const double d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0;
+        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
+      } else if (s_ok && j < p.dims[1]) {
+        p.out[(int64_t)gs * p.dims[1] + j] = a;
+      }
+    } else {
+      hs[0][s][j] = a;
+      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
+    }
+  }
+  __syncthreads();
+
+  // ---- layers 2..L
+#pragma unroll
+  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
+    if (l > p.L) break;
+    if (active) {
+      const int dl = p.dims[l];
+      const double z = dot32d(ws[l - 2][j], hs[cur][s]);
+      double a = 0.0, f = 0.0;
+      if (j < dl) act_eval(p.acts[l - 1], z + bias[l - 1], a, f);
+      fp[l - 1] = f;
+      if (l == p.L) {
+        if (TRAIN) {
+          const double d = (j < dl && s_ok) ? (a - ytg) * f : 0.0;
+          hs[cur ^ 1][s][j] = d;
+          if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+        } else if (s_ok && j < dl) {
+          p.out[(int64_t)gs * dl + j] = a;
+        }
+      } else {
+        hs[cur ^ 1][s][j] = a;
+        if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
+      }
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (!TRAIN) return;
+
+  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
+  // (layer 1's delta is read by no later phase: no LDS copy, no barrier)
+#pragma unroll
+  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
+    if (l >= p.L) continue;
+    if (active) {
+      const double t = dot32d(wsT[l - 1][j], hs[cur][s]);
+      const double d = j < p.dims[l] ? t * fp[l - 1] : 0.0;
+      if (l > 1) hs[cur ^ 1][s][j] = d;
+      if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
+    }
+    cur ^= 1;
+    if (l > 1) __syncthreads();
+  }
+}
+
+// 4-sample tiles: layer 1 on v_mfma_f64_4x4x4f64, whose four 4x4x4 blocks
+// take lane l = 16 k + 4 b + x as row x, input k of block b's A and input k,
+// column x of its B, and leave block b's (i, j) entry in lane 16 i + 4 b + j.
+constexpr int D4_T = 4;                    // samples per tile
+constexpr int D4_KS = 32;                  // inputs per step: one 16-byte pair per (block, input) lane
+constexpr int D4_PRE = 4;                  // steps per wave requested together
+constexpr int D4_UG = NARROW_WIDTH / 4;    // groups of 4 units
+constexpr int D4_PARTS = D_WAVES * 4;      // (wave, block) sums of each output
+constexpr int D4_RP = NARROW_WIDTH + 4;    // row pitch of the sums: a wave's 16-lane groups write 32 banks
+constexpr int D4_SS = D4_PARTS * D4_RP;    // sample stride of the sums
+
 }  // namespace
 
 template <bool TRAIN>
@@ -72,24 +216,9 @@ __global__ void __launch_bounds__(D_WAVES * 64) narrow64_fwd_kernel(const Narrow
   const int wave = tid >> 6;
   const int s0 = blockIdx.x * T;
 
-  // the weights of layers 2..L (padded 32 x 32 blocks, a zero block past the
-  // last layer) for LDS, and the biases of unit tid % 32 (the unit this
-  // thread takes in the tail)
-  double wsm[NARROW_MAX_LAYERS - 1][D_NSTAGE], bias[NARROW_MAX_LAYERS];
-#pragma unroll
-  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
-#pragma unroll
-    for (int u = 0; u < D_NSTAGE; ++u) wsm[li][u] = p.W[li + 1][tid + u * D_WAVES * 64];
-#pragma unroll
-  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) bias[l] = p.bias[l][tid & (NW - 1)];
-  // target of (sample tid / 32, unit tid % 32), read from a clamped position
-  double ytg = 0.0;
-  if (TRAIN) {
-    const int ys = s0 + (tid >> 5), yu = tid & 31;
-    const int yr = ys < p.B ? ys : p.B - 1, yc = yu < p.dout ? yu : p.dout - 1;
-    const double v = p.Y[(int64_t)yr * p.dout + yc];
-    ytg = (ys < p.B && yu < p.dout) ? v : 0.0;
-  }
+  Small64 sl;
+  load_small64(p, tid, sl);
+  const double ytg = TRAIN ? load_target64<T>(p, s0, tid) : 0.0;
 
   // ---- layer 1: lane (r, g) = (lane % 16, lane / 16) feeds sample r and
   // units r, 16 + r with inputs 8 c + 2 g and 8 c + 2 g + 1 of chunk c (one
@@ -129,85 +258,125 @@ __global__ void __launch_bounds__(D_WAVES * 64) narrow64_fwd_kernel(const Narrow
       zp[wave][4 * v + g][16 + r] = acc1[v];
     }
   }
-  // the small layers to LDS: ws[l][j][i] = W(j, i) for the forward sums and,
-  // when training, wsT[l][i][j] = W(j, i) for the delta sums
-#pragma unroll
-  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
-#pragma unroll
-    for (int u = 0; u < D_NSTAGE; ++u) {
-      const int e = tid + u * D_WAVES * 64;
-      ws[li][e / NW][e % NW] = wsm[li][u];
-      if (TRAIN) wsT[li][e % NW][e / NW] = wsm[li][u];
-    }
+  store_small64<TRAIN>(sl, tid, ws, wsT);
   __syncthreads();
 
-  // ---- thread (s, j) = (tid / 32, tid % 32): sample s of the tile, unit j
-  const int s = tid >> 5, j = tid & 31;
-  const int gs = s0 + s;
-  const bool s_ok = gs < p.B;
-  double z1 = zp[0][s][j];
-#pragma unroll
-  for (int w = 1; w < D_WAVES; ++w) z1 += zp[w][s][j];
-  double fp[NARROW_MAX_LAYERS];
-#pragma unroll
-  for (int l = 0; l < NARROW_MAX_LAYERS; ++l) fp[l] = 0.0;
-  int cur = 0;
+  // the waves' sums in wave order
+  double z1 = 0.0;
   {
-    double a = 0.0, f = 0.0;
-    if (j < p.dims[1]) act_eval(p.acts[0], z1 + bias[0], a, f);
-    fp[0] = f;
-    if (p.L == 1) {
-      if (TRAIN) {
-        const double d = (j < p.dims[1] && s_ok) ? (a - ytg) * f : 0.0;
-        if (s_ok) p.D[0][(int64_t)gs * NW + j] = d;
-      } else if (s_ok && j < p.dims[1]) {
-        p.out[(int64_t)gs * p.dims[1] + j] = a;
-      }
-    } else {
-      hs[0][s][j] = a;
-      if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
-    }
+    const int s = tid >> 5, j = tid & 31;
+    z1 = zp[0][s][j];
+#pragma unroll
+    for (int w = 1; w < D_WAVES; ++w) z1 += zp[w][s][j];
   }
+  narrow64_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, sl.b);
+}
+
+// One workgroup of 8 waves per 4-sample tile (batches up to
+// NARROW_SMALL_BATCH, so a 1000-sample batch spreads over 250 CUs).  Layer 1:
+// lane (k, b, x) = (lane / 16, lane / 4 % 4, lane % 4) loads a 16-byte pair of
+// sample x's row and of W_1 rows 4 g + x (the 8 unit groups g) at inputs
+// 32 t + 2 (4 b + k) and + 1 of step t; the pair's two elements feed two
+// instructions per unit group.  Block b of wave w thus sums its own inputs,
+// and the 32 (wave, block) sums of each output are added in a fixed order.
+template <bool TRAIN>
+__global__ void __launch_bounds__(D_WAVES * 64) narrow64_fwd4_kernel(const NarrowFwdParamsT<double> p) {
+  constexpr int T = D4_T;
+  constexpr int NW = NARROW_WIDTH;
+  __shared__ double red[T * D4_SS];                                 // [sample][wave*4+block][unit]
+  __shared__ double psum[4][T][NW];
+  __shared__ __attribute__((aligned(16))) double hs[2][T][D_NWP];
+  __shared__ __attribute__((aligned(16))) double ws[NARROW_MAX_LAYERS - 1][NW][D_NWP];
+  __shared__ __attribute__((aligned(16))) double wsT[TRAIN ? NARROW_MAX_LAYERS - 1 : 1][NW][D_NWP];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int s0 = blockIdx.x * T;
+
+  Small64 sl;
+  load_small64(p, tid, sl);
+  const double ytg = TRAIN ? load_target64<T>(p, s0, tid) : 0.0;
+
+  {
+    const int x = lane & 3, b = (lane >> 2) & 3, kq = lane >> 4;
+    const int pos = 4 * b + kq;
+    // the tile's input rows and W_1's d_1 rows through buffer resources that
+    // end at the last row: rows past the batch, W_1's padding rows and inputs
+    // past the width (given an offset past the end) read as zeros without a
+    // memory access.  The width is even, so a pair is wholly in or out.
+    const int nrows = p.B - s0 < T ? p.B - s0 : T;
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.X + (int64_t)s0 * p.d0), (short)0, nrows * p.d0 * 8, 0x00020000);
+    const int ldw1 = (int)p.ldw[0];
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)p.W[0], (short)0, p.dims[1] * ldw1 * 8, 0x00020000);
+    double acc[D4_UG];
+#pragma unroll
+    for (int ug = 0; ug < D4_UG; ++ug) acc[ug] = 0.0;
+    const int nsteps = (p.d0 + D4_KS - 1) / D4_KS;
+    // workgroups start at different steps (rotated by the tile index), so the
+    // workgroups that start together do not all ask for the same W_1 lines
+    const int rot = (int)(blockIdx.x % (unsigned)nsteps);
+    // the first block of steps runs unconditionally (a wave without steps adds
+    // zeros), so its loads are not held behind a branch
+    int t0 = wave;
+    do {
+      double2 xr[D4_PRE], wr[D4_PRE][D4_UG];
+#pragma unroll
+      for (int u = 0; u < D4_PRE; ++u) {
+        int t = t0 + u * D_WAVES;
+        if (t < nsteps) t = t + rot < nsteps ? t + rot : t + rot - nsteps;
+        const int k = t * D4_KS + 2 * pos;
+        const bool ok = k < p.d0;
+        xr[u] = __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(
+                                                xres, ok ? 8 * (x * p.d0 + k) : (int)D_OOB, 0, 0));
+#pragma unroll
+        for (int ug = 0; ug < D4_UG; ++ug)
+          wr[u][ug] = __builtin_bit_cast(
+              double2, __builtin_amdgcn_raw_buffer_load_b128(
+                           wres, ok ? 8 * ((4 * ug + x) * ldw1 + k) : (int)D_OOB, 0, 0));
+      }
+      // keep every load of the block ahead of the first matrix instruction
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < D4_PRE; ++u) {
+#pragma unroll
+        for (int ug = 0; ug < D4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f64_4x4x4f64(xr[u].x, wr[u][ug].x, acc[ug], 0, 0, 0);
+#pragma unroll
+        for (int ug = 0; ug < D4_UG; ++ug)
+          acc[ug] = __builtin_amdgcn_mfma_f64_4x4x4f64(xr[u].y, wr[u][ug].y, acc[ug], 0, 0, 0);
+      }
+      t0 += D_WAVES * D4_PRE;
+    } while (t0 < nsteps);
+    // lane (i, b, j) = (lane / 16, lane / 4 % 4, lane % 4) holds block b's sum
+    // for sample i, unit 4 g + j
+    const int i = lane >> 4, j = lane & 3;
+#pragma unroll
+    for (int ug = 0; ug < D4_UG; ++ug)
+      red[i * D4_SS + (wave * 4 + b) * D4_RP + 4 * ug + j] = acc[ug];
+  }
+  store_small64<TRAIN>(sl, tid, ws, wsT);
   __syncthreads();
 
-  // ---- layers 2..L (padded units carry zeros, so every sum runs over 32)
+  // every thread adds a quarter of the (wave, block) sums of one output, in
+  // order; the quarters are then added pairwise
+  {
+    const int part = tid >> 7, s = (tid >> 5) & 3, j = tid & 31;
+    const double* src = red + s * D4_SS + part * (D4_PARTS / 4) * D4_RP + j;
+    double t = src[0];
 #pragma unroll
-  for (int l = 2; l <= NARROW_MAX_LAYERS; ++l) {
-    if (l > p.L) break;
-    const int dl = p.dims[l];
-    const double z = dot32d(ws[l - 2][j], hs[cur][s]);
-    double a = 0.0, f = 0.0;
-    if (j < dl) act_eval(p.acts[l - 1], z + bias[l - 1], a, f);
-    fp[l - 1] = f;
-    if (l == p.L) {
-      if (TRAIN) {
-        const double d = (j < dl && s_ok) ? (a - ytg) * f : 0.0;
-        hs[cur ^ 1][s][j] = d;
-        if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
-      } else if (s_ok && j < dl) {
-        p.out[(int64_t)gs * dl + j] = a;
-      }
-    } else {
-      hs[cur ^ 1][s][j] = a;
-      if (TRAIN && s_ok) p.A[l - 1][(int64_t)gs * NW + j] = a;
-    }
-    cur ^= 1;
-    __syncthreads();
+    for (int r = 1; r < D4_PARTS / 4; ++r) t += src[r * D4_RP];
+    psum[part][s][j] = t;
   }
-  if (!TRAIN) return;
-
-  // ---- hidden deltas, l = L-1 .. 1, with the weights W_{l+1} of this step
-  // (layer 1's delta is read by no later phase: no LDS copy, no barrier)
-#pragma unroll
-  for (int l = NARROW_MAX_LAYERS - 1; l >= 1; --l) {
-    if (l >= p.L) continue;
-    const double t = dot32d(wsT[l - 1][j], hs[cur][s]);
-    const double d = j < p.dims[l] ? t * fp[l - 1] : 0.0;
-    if (l > 1) hs[cur ^ 1][s][j] = d;
-    if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
-    cur ^= 1;
-    if (l > 1) __syncthreads();
+  __syncthreads();
+  double z1 = 0.0;
+  if (tid < T * NW) {
+    const int s = tid >> 5, j = tid & 31;
+    z1 = (psum[0][s][j] + psum[1][s][j]) + (psum[2][s][j] + psum[3][s][j]);
   }
+  narrow64_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, sl.b);
 }
 
 // Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the
@@ -319,12 +488,25 @@ __global__ void __launch_bounds__(D2_WAVES * 64) narrow64_dw_kernel(const Narrow
 }
 
 hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hipStream_t s) {
+  if (p.B <= NARROW_SMALL_BATCH) {
+    const dim3 grid((p.B + D4_T - 1) / D4_T);
+    if (train)
+      narrow64_fwd4_kernel<true><<<grid, D_WAVES * 64, 0, s>>>(p);
+    else
+      narrow64_fwd4_kernel<false><<<grid, D_WAVES * 64, 0, s>>>(p);
+    return hipGetLastError();
+  }
   const dim3 grid((p.B + D_T - 1) / D_T);
   if (train)
     narrow64_fwd_kernel<true><<<grid, D_WAVES * 64, 0, s>>>(p);
   else
     narrow64_fwd_kernel<false><<<grid, D_WAVES * 64, 0, s>>>(p);
   return hipGetLastError();
+}
+
+const char* narrow64_fwd_name(bool train, const NarrowFwdParamsT<double>& p) {
+  if (p.B <= NARROW_SMALL_BATCH) return train ? "narrow64_fwd4_train" : "narrow64_fwd4_infer";
+  return train ? "narrow64_fwd_train" : "narrow64_fwd_infer";
 }
 
 hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s) {

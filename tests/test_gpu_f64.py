@@ -119,8 +119,9 @@ def test_f64_trajectory(dims, acts, batch, shards, eta, steps):
 
 
 # narrow fp64 networks (every layer after the input <= 32 units, even input
-# width) take the two-kernel step of csrc/nf_narrow64.hip; odd input widths and
-# split batches take the medium per-sample kernel on the same padded layout
+# width) take the two-kernel step of csrc/nf_narrow64.hip (4-sample tiles up
+# to 2048 samples, 16-sample tiles above); odd input widths and split batches
+# take the medium per-sample kernel on the same padded layout
 NARROW64 = [
     # dims, acts, batch, shards
     ((4, 3), ("sigmoid",), 1, 1),
@@ -128,7 +129,9 @@ NARROW64 = [
     ((60, 7, 2), ("sigmoid", "tanh"), 3, 1),
     ((64, 32, 31, 1), ("gaussian", "tanh", "sigmoid"), 17, 1),
     ((66, 20, 20, 20, 20), ("tanh",), 33, 1),
-    ((1026, 30, 10), ("sigmoid",), 2049, 1),
+    ((1026, 30, 10), ("sigmoid",), 2049, 1),         # above 2048: 16-sample tiles
+    ((1090, 30, 10), ("sigmoid",), 37, 1),           # 4-sample tiles, two rounds of input steps
+    ((2050, 5), ("tanh",), 6, 1),                     # three rounds, a ragged last tile
     ((12, 32, 32, 32, 32), ("relu", "tanh", "tanh", "sigmoid"), 100, 1),
     ((7, 9, 4), ("tanh", "sigmoid"), 40, 1),          # odd input width: medium kernel
     ((64, 32, 10), ("sigmoid",), 96, 4),              # split batch: medium kernel
