@@ -1,10 +1,11 @@
 // Training step and inference for narrow fp64 networks (the paper's real64
 // kind, section 2; every layer after the input has at most 32 units), on the
-// fp64 matrix cores (v_mfma_f64_16x16x4f64).  Two kernels per step, as in
-// fp32:
-//   per-sample pass   one workgroup of 8 waves per 16-sample tile: layer 1
-//                     with the input width split over the waves and their
-//                     sums added in wave order; layers 2..L, the output delta
+// fp64 matrix cores.  Two kernels per step, as in fp32:
+//   per-sample pass   one workgroup of 8 waves per 4-sample tile (batches up
+//                     to NARROW_SMALL_BATCH, v_mfma_f64_4x4x4f64) or 16-sample
+//                     tile (v_mfma_f64_16x16x4f64): layer 1 with the input
+//                     width split over the waves and their sums added in a
+//                     fixed order; layers 2..L, the output delta
 //                     (a_L - y) f'(z_L) and the hidden deltas
 //                     (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) one thread
 //                     per (sample, unit) with the small layers in LDS;
@@ -13,9 +14,9 @@
 //                     block, its waves splitting the batch and their sums
 //                     added in wave order, and writes W' = W - (eta/B) G into
 //                     the other parameter buffer (sections 3.3-3.5).
-// The fp64 matrix core takes 4 inputs per instruction with lane l supplying
-// row l % 16 and input l / 16 of A, input l / 16 and column l % 16 of B;
-// accumulator register v of lane l holds row 4 v + l / 16, column l % 16.
+// The 16x16x4 fp64 instruction takes lane l's A entry (row l % 16, input
+// l / 16) and B entry (input l / 16, column l % 16); accumulator register v of
+// lane l holds row 4 v + l / 16, column l % 16.
 // Every sum runs in a fixed order, so results are reproducible bit for bit.
 #include "nf_act.h"
 #include "nf_internal.h"
