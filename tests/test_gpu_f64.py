@@ -132,6 +132,7 @@ NARROW64 = [
     ((1026, 30, 10), ("sigmoid",), 2049, 1),         # above 2048: 16-sample tiles
     ((1090, 30, 10), ("sigmoid",), 37, 1),           # 4-sample tiles, two rounds of input steps
     ((2050, 5), ("tanh",), 6, 1),                     # three rounds, a ragged last tile
+    ((65536, 30, 10), ("sigmoid",), 5, 1),           # the widest input: 2048 input steps
     ((12, 32, 32, 32, 32), ("relu", "tanh", "tanh", "sigmoid"), 100, 1),
     ((7, 9, 4), ("tanh", "sigmoid"), 40, 1),          # odd input width: medium kernel
     ((64, 32, 10), ("sigmoid",), 96, 4),              # split batch: medium kernel

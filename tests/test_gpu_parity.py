@@ -106,6 +106,26 @@ def test_narrow_edges(dims, acts, batch):
     _compare_trajectory(dims, acts, theta, X, Y, batch, 1.0, 1, 2)
 
 
+# the widest layers the library takes (65536 units): the input of a narrow
+# network (4-sample tiles over 1024 input steps), a hidden layer of a general
+# one, and an output layer with a split batch.  The step size keeps the
+# second step's output pre-activations O(1): at eta = 1 the 65536-input output
+# units reach |z| ~ 2000, every sigmoid but one saturates, and the one
+# remaining gradient hangs on an fp32 sum of 65536 terms with partial sums far
+# larger than its value (a 1e-3 relative spread for any fp32 summation order)
+MAX_WIDTHS = [
+    ((65536, 30, 10), ("sigmoid",), 9, 1, 1.0),
+    ((5, 65536, 3), ("tanh", "sigmoid"), 7, 1, 1e-3),
+    ((3, 200, 65536), ("relu", "sigmoid"), 6, 2, 1.0),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards,eta", MAX_WIDTHS)
+def test_maximum_widths(dims, acts, batch, shards, eta):
+    theta, X, Y = _problem(dims, 11 + batch, batch * 2)
+    _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 2)
+
+
 # the per-sample pass for fp32 networks of 2 to 4 layers up to 128 units
 # wide: tiles of one, two and three 16-sample blocks (the tile grows with the
 # batch: over 4096 and over 8192 samples), several rounds of tiles per
