@@ -6,7 +6,10 @@ One step is one pass of the whole training path over the workload's data:
 every SGD step of one epoch (forward, back-propagation, batch tendencies,
 update) plus, where the workload has a held-out set, batched inference on it.
 Inputs are resident in device memory before timing starts.  Prints one JSON
-line on stdout; per-kernel timings go to stderr.
+line on stdout; per-kernel timings go to stderr.  `value` is the warm rate
+(the K timed steps back to back); `cold_cache` times single steps after a
+write larger than the 256 MB memory-side cache, each from the initial
+parameters.
 
 --dtype f64 runs the same workload with an fp64 net (the paper's real64 kind):
 inputs, targets and parameters in fp64, every kernel in fp64, the roofline
@@ -126,6 +129,10 @@ def main(argv=None) -> int:
                     help="element type of the net (f64: the real64 variant)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU-reference timing (0 skips it)")
+    ap.add_argument("--cold-reps", type=int, default=3,
+                    help="steps timed one at a time after flushing the memory-side cache")
+    ap.add_argument("--flush-mib", type=int, default=512,
+                    help="bytes written between cold steps (above the 256 MB memory-side cache)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="only run a plain device copy of this size 20 times (counter scale)")
     args = ap.parse_args(argv)
@@ -201,6 +208,30 @@ def main(argv=None) -> int:
         print(f"[bench] timed {args.steps} steps: {ms:.3f} ms (events), {wall * 1e3:.3f} ms (wall)",
               file=sys.stderr, flush=True)
 
+        # the same step with the data out of the 256 MB memory-side cache (the
+        # 188 MB training set of the 784-30-10 workload fits in it): each
+        # repetition restarts from the initial parameters, writes a larger
+        # buffer, then times one step on its own (all but the step untimed)
+        cold = []
+        if args.cold_reps > 0:
+            flush = torch.empty(args.flush_mib * (1 << 18), dtype=torch.float32, device=dev)
+            for r in range(args.cold_reps):
+                if f64:
+                    nf.nf_set_params_f64(net, theta0.astype(np.float64))
+                else:
+                    nf.nf_set_params(net, theta0)
+                flush.fill_(float(r))
+                torch.cuda.synchronize()
+                ev0.record(stream)
+                step()
+                ev1.record(stream)
+                torch.cuda.synchronize()
+                cold.append(ev0.elapsed_time(ev1))
+            del flush
+            print(f"[bench] after a {args.flush_mib} MiB flush: "
+                  + ", ".join(f"{c:.3f}" for c in cold) + " ms per step", file=sys.stderr,
+                  flush=True)
+
         # per-kernel durations, same workload and launch configuration: every
         # launch runs PROFILE_REPEATS times back to back between two events on
         # the stream it is launched on (kernels never write what they read)
@@ -270,6 +301,11 @@ def main(argv=None) -> int:
         "kernels": kernels,
         "params_finite": finite,
     }
+    if cold:
+        med = float(np.median(cold))
+        line["cold_cache"] = {"value": n_train / (med / 1e3), "unit": "samples/s",
+                              "ms_per_step_median": med, "ms_per_step": cold,
+                              "flush_bytes": args.flush_mib << 20}
     if args.cpu_seconds > 0:
         print(f"[bench] timing the CPU reference (~{args.cpu_seconds:.0f} s)", file=sys.stderr,
               flush=True)
