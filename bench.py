@@ -91,7 +91,7 @@ def cpu_baseline(w, X, Y, Xh, budget_s: float, precision: str = "f32"):
     except Exception:
         cores = os.cpu_count() or 1
     theta = W.make_params(w)
-    t0 = time.perf_counter()
+    t0, c0 = time.perf_counter(), time.process_time()
     reps, sgd_steps, stop = 0, 0, False
     n_train = w.batch * w.steps
     while not stop:
@@ -109,6 +109,7 @@ def cpu_baseline(w, X, Y, Xh, budget_s: float, precision: str = "f32"):
             reps += 1
             stop = time.perf_counter() - t0 >= budget_s
     el = time.perf_counter() - t0
+    busy = (time.process_time() - c0) / el   # CPU seconds of all threads per second
     samples = sgd_steps * w.batch
     if reps >= 1 and sgd_steps == reps * w.steps:
         sample = f"{reps} full step(s) of the workload ({reps * n_train} training samples" + (
@@ -116,7 +117,8 @@ def cpu_baseline(w, X, Y, Xh, budget_s: float, precision: str = "f32"):
     else:
         sample = f"the first {sgd_steps} SGD steps ({samples} training samples) of the workload"
     return {"value": samples / el, "unit": "samples/s", "cores": cores, "kind": "oracle",
-            "sample": sample + f", {el:.1f} s on the host"}
+            "sample": sample + f", {el:.1f} s on the host",
+            "cpu_seconds_per_second": round(busy, 2)}
 
 
 def main(argv=None) -> int:
@@ -310,6 +312,18 @@ def main(argv=None) -> int:
         print(f"[bench] timing the CPU reference (~{args.cpu_seconds:.0f} s)", file=sys.stderr,
               flush=True)
         line["cpu_baseline"] = cpu_baseline(w, X, Y, Xh, args.cpu_seconds, args.dtype)
+        if w.name in ("c1", "c2"):
+            # the same reference on one core, beside the paper's one-core timing
+            # of this network shape (section 5); context only
+            try:
+                from threadpoolctl import threadpool_limits
+            except ImportError:
+                threadpool_limits = None
+            if threadpool_limits is not None:
+                with threadpool_limits(limits=1):
+                    one = cpu_baseline(w, X, Y, Xh, args.cpu_seconds / 2, args.dtype)
+                one["cores"] = 1
+                line["cpu_baseline_1core"] = one
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)
