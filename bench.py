@@ -198,15 +198,18 @@ def main(argv=None) -> int:
             step()
         torch.cuda.synchronize()
         stream = torch.cuda.current_stream()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # an event between consecutive steps gives the spread of single steps
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        ev0, ev1 = evs[0], evs[-1]
         t0 = time.perf_counter()
         ev0.record(stream)
-        for _ in range(args.steps):
+        for i in range(args.steps):
             step()
-        ev1.record(stream)
+            evs[i + 1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         ms = ev0.elapsed_time(ev1)
+        per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
         print(f"[bench] timed {args.steps} steps: {ms:.3f} ms (events), {wall * 1e3:.3f} ms (wall)",
               file=sys.stderr, flush=True)
 
@@ -303,6 +306,9 @@ def main(argv=None) -> int:
         "kernels": kernels,
         "params_finite": finite,
     }
+    line["per_step_ms"] = {"mean": float(np.mean(per_step)), "std": float(np.std(per_step)),
+                           "median": float(np.median(per_step)), "min": float(np.min(per_step)),
+                           "max": float(np.max(per_step))}
     if cold:
         med = float(np.median(cold))
         line["cold_cache"] = {"value": n_train / (med / 1e3), "unit": "samples/s",
