@@ -119,12 +119,30 @@ __device__ __forceinline__ float load_target(const NarrowFwdParams& p, int s0, i
   return ok ? v : 0.0f;
 }
 
+// The tail's thread (s, j) = (tid / 32, tid % 32) keeps each sample's 32 units
+// in one wave, so every phase of the tail reads only what its own wave wrote
+// in the phase before: LDS operations of a wave complete in order, and a
+// wavefront-scope fence keeps the compiler from moving them across the
+// boundary.  The persistent inference kernel (BLOCK) still needs workgroup
+// barriers: it reuses the layer-1 sums and the staged outputs across waves.
+template <bool BLOCK>
+__device__ __forceinline__ void tail_sync() {
+  if constexpr (BLOCK) {
+    __syncthreads();
+  } else {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
 // Everything after the layer-1 sums, for thread (s, j) = (tid / 32, tid % 32):
 // sample s of the T-sample tile, unit j of the current layer.  Layer 1's
 // activation, layers 2..L with the previous layer in LDS (padded units carry
 // zeros, so every sum runs over 32), the output delta (a_L - y) f'(z_L) and
 // the hidden deltas (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with
-// f'(z_l) kept in registers.  Threads past 32 T only join the barriers.
+// f'(z_l) kept in registers.  Threads past 32 T only join the workgroup
+// barriers of the inference kernel.
 // Inference writes f(z_L) to the output, or with STAGED to ostage[s][j] in LDS.
 template <bool TRAIN, int T, bool STAGED = false>
 __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, int tid, float z1,
@@ -160,7 +178,7 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
       if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
     }
   }
-  __syncthreads();
+  tail_sync<STAGED>();
 
   // ---- layers 2..L
 #pragma unroll
@@ -188,7 +206,7 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
       }
     }
     cur ^= 1;
-    __syncthreads();
+    tail_sync<STAGED>();
   }
   if (!TRAIN) return;
 
@@ -204,7 +222,7 @@ __device__ __forceinline__ void narrow_tail(const NarrowFwdParams& p, int s0, in
       if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
     }
     cur ^= 1;
-    if (l > 1) __syncthreads();
+    if (l > 1) tail_sync<STAGED>();
   }
 }
 

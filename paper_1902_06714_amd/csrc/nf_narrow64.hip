@@ -107,12 +107,23 @@ __device__ __forceinline__ double load_target64(const NarrowFwdParamsT<double>& 
   return ok ? v : 0.0;
 }
 
+// The tail's thread (s, j) = (tid / 32, tid % 32) keeps each sample's 32 units
+// in one wave, so every phase of the tail reads only what its own wave wrote
+// in the phase before: LDS operations of a wave complete in order, and a
+// wavefront-scope fence keeps the compiler from moving them across the
+// boundary.
+__device__ __forceinline__ void tail_sync64() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Everything after the layer-1 sums, for thread (s, j) = (tid / 32, tid % 32):
 // sample s of the T-sample tile, unit j.  Layer 1's activation, layers 2..L
 // with the previous layer in LDS (padded units carry zeros, so every sum runs
 // over 32), the output delta (a_L - y) f'(z_L) and the hidden deltas
 // (W_{l+1}^T delta_{l+1}) f'(z_l) (section 3.3) with f'(z_l) kept in
-// registers.  Threads past 32 T only join the barriers.
+// registers.  Threads past 32 T have no part in it.
 template <bool TRAIN, int T>
 __device__ __forceinline__ void narrow64_tail(const NarrowFwdParamsT<double>& p, int s0, int tid,
                                               double z1, double ytg, double (*hs)[T][D_NWP],
@@ -144,7 +155,7 @@ __device__ __forceinline__ void narrow64_tail(const NarrowFwdParamsT<double>& p,
       if (TRAIN && s_ok) p.A[0][(int64_t)gs * NW + j] = a;
     }
   }
-  __syncthreads();
+  tail_sync64();
 
   // ---- layers 2..L
 #pragma unroll
@@ -170,7 +181,7 @@ __device__ __forceinline__ void narrow64_tail(const NarrowFwdParamsT<double>& p,
       }
     }
     cur ^= 1;
-    __syncthreads();
+    tail_sync64();
   }
   if (!TRAIN) return;
 
@@ -186,7 +197,7 @@ __device__ __forceinline__ void narrow64_tail(const NarrowFwdParamsT<double>& p,
       if (s_ok) p.D[l - 1][(int64_t)gs * NW + j] = d;
     }
     cur ^= 1;
-    if (l > 1) __syncthreads();
+    if (l > 1) tail_sync64();
   }
 }
 
