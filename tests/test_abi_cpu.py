@@ -3,6 +3,7 @@ function include/nf.h declares, rejects bad arguments before touching the
 device, and reports a missing device as an error instead of falling back."""
 
 import ctypes
+import os
 
 import pytest
 
@@ -175,3 +176,46 @@ def test_load_of_a_valid_file_needs_a_device(tmp_path):
 
 def test_save_rejects_null():
     assert nf.raw().nf_save(None, b"/tmp/x") == nf.NF_EINVAL
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include "nf.h"
+int main(void) {
+  int32_t bad[2] = {784, 0};
+  nf_net* net = NULL;
+  if (nf_net_create(bad, 2, NULL, 0, &net) != NF_ESHAPE || net != NULL) return 1;
+  if (nf_last_error()[0] == '\0') return 2;
+  int32_t dims[3] = {784, 30, 10};
+  nf_status st = nf_net_create(dims, 3, NULL, 0, &net);
+  if (st == NF_OK) {
+    if (nf_param_count(net) != 784 * 30 + 30 + 30 * 10 + 10) return 3;
+    nf_net_destroy(net);
+    puts("created");
+    return 0;
+  }
+  if (st == NF_EDEVICE) {
+    puts("no device");
+    return 0;
+  }
+  return 4;
+}
+"""
+
+
+def test_plain_c_program_links_and_calls_the_library(tmp_path):
+    """The ABI used from C, without Python: a program built with gcc against
+    include/nf.h and linked to the library validates a bad net, then creates
+    one (or reports the missing device) through the same entry points."""
+    import subprocess
+    src = tmp_path / "prog.c"
+    src.write_text(C_PROGRAM)
+    exe = tmp_path / "prog"
+    libdir = os.path.dirname(nf.LIB_PATH)
+    res = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(nf.HEADER),
+                          str(src), "-L", libdir, "-lnf", f"-Wl,-rpath,{libdir}", "-o", str(exe)],
+                         capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, (run.returncode, run.stdout, run.stderr)
+    assert run.stdout.strip() in ("created", "no device")
