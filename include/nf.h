@@ -120,6 +120,20 @@ nf_status nf_get_params(nf_net* net, float* host_dst, int64_t n);
  * n floats.  Zero before the first step.  Waits for outstanding work. */
 nf_status nf_get_grads(nf_net* net, float* host_dst, int64_t n);
 
+/* Copy f'(z_layer), the activation derivative at the pre-activations of layer
+ * `layer` (1 .. L-1) that the most recent training step kept for
+ * back-propagation (section 3.2: z is stored for the backward pass), into
+ * host memory as [batch][d_layer] rows, batch = that step's batch.  For a relu
+ * layer the entries are its kink decisions, 1 where z > 0 and 0 elsewhere:
+ * a parity check takes them to resolve units that lie within rounding of the
+ * kink, where either side is a correct result.  Only steps that store f' in
+ * device memory keep it: NF_EINVAL after a step that held f' in registers
+ * (nets of at most 32 units per layer after the input with one shard, or at
+ * most 128 units in 2 to 4 layers), before any step, and once a larger batch
+ * has replaced the per-sample buffers; NF_ESHAPE if batch differs from the
+ * step's.  Waits for the net's outstanding work. */
+nf_status nf_get_fprime(nf_net* net, int32_t layer, float* host_dst, int64_t batch);
+
 /* Batched inference: the network output for every sample, storing nothing in
  * the net (the output function of section 3.2).
  * d_x: [batch][d_0] input, d_out: [batch][d_L] output; batch >= 1. */
@@ -180,6 +194,7 @@ nf_status nf_accuracy(nf_net* net, const float* d_x, const float* d_y, int64_t n
 nf_status nf_set_params_f64(nf_net* net, const double* host_src, int64_t n);
 nf_status nf_get_params_f64(nf_net* net, double* host_dst, int64_t n);
 nf_status nf_get_grads_f64(nf_net* net, double* host_dst, int64_t n);
+nf_status nf_get_fprime_f64(nf_net* net, int32_t layer, double* host_dst, int64_t batch);
 nf_status nf_forward_f64(nf_net* net, const double* d_x, int64_t batch, double* d_out,
                          void* stream);
 nf_status nf_train_batch_f64(nf_net* net, const double* d_x, const double* d_y, int64_t batch,

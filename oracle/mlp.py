@@ -240,55 +240,101 @@ def _kink_side(name: str, Z: np.ndarray, fp: np.ndarray, kink_tol: float) -> np.
     that rounds z may land on either side, and both results are correct."""
     if kink_tol <= 0.0 or name != "relu":
         return fp
-    near = np.abs(Z) <= kink_tol * np.sqrt(np.mean(Z * Z))
+    near = kink_band(Z, kink_tol)
     return np.where(near, 1.0 - fp, fp)
 
 
-def piece_gradient(theta, dims, acts, X, Y, kink_tol: float = 0.0) -> np.ndarray:
+def kink_band(Z: np.ndarray, kink_tol: float) -> np.ndarray:
+    """Mask of the units of one layer's pre-activations Z [B][d] that lie
+    within kink_tol * rms(Z) of the relu kink (see _kink_side)."""
+    Z = np.asarray(Z, dtype=np.float64)
+    return np.abs(Z) <= kink_tol * np.sqrt(np.mean(Z * Z))
+
+
+def piece_gradient(theta, dims, acts, X, Y, kink_tol: float = 0.0, sides=None) -> np.ndarray:
     """Tendencies summed over the samples of one piece of a batch: for each
     layer, sum over samples s of delta_s (outer) a_s, and sum of delta_s.
     The delta recurrences are the single-sample ones, applied to each row.
     kink_tol > 0 takes the other side of the relu kink for units within that
     relative distance of it (used to measure how much a result depends on
-    those undetermined decisions; 0 is the method itself)."""
+    those undetermined decisions); kink_tol = 0 is the method itself.
+    sides[l-1], where given (rows like X), is the relu derivative to use for
+    layer l in place of the method's own (see batch_gradient)."""
     acts = _check_acts(acts, dims)
     layers = unpack(theta, dims)
     L = len(layers)
+    sides = list(sides) if sides is not None else [None] * L
     Z, A = forward(theta, dims, acts, X)
     Yd = np.asarray(Y, dtype=np.float64)
+
+    def fprime(l):                      # f' of layer l (1-based)
+        if sides[l - 1] is not None:
+            return np.asarray(sides[l - 1], dtype=np.float64)
+        return _kink_side(acts[l - 1], Z[l], act_prime(acts[l - 1], Z[l]), kink_tol)
+
     parts: List[Tuple[np.ndarray, np.ndarray]] = [None] * L
-    D = (A[L] - Yd) * _kink_side(acts[L - 1], Z[L], act_prime(acts[L - 1], Z[L]), kink_tol)
+    D = (A[L] - Yd) * fprime(L)
     for l in range(L - 1, -1, -1):
         parts[l] = (D.T @ A[l], D.sum(axis=0))              # sum_s delta_s a_s^T, sum_s delta_s
         if l > 0:
             W = layers[l][0]
-            D = (D @ W) * _kink_side(acts[l - 1], Z[l], act_prime(acts[l - 1], Z[l]), kink_tol)
+            D = (D @ W) * fprime(l)
     return pack(parts)
 
 
-def batch_gradient(theta, dims, acts, X, Y, shards: int = 1, kink_tol: float = 0.0) -> np.ndarray:
+def kink_sides(theta, dims, acts, X, kink_tol: float, given) -> list:
+    """The relu derivative of every layer when the units within kink_tol *
+    rms(z of the layer over the batch) of the kink take the sides in given
+    (given[l-1]: rows like X, nonzero where the unit counts as above the
+    kink; None keeps the method's own decisions for that layer).  Units
+    outside that band keep the method's own decision 1[z > 0].  Entries are
+    None for layers whose activation is not relu."""
+    acts = _check_acts(acts, dims)
+    Z, _ = forward(theta, dims, acts, X)
+    out = []
+    for l, a in enumerate(acts):
+        if a != "relu":
+            out.append(None)
+            continue
+        own = Z[l + 1] > 0
+        if given is not None and given[l] is not None:
+            own = np.where(kink_band(Z[l + 1], kink_tol), np.asarray(given[l]) > 0, own)
+        out.append(own.astype(np.float64))
+    return out
+
+
+def batch_gradient(theta, dims, acts, X, Y, shards: int = 1, kink_tol: float = 0.0,
+                   kink_given=None) -> np.ndarray:
     """Tendencies summed over the whole mini-batch.  The batch is split into
     `shards` equal contiguous pieces whose sums are added in piece order, the
-    single-process picture of the collective sum of section 3.5."""
+    single-process picture of the collective sum of section 3.5.  With
+    kink_given, relu units within kink_tol * rms(z) of the kink (rms over the
+    whole batch) take the sides given for them (kink_sides); without it,
+    kink_tol > 0 takes the other side for them (piece_gradient)."""
     X = np.asarray(X)
     B = X.shape[0]
     if shards < 1 or B % shards != 0:
         raise ValueError("the batch must split evenly into the shards")
     per = B // shards
+    sides = kink_sides(theta, dims, acts, X, kink_tol, kink_given) if kink_given is not None else None
     total = None
     for k in range(shards):
-        gk = piece_gradient(theta, dims, acts, X[k * per:(k + 1) * per], Y[k * per:(k + 1) * per],
-                            kink_tol)
+        rows = slice(k * per, (k + 1) * per)
+        if sides is None:
+            gk = piece_gradient(theta, dims, acts, X[rows], Y[rows], kink_tol)
+        else:
+            gk = piece_gradient(theta, dims, acts, X[rows], Y[rows], 0.0,
+                                [None if sd is None else sd[rows] for sd in sides])
         total = gk if total is None else total + gk
     return total
 
 
 def train_batch(theta, dims, acts, X, Y, eta, shards: int = 1, precision="f32",
-                kink_tol: float = 0.0):
+                kink_tol: float = 0.0, kink_given=None):
     """One SGD step on a mini-batch: theta - (eta / B) * (summed tendencies).
     Returns (new theta, summed tendencies in fp64)."""
     B = np.asarray(X).shape[0]
-    g = batch_gradient(theta, dims, acts, X, Y, shards, kink_tol)
+    g = batch_gradient(theta, dims, acts, X, Y, shards, kink_tol, kink_given)
     new = np.asarray(theta, dtype=np.float64) - (eta / B) * g
     return _round(new, precision), g
 

@@ -14,6 +14,7 @@ a second one.  The Python binding imports torch before loading the library.
 
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import shutil
 import subprocess
@@ -56,12 +57,15 @@ def _run(cmd, verbose):
 def build(verbose: bool = False) -> str:
     objdir = os.path.join(ROOT, "_build")
     os.makedirs(objdir, exist_ok=True)
-    objs = []
-    for src in SOURCES:
-        obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
-        _run([hipcc(), *HIPCC_FLAGS, "-c", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-              os.path.join(CSRC, src), "-o", obj], verbose)
-        objs.append(obj)
+    objs = [os.path.join(objdir, os.path.splitext(src)[0] + ".o") for src in SOURCES]
+    cmds = [[hipcc(), *HIPCC_FLAGS, "-c", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+             os.path.join(CSRC, src), "-o", obj] for src, obj in zip(SOURCES, objs)]
+    # one compiler process per source, at most as many as the CPUs this
+    # process may use
+    workers = max(1, min(len(cmds), len(os.sched_getaffinity(0)), 8))
+    with concurrent.futures.ThreadPoolExecutor(workers) as pool:
+        for f in [pool.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     rocm_lib = os.path.join(os.path.dirname(os.path.dirname(os.path.realpath(hipcc()))), "lib")
     tmp = LIB + ".tmp"
     _run([hipcc(), "-shared", "-fPIC", *objs, "-o", tmp, f"-Wl,-rpath,{rocm_lib}"], verbose)

@@ -14,6 +14,7 @@
 
 #include "nf.h"
 #include "nf_internal.h"
+#include "nf_split.h"
 
 namespace {
 
@@ -96,6 +97,9 @@ struct nf_net {
   int64_t zero_off = 0;
   hipStream_t last = nullptr;
   bool used = false;
+  // samples whose f'(z_l), l < L, the last training step left in fbuf (0 when
+  // that step kept f' in registers, or the workspace has been replaced since)
+  int64_t stash_batch = 0;
   // per-kernel timing (nf_profile)
   struct Rec {
     const char* name;
@@ -136,6 +140,7 @@ void free_ws(nf_net* n) {
   if (n->ws) (void)hipFree(n->ws);
   n->ws = nullptr;
   n->ws_batch = 0;
+  n->stash_batch = 0;
   n->actv.assign(n->dims.size(), nullptr);
   n->fbuf.assign(n->dims.size(), nullptr);
   n->dbuf.assign(n->dims.size(), nullptr);
@@ -346,9 +351,10 @@ nf_status run_forward(nf_net* n, const T* x, const T* y, int64_t batch, T* out, 
     } else {
       // pieces start on whole 16-input stages, so a vector load never
       // reaches into the next piece and every piece start stays 16-byte
-      // aligned
-      const int sub_len = (int)round_up((p.K + nsplit - 1) / nsplit, 16);
-      nsplit = (p.K + sub_len - 1) / sub_len;
+      // aligned (nf_split.h)
+      const nf::KSplit ks = nf::k_split(p.K, nsplit);
+      const int sub_len = ks.sub_len;
+      nsplit = ks.nsplit;
       const int64_t ldp = round_up(p.N, 4);
       const int64_t pstride = round_up((int64_t)p.M * ldp, kAlign);
       st = ensure_partial(n, nsplit * pstride);
@@ -741,9 +747,10 @@ nf_status medium_forward_deltas(nf_net* n, const T* x, const T* y, int64_t batch
   int nsplit = 1;
   if (tiles < want && p.K >= 256)
     nsplit = (int)std::min<int64_t>({(want + tiles - 1) / tiles, p.K / 128, 16});
-  // pieces start on whole 16-input stages (see run_forward)
-  const int sub_len = (int)round_up((p.K + nsplit - 1) / nsplit, 16);
-  nsplit = (p.K + sub_len - 1) / sub_len;
+  // pieces start on whole 16-input stages (nf_split.h)
+  const nf::KSplit ks = nf::k_split(p.K, nsplit);
+  const int sub_len = ks.sub_len;
+  nsplit = ks.nsplit;
   const int64_t ldz = round_up(p.N, 4);
   const int64_t zstride = round_up((int64_t)p.M * ldz, kAlign);
   nf_status st = ensure_partial(n, nsplit * zstride);
@@ -802,6 +809,7 @@ nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double et
     st = run_forward<T>(n, x, y, batch, nullptr, true, s);
     if (st == NF_OK) st = run_backward_update<T>(n, x, batch, eta, shards, s);
   }
+  n->stash_batch = (!narrow && !medium_layout<T>(n, batch, &mp) && st == NF_OK) ? batch : 0;
   // the updated parameters are in the other buffer from here on (a failed
   // launch leaves the net in an undefined state, reported as NF_EDEVICE)
   if (st == NF_OK) n->cur ^= 1;
@@ -1008,6 +1016,32 @@ nf_status get_params(nf_net* net, T* host_dst, int64_t n, bool grads) {
     if (st != NF_OK) return st;
     if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
     return copy_params(net, grads ? net->grads : net->pbuf[net->cur], nullptr, host_dst, n);
+  });
+}
+
+// f'(z_layer) of the last training step's samples, [batch][d_layer] rows
+template <class T>
+nf_status get_fprime(nf_net* net, int32_t layer, T* host_dst, int64_t batch) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<T>(net);
+    if (st != NF_OK) return st;
+    if (!host_dst) return fail(NF_EINVAL, "host_dst is NULL");
+    const int L = num_layers(net);
+    if (layer < 1 || layer >= L) return fail(NF_EINVAL, "layer must be in 1 .. L-1");
+    if (net->stash_batch == 0)
+      return fail(NF_EINVAL, "the last training step kept f'(z) in registers (or none ran)");
+    if (batch != net->stash_batch)
+      return fail(NF_ESHAPE, "batch differs from the last training step's");
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    st = sync_net(net);
+    if (st != NF_OK) return st;
+    const LayerLayout& ly = net->layers[layer];
+    const size_t es = net->esz;
+    hipError_t e = hipMemcpy2D(host_dst, (size_t)ly.out * es, net->fbuf[layer], (size_t)ly.lda * es,
+                               (size_t)ly.out * es, (size_t)batch, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "f' copy");
+    return NF_OK;
   });
 }
 
@@ -1403,6 +1437,12 @@ nf_status nf_get_params_f64(nf_net* net, double* host_dst, int64_t n) {
 }
 nf_status nf_get_grads_f64(nf_net* net, double* host_dst, int64_t n) {
   return get_params<double>(net, host_dst, n, true);
+}
+nf_status nf_get_fprime(nf_net* net, int32_t layer, float* host_dst, int64_t batch) {
+  return get_fprime<float>(net, layer, host_dst, batch);
+}
+nf_status nf_get_fprime_f64(nf_net* net, int32_t layer, double* host_dst, int64_t batch) {
+  return get_fprime<double>(net, layer, host_dst, batch);
 }
 nf_status nf_forward_f64(nf_net* net, const double* d_x, int64_t batch, double* d_out,
                          void* stream) {

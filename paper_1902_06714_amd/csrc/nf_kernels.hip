@@ -18,6 +18,7 @@
 // reproducible from run to run.  No floating-point atomics are used.
 #include "nf_act.h"
 #include "nf_internal.h"
+#include "nf_split.h"
 
 namespace nf {
 
@@ -490,6 +491,18 @@ template <class T>
 hipError_t launch_gemm(int epi, int tile, bool a_kcontig, bool b_kcontig, bool a_vec, bool b_vec,
                        int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0 || nsplit <= 0) return hipErrorInvalidValue;
+  // The epilogues that work on pieces of the k range read an operand that is
+  // k-contiguous and loaded 16 bytes at a time only if every piece starts on
+  // a whole BK stage (nf_split.h): a piece start off that grid would make
+  // the last vector of the piece before it read into this piece and past the
+  // operand's rows.  (The tendency pieces split the batch, which is not the
+  // contiguous index of either of their operands, so any cut is safe there.)
+  if (epi == EPI_FWD_PIECE || epi == EPI_DW_SGD || epi == EPI_DW_PARTIAL) {
+    if (p.nsub <= 0 || nsplit % p.nsub != 0) return hipErrorInvalidValue;
+    if (((a_kcontig && a_vec) || (b_kcontig && b_vec)) &&
+        !k_pieces_aligned(nsplit / p.nsub, p.shard_len, p.nsub, p.sub_len))
+      return hipErrorInvalidValue;
+  }
   // The 128 x 128 tile runs 8 waves of 64 x 32 (two per SIMD, so one
   // wave's LDS reads and barrier waits overlap the other's matrix work).
   constexpr int WN128 = 32;
@@ -604,8 +617,11 @@ template <class T>
 hipError_t launch_dw_partial_group(int tile, bool b_vec, const GemmGroupT<T>& g,
                                    const int* nsplit, hipStream_t s) {
   if (g.n < 1 || g.n > GEMM_GROUP_MAX) return hipErrorInvalidValue;
+  // the group kernels read both operands mn-contiguous (the batch, which the
+  // pieces split, is their row index), so no piece alignment is needed
   for (int q = 0; q < g.n; ++q) {
     if (g.p[q].M <= 0 || g.p[q].N <= 0 || nsplit[q] <= 0) return hipErrorInvalidValue;
+    if (g.p[q].nsub <= 0 || nsplit[q] % g.p[q].nsub != 0) return hipErrorInvalidValue;
     const int64_t ld = g.p[q].lda > g.p[q].ldb ? g.p[q].lda : g.p[q].ldb;
     if ((int64_t)128 * ld * (int64_t)sizeof(T) >= (int64_t)TILE_OOB) return hipErrorInvalidValue;
   }

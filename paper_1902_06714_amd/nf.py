@@ -81,6 +81,9 @@ _sig = {
     "nf_set_params_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
     "nf_get_params_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
     "nf_get_grads_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64]),
+    "nf_get_fprime": (ctypes.c_int, [_net_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64]),
+    "nf_get_fprime_f64": (ctypes.c_int, [_net_p, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.c_int64]),
     "nf_forward_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                       ctypes.c_void_p]),
     "nf_train_batch_f64": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -201,6 +204,13 @@ def nf_get_grads(net) -> np.ndarray:
     return out
 
 
+def nf_get_fprime(net, layer: int, batch: int, width: int) -> np.ndarray:
+    """f'(z_layer) [batch][width] of the last training step (width = d_layer)."""
+    out = np.empty((batch, width), dtype=np.float32)
+    _check(_lib.nf_get_fprime(net, layer, out.ctypes.data, batch), "nf_get_fprime")
+    return out
+
+
 def nf_forward(net, x, out, stream=None) -> None:
     """x: [batch][d_0] GPU tensor, out: [batch][d_L] GPU tensor."""
     _check(_lib.nf_forward(net, _dev_ptr(x, "x"), x.shape[0], _dev_ptr(out, "out"),
@@ -255,6 +265,12 @@ def nf_get_params_f64(net) -> np.ndarray:
 def nf_get_grads_f64(net) -> np.ndarray:
     out = np.empty(nf_param_count(net), dtype=np.float64)
     _check(_lib.nf_get_grads_f64(net, out.ctypes.data, out.size), "nf_get_grads_f64")
+    return out
+
+
+def nf_get_fprime_f64(net, layer: int, batch: int, width: int) -> np.ndarray:
+    out = np.empty((batch, width), dtype=np.float64)
+    _check(_lib.nf_get_fprime_f64(net, layer, out.ctypes.data, batch), "nf_get_fprime_f64")
     return out
 
 

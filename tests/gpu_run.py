@@ -63,13 +63,13 @@ class GpuNet:
 
 def trajectory(dims, acts, theta0, X, Y, batch, eta, shards, steps,
                each: Optional[Callable] = None):
-    """Train on consecutive batches on the GPU, calling each(t, params, grads)
-    after every step.  Returns the final parameters."""
+    """Train on consecutive batches on the GPU, calling each(t, params, grads,
+    net) after every step.  Returns the final parameters."""
     xd, yd = to_dev(X[:batch * steps]), to_dev(Y[:batch * steps])
     with GpuNet(dims, acts, theta0) as net:
         for t in range(steps):
             net.train_batch(xd[t * batch:(t + 1) * batch], yd[t * batch:(t + 1) * batch], eta,
                             shards)
             if each is not None:
-                each(t, net.params(), net.grads())
+                each(t, net.params(), net.grads(), net)
         return net.params()

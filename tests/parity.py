@@ -5,33 +5,51 @@ Gates (fp32 GPU against the fp64 reference, same seeded inputs):
 
 * parameters, every tensor t, every element i:
       |gpu_i - ref_i| <= 1e-4 * max(|ref_i|, rms(ref_t))
-  i.e. a relative error of 1e-4, with the tensor's rms as the floor of the
-  denominator so that weights that happen to sit near zero are judged on the
-  tensor's scale rather than on their own.
-* tendencies (the batch-summed gradient of the last step), networks without
-  relu or step units: the same elementwise rule with tolerance 1e-4.  An fp32
-  emulation of the step on the CPU stays below 4e-6 on these networks.
-* tendencies, networks with relu units: a unit whose pre-activation lies
-  within fp32 rounding of zero may take either side of the kink, which moves
-  one sample's whole contribution in that gradient row (~1 % of the row for a
-  4096-sample batch) and a ~1/sqrt(width) share of it in every lower layer.
-  Both outcomes are correct results, so these networks are gated normwise:
-      ||gpu_t - ref_t||_F <= 5e-3 * ||ref_t||_F
-  (the fp32 emulation stays below 6.2e-4 on the 784-1024^3-10 and
-  4096^4-10 workloads), while the parameters keep the elementwise gate.
+  a relative error of 1e-4 with the tensor's rms as the floor of the
+  denominator.  The error of a weight that lands near zero after a step is
+  the fp32 error of its update (eta/B) * G, not a fraction of its own value,
+  so a floor is needed; with the smaller floor 1e-3 * rms(ref_t) an
+  independent fp32 computation of the same step (numpy float32 products on
+  the CPU) already reaches 1.0-1.7e-4 on the first layer of the 784-30-10
+  and 784-100-100-10 workloads.  Every comparison also reports the error
+  under that smaller floor and the unfloored largest relative error with the
+  element that holds it (tensor_report).
+* update, every tensor, in the step-along comparisons (both sides start from
+  the same theta_t): with d_gpu = theta_gpu - theta_t and the exact
+  d_ref = -(eta/B) G_ref,
+      max_i (|d_gpu,i - d_ref,i| - ulp(theta_gpu,i) / 2) <= 1e-3 * max_i |d_ref,i|
+  The half ulp is the rounding of the stored fp32 result, which no fp32
+  implementation can avoid; where the step is small against the parameters
+  (the 4096^4-10 workload moves b_1 by ~1e-4 of its size) it is of the same
+  order as the gate.  This check is what sees an update that was not applied:
+  the parameter gate alone passes a parameter that did not move when the
+  step is below 1e-4 of the tensor's rms.
+* tendencies (the batch-summed gradient of the last step): the parameter
+  rule elementwise with tolerance 1e-4.  For networks with relu units the
+  tendencies depend on which side of the kink each unit falls, and a unit
+  whose pre-activation lies within rounding of zero may fall on either side
+  in any fp32 computation, both results being correct.  Such comparisons
+  take the GPU's own decisions for the units within KINK_BAND * rms(z of the
+  layer) of the kink (nf_get_fprime), require the GPU to decide every other
+  unit as the reference does, and then compare elementwise: the result is
+  unique once those decisions are fixed.
 * network outputs (inference): the parameter rule with tolerance 1e-4.
 """
 
 from __future__ import annotations
 
-from typing import List, Sequence, Tuple
+import json
+import sys
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
 PARAM_TOL = 1e-4
 GRAD_TOL = 1e-4
-GRAD_FRO_TOL_RELU = 5e-3
+UPDATE_TOL = 1e-3
 OUT_TOL = 1e-4
+SMALL_FLOOR = 1e-3      # the smaller floor, reported beside the gated one
+KINK_BAND = 1e-4        # relu units within this * rms(z) of the kink take the GPU's side
 
 
 def tensor_slices(dims: Sequence[int]) -> List[Tuple[str, slice]]:
@@ -45,59 +63,165 @@ def tensor_slices(dims: Sequence[int]) -> List[Tuple[str, slice]]:
     return out
 
 
-def floored_rel(got, ref) -> Tuple[float, int]:
+def floored_rel(got, ref, floor: float = 1.0) -> Tuple[float, int]:
+    """Largest |got - ref| / max(|ref|, floor * rms(ref)) and where it is."""
     got = np.asarray(got, dtype=np.float64).ravel()
     ref = np.asarray(ref, dtype=np.float64).ravel()
     if ref.size == 0:
         return 0.0, -1
-    rms = float(np.sqrt(np.mean(ref * ref)))
-    den = np.maximum(np.abs(ref), rms)
-    den[den == 0] = 1.0
-    err = np.abs(got - ref) / den
     if not np.all(np.isfinite(got)):
         return float("inf"), int(np.argmax(~np.isfinite(got)))
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    den = np.maximum(np.abs(ref), floor * rms)
+    den[den == 0] = 1.0
+    err = np.abs(got - ref) / den
     i = int(np.argmax(err))
     return float(err[i]), i
 
 
-def check_params(got, ref, dims, tol=PARAM_TOL, what="params") -> List[str]:
+def tensor_report(got, ref) -> Dict:
+    """The gated error (rms floor), the error under the 1e-3 * rms floor, and
+    the unfloored largest relative error with its element and values."""
+    g = np.asarray(got, dtype=np.float64).ravel()
+    r = np.asarray(ref, dtype=np.float64).ravel()
+    e, i = floored_rel(g, r, 1.0)
+    e3, i3 = floored_rel(g, r, SMALL_FLOOR)
+    nz = r != 0
+    if np.any(nz) and np.all(np.isfinite(g)):
+        rel = np.full(r.shape, 0.0)
+        rel[nz] = np.abs(g[nz] - r[nz]) / np.abs(r[nz])
+        j = int(np.argmax(rel))
+        raw = {"rel": float(rel[j]), "at": j, "gpu": float(g[j]), "ref": float(r[j])}
+    else:
+        raw = None
+    return {"gated": e, "at": i, "floor_1e-3": e3, "floor_1e-3_at": i3, "unfloored": raw}
+
+
+def check_params(got, ref, dims, tol=PARAM_TOL, what="params", report=None) -> List[str]:
+    """Elementwise gate per tensor; report (a dict) collects tensor_report."""
     fails = []
     for name, sl in tensor_slices(dims):
-        e, i = floored_rel(got[sl], ref[sl])
-        if not e <= tol:
-            fails.append(f"{what} {name}: floored relative error {e:.3e} > {tol:g} "
+        rep = tensor_report(got[sl], ref[sl])
+        if report is not None:
+            report[name] = rep
+        if not rep["gated"] <= tol:
+            i = rep["at"]
+            fails.append(f"{what} {name}: floored relative error {rep['gated']:.3e} > {tol:g} "
                          f"at {i} (gpu {got[sl][i]!r}, ref {ref[sl][i]!r})")
     return fails
 
 
-def check_grads(got, ref, dims, acts, tol=GRAD_TOL, fro_tol=GRAD_FRO_TOL_RELU) -> List[str]:
-    kinked = any(a in ("relu", "step") for a in acts)
+def check_grads(got, ref, dims, tol=GRAD_TOL, report=None) -> List[str]:
+    """Tendencies, elementwise.  Relu networks must be compared against a
+    reference that took the GPU's decisions at the kink (see kink_sides)."""
+    return check_params(got, ref, dims, tol, "grads", report)
+
+
+def check_update(got, theta_t, ref_grad, scale: float, dims, tol=UPDATE_TOL,
+                 report=None) -> List[str]:
+    """The applied step against the exact step -(eta/B) G_ref from the same
+    theta_t, allowing the half ulp of the stored fp32 result (module doc)."""
     fails = []
     for name, sl in tensor_slices(dims):
-        g = np.asarray(got[sl], dtype=np.float64)
-        r = np.asarray(ref[sl], dtype=np.float64)
-        if not np.all(np.isfinite(g)):
-            fails.append(f"grads {name}: non-finite values")
+        p = np.asarray(got[sl], dtype=np.float32)
+        d_gpu = p.astype(np.float64) - np.asarray(theta_t[sl], dtype=np.float32).astype(np.float64)
+        d_ref = -scale * np.asarray(ref_grad[sl], dtype=np.float64)
+        dinf = float(np.max(np.abs(d_ref))) if d_ref.size else 0.0
+        if not np.all(np.isfinite(d_gpu)):
+            fails.append(f"update {name}: non-finite parameters")
             continue
-        if kinked:
-            nr = np.linalg.norm(r)
-            e = np.linalg.norm(g - r) / nr if nr > 0 else np.linalg.norm(g)
-            if not e <= fro_tol:
-                fails.append(f"grads {name}: Frobenius relative error {e:.3e} > {fro_tol:g}")
-        else:
-            e, i = floored_rel(g, r)
-            if not e <= tol:
-                fails.append(f"grads {name}: floored relative error {e:.3e} > {tol:g} at {i} "
-                             f"(gpu {g[i]!r}, ref {r[i]!r})")
+        half_ulp = np.spacing(np.abs(p)).astype(np.float64) / 2
+        diff = np.abs(d_gpu - d_ref)
+        if dinf == 0.0:
+            if np.any(diff > half_ulp):
+                fails.append(f"update {name}: parameters moved where the step is zero")
+            if report is not None:
+                report[name] = {"raw": 0.0, "gated": 0.0, "storage": 0.0}
+            continue
+        raw = float(np.max(diff)) / dinf
+        adj = float(np.max(np.maximum(diff - half_ulp, 0.0))) / dinf
+        if report is not None:
+            report[name] = {"raw": raw, "gated": adj, "storage": float(np.max(half_ulp)) / dinf}
+        if not adj <= tol:
+            i = int(np.argmax(np.maximum(diff - half_ulp, 0.0)))
+            fails.append(f"update {name}: {adj:.3e} of the largest step > {tol:g} at {i} "
+                         f"(gpu step {d_gpu[i]!r}, reference step {d_ref[i]!r})")
     return fails
+
+
+def full_acts(dims, acts) -> List[str]:
+    return list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+
+
+def has_kinks(acts) -> bool:
+    return any(a in ("relu", "step") for a in acts)
+
+
+def gpu_kink_sides(nf, h, dims, acts, batch) -> Optional[list]:
+    """The GPU's relu decisions of the last training step, per layer (None for
+    other layers and for the output layer, whose f' is not kept), or None when
+    the step kept f' in registers."""
+    acts = full_acts(dims, acts)
+    L = len(dims) - 1
+    out = []
+    for l in range(1, L + 1):
+        if acts[l - 1] != "relu" or l == L:
+            out.append(None)
+            continue
+        try:
+            out.append(nf.nf_get_fprime(h, l, batch, dims[l]))
+        except nf.NfError as e:
+            if e.status != nf.NF_EINVAL:
+                raise
+            return None
+    return out
+
+
+def check_kink_sides(sides, theta, dims, acts, X, band=KINK_BAND, stats=None) -> List[str]:
+    """The GPU's relu decisions must equal the reference's own for every unit
+    outside the band; stats collects, per layer, the units in the band and how
+    many of them the GPU put on the other side from the reference."""
+    from oracle import mlp
+    acts = full_acts(dims, acts)
+    Z, _ = mlp.forward(theta, dims, acts, X)
+    fails = []
+    for l, sd in enumerate(sides):
+        if sd is None:
+            continue
+        z = Z[l + 1]
+        own = z > 0
+        gpu = np.asarray(sd) > 0
+        near = mlp.kink_band(z, band)
+        off = (gpu != own) & ~near
+        if stats is not None:
+            stats[f"z{l + 1}"] = {"in_band": int(near.sum()),
+                                  "other_side_in_band": int(((gpu != own) & near).sum()),
+                                  "other_side_outside": int(off.sum())}
+        if off.any():
+            s, j = np.argwhere(off)[0]
+            rms = float(np.sqrt(np.mean(z * z)))
+            fails.append(f"layer {l + 1}: {int(off.sum())} relu decisions differ outside the band, "
+                         f"e.g. sample {s} unit {j} at z = {z[s, j]:.3e} ({abs(z[s, j]) / rms:.2e} rms)")
+    return fails
+
+
+def emit(tag: str, record: Dict) -> None:
+    """One machine-readable line of measured errors on stderr."""
+    print(f"[parity-json] {tag} " + json.dumps(record, default=float), file=sys.stderr, flush=True)
+
+
+def worst(report: Dict, key: str = "gated") -> float:
+    vals = [v[key] for v in report.values() if isinstance(v, dict) and key in v]
+    return max(vals) if vals else 0.0
 
 
 def relu_clear(theta, dims, acts, X, rel=1e-3) -> bool:
     """True when no relu / step pre-activation of the reference forward pass on
     X lies within rel * (that layer's rms |z|) of zero, so that rounding cannot
-    flip a unit across the kink and gradients can be compared elementwise."""
+    flip a unit across the kink and gradients can be compared elementwise
+    without the GPU's decisions (used where the GPU keeps f' in registers)."""
     from oracle import mlp
-    acts = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+    acts = full_acts(dims, acts)
     Z, _ = mlp.forward(theta, dims, acts, X)
     for l, a in enumerate(acts):
         if a in ("relu", "step"):

@@ -303,6 +303,30 @@ def check_kink_side(m) -> List[str]:
         fails.append(f"tendencies at the kink {g0}")
     if not np.array_equal(g1, [2.0, 2.0, 0.0, 1.0]):
         fails.append(f"tendencies on the other side of the kink {g1}")
+    # sides given for the units in the band: "above" gives the other side,
+    # "below" the method's own; a given side outside the band is ignored
+    # (b1 = -0.5: z1 = 0.5, a1 = 0.5, z2 = 2, delta2 = 2, delta1 = 4)
+    up, down = [np.array([[1.0]]), None], [np.array([[0.0]]), None]
+    g_up = m.batch_gradient(theta, (1, 1, 1), ["relu"], X, Y, kink_tol=1e-5, kink_given=up)
+    g_dn = m.batch_gradient(theta, (1, 1, 1), ["relu"], X, Y, kink_tol=1e-5, kink_given=down)
+    if not np.array_equal(g_up, [2.0, 2.0, 0.0, 1.0]):
+        fails.append(f"given side above the kink {g_up}")
+    if not np.array_equal(g_dn, [0.0, 0.0, 0.0, 1.0]):
+        fails.append(f"given side below the kink {g_dn}")
+    clear = np.array([1.0, -0.5, 2.0, 1.0])
+    g_cl = m.batch_gradient(clear, (1, 1, 1), ["relu"], X, Y, kink_tol=1e-5, kink_given=down)
+    if not np.array_equal(g_cl, [4.0, 4.0, 1.0, 2.0]):
+        fails.append(f"a given side outside the band changed the tendencies {g_cl}")
+    # two samples, one at the kink and one clear of it, in one or two shards:
+    # the band is taken over the whole batch and each shard gets its rows
+    X2, Y2 = np.array([[1.0], [1.5]]), np.array([[0.0], [0.0]])
+    given2 = [np.array([[1.0], [0.0]]), None]
+    g_1 = m.batch_gradient(theta, (1, 1, 1), ["relu"], X2, Y2, 1, kink_tol=1e-5, kink_given=given2)
+    g_2 = m.batch_gradient(theta, (1, 1, 1), ["relu"], X2, Y2, 2, kink_tol=1e-5, kink_given=given2)
+    # sample 2: z1 = 0.5, a1 = 0.5, z2 = 2, delta2 = 2, delta1 = 4, x = 1.5
+    want2 = np.array([2.0 + 6.0, 2.0 + 4.0, 0.0 + 1.0, 1.0 + 2.0])
+    if not (np.array_equal(g_1, want2) and np.array_equal(g_2, want2)):
+        fails.append(f"given sides over shards {g_1} {g_2}, expected {want2}")
     return fails
 
 

@@ -1,21 +1,24 @@
 """GPU library against the CPU reference on the five benchmark workloads at
 their full sizes, in the launch configuration bench.py times.
 
-Two comparisons per workload:
+Two comparisons per workload (the gates are those of tests/parity.py):
 
 * step along the reference: before every step the GPU net is loaded with the
-  reference's parameters for that step (data flows from the reference to the
-  GPU only), takes one step, and its parameters and tendencies are compared
-  with the reference's next step.  Every step of the schedule is gated at the
-  fixed tolerances of tests/parity.py.
+  reference's parameters theta_t for that step (data flows from the
+  reference to the GPU only) and takes one step.  Its parameters, its
+  tendencies and the step it applied are compared with the reference's step
+  from the same theta_t.
 * free-running trajectory: the GPU trains on its own from the seeded initial
-  parameters and is compared after every step.  Where the schedule is chaotic
-  the result after t steps is not determined to fp32 precision: for networks
-  with relu units the reference is run a second time with the other side of
-  the kink taken by every unit within 1e-5 * rms(z) of it (units an fp32
-  computation may legitimately put on either side), and the gate after step t
-  is max(fixed tolerance, 2 * the spread between those two reference runs).
-  Networks without kinks keep the fixed tolerance throughout.
+  parameters, the reference likewise, and the parameters are compared after
+  every step (the tendencies too for networks without kinks).
+
+For networks with relu units the reference step takes the GPU's decisions
+for the units within KINK_BAND * rms(z) of the kink, where the method leaves
+the side to rounding (nf_get_fprime), and every other unit must be decided
+as the reference decides it.  The free-running reference takes the free
+GPU run's decisions step by step in the same way; the distance to the plain
+reference (which decides every unit itself) and the spread of the plain
+reference under the other choice for the band units are reported beside it.
 """
 
 import sys
@@ -31,23 +34,6 @@ from .gpu_run import GpuNet, note, to_dev
 
 pytestmark = pytest.mark.gpu
 
-KINK_TOL = 1e-5
-
-
-def _tensor_spread(a, b, dims):
-    out = {}
-    for name, sl in parity.tensor_slices(dims):
-        out[name] = parity.floored_rel(b[sl], a[sl])[0]
-    return out
-
-
-def _tensor_fro(a, b, dims):
-    out = {}
-    for name, sl in parity.tensor_slices(dims):
-        n = np.linalg.norm(a[sl])
-        out[name] = float(np.linalg.norm(np.asarray(b[sl], np.float64) - a[sl]) / n) if n > 0 else 0.0
-    return out
-
 
 def _reference(w, X, Y, theta, steps, shards, kink_tol=0.0):
     thetas, grads = [theta], []
@@ -60,20 +46,39 @@ def _reference(w, X, Y, theta, steps, shards, kink_tol=0.0):
     return thetas, grads
 
 
+def _kink_step(w, theta, X, Y, shards, sides):
+    if sides is None:       # already a failure; the plain step keeps the rest meaningful
+        return mlp.train_batch(theta, w.dims, list(w.acts), X, Y, w.eta, shards)
+    return mlp.train_batch(theta, w.dims, list(w.acts), X, Y, w.eta, shards,
+                           kink_tol=parity.KINK_BAND, kink_given=sides)
+
+
+def _sides(net, w, theta, X, fails, what):
+    sides = parity.gpu_kink_sides(net.nf, net.h, w.dims, w.acts, X.shape[0])
+    if sides is None:
+        fails.append(f"{what}: the GPU step kept no relu decisions")
+        return None, {}
+    stats = {}
+    fails += [f"{what}: {m}" for m in parity.check_kink_sides(sides, theta, w.dims, w.acts, X,
+                                                              stats=stats)]
+    return sides, stats
+
+
 def _run(name, steps=None, shards=None):
     w = W.WORKLOADS[name]
     steps = w.steps if steps is None else steps
     shards = w.shards if shards is None else shards
     acts = list(w.acts)
-    kinked = any(a in ("relu", "step") for a in acts)
+    kinked = "relu" in parity.full_acts(w.dims, acts)
+    scale = w.eta / w.batch
     X, Y = W.make_data(w, w.batch * steps)
     theta0 = W.make_params(w)
     ref_t, ref_g = _reference(w, X, Y, theta0, steps, shards)
-    if kinked:
-        alt_t, alt_g = _reference(w, X, Y, theta0, steps, shards, KINK_TOL)
     xd, yd = to_dev(X), to_dev(Y)
-    fails, worst = [], {"step_p": 0.0, "step_g": 0.0, "free_p": 0.0}
+    fails = []
+    worst = {"along_params": 0.0, "along_grads": 0.0, "along_update": 0.0, "free_params": 0.0}
     note(f"{name}: {w.dims} batch={w.batch} shards={shards} steps={steps}")
+    free_plain, free_dec = [], []
     with GpuNet(w.dims, acts, theta0) as net:
         # step along the reference
         for t in range(steps):
@@ -81,46 +86,80 @@ def _run(name, steps=None, shards=None):
             net.nf.nf_set_params(net.h, ref_t[t])
             net.train_batch(xd[sl], yd[sl], w.eta, shards)
             p, g = net.params(), net.grads()
-            fails += [f"step-along {t}: {m}" for m in parity.check_params(p, ref_t[t + 1], w.dims)]
-            fails += [f"step-along {t}: {m}" for m in parity.check_grads(g, ref_g[t], w.dims, acts)]
-            worst["step_p"] = max(worst["step_p"], max(_tensor_spread(ref_t[t + 1], p, w.dims).values()))
+            kstats = {}
+            if kinked:
+                sides, kstats = _sides(net, w, ref_t[t], X[sl], fails, f"step-along {t}")
+                new, G = _kink_step(w, ref_t[t], X[sl], Y[sl], shards, sides)
+            else:
+                new, G = ref_t[t + 1], ref_g[t]
+            rp, rg, ru = {}, {}, {}
+            fails += [f"step-along {t}: {m}" for m in parity.check_params(p, new, w.dims, report=rp)]
+            fails += [f"step-along {t}: {m}" for m in parity.check_grads(g, G, w.dims, report=rg)]
+            fails += [f"step-along {t}: {m}" for m in parity.check_update(p, ref_t[t], G, scale,
+                                                                          w.dims, report=ru)]
+            parity.emit(f"{name} along {t}", {"params": rp, "grads": rg, "update": ru,
+                                              "kinks": kstats})
+            worst["along_params"] = max(worst["along_params"], parity.worst(rp))
+            worst["along_grads"] = max(worst["along_grads"], parity.worst(rg))
+            worst["along_update"] = max(worst["along_update"], parity.worst(ru))
         # free-running trajectory
         net.nf.nf_set_params(net.h, theta0)
+        th_o = theta0
         for t in range(steps):
             sl = slice(t * w.batch, (t + 1) * w.batch)
             net.train_batch(xd[sl], yd[sl], w.eta, shards)
             p, g = net.params(), net.grads()
-            gp = _tensor_spread(ref_t[t + 1], p, w.dims)
-            gg = _tensor_fro(ref_g[t], g, w.dims)
+            kstats = {}
             if kinked:
-                sp = _tensor_spread(ref_t[t + 1], alt_t[t + 1], w.dims)
-                sg = _tensor_fro(ref_g[t], alt_g[t], w.dims)
-            for tn, _ in parity.tensor_slices(w.dims):
-                tol_p = parity.PARAM_TOL
-                tol_g = parity.GRAD_FRO_TOL_RELU if kinked else None
-                if kinked:
-                    tol_p = max(tol_p, 2 * sp[tn])
-                    tol_g = max(tol_g, 2 * sg[tn])
-                if not gp[tn] <= tol_p:
-                    fails.append(f"free {t}: params {tn} {gp[tn]:.3e} > {tol_p:.3e}")
-                if tol_g is not None and not gg[tn] <= tol_g:
-                    fails.append(f"free {t}: grads {tn} Frobenius {gg[tn]:.3e} > {tol_g:.3e}")
+                sides, kstats = _sides(net, w, th_o, X[sl], fails, f"free {t}")
+                th_new, G_o = _kink_step(w, th_o, X[sl], Y[sl], shards, sides)
+            else:
+                th_new, G_o = ref_t[t + 1], ref_g[t]
+            rp, rg = {}, {}
+            fails += [f"free {t}: {m}" for m in parity.check_params(p, th_new, w.dims, report=rp)]
+            gfails = parity.check_grads(g, G_o, w.dims, report=rg)
             if not kinked:
-                fails += [f"free {t}: {m}" for m in parity.check_grads(g, ref_g[t], w.dims, acts)]
-            worst["free_p"] = max(worst["free_p"], max(gp.values()))
-        final = net.params()
+                fails += [f"free {t}: {m}" for m in gfails]
+            rec = {"params": rp, "grads": rg, "kinks": kstats}
+            if kinked:
+                plain = {}
+                parity.check_params(p, ref_t[t + 1], w.dims, report=plain)
+                rec["params_vs_plain_reference"] = plain
+                free_plain.append(parity.worst(plain))
+            parity.emit(f"{name} free {t}", rec)
+            worst["free_params"] = max(worst["free_params"], parity.worst(rp))
+            free_dec.append(parity.worst(rp))
+            th_o = th_new
         if w.heldout:
             Xh, _ = W.make_data(w, heldout=True)
             note(f"{name}: inference on {Xh.shape[0]} held-out samples")
             net.nf.nf_set_params(net.h, ref_t[-1])
             out = net.forward(to_dev(Xh))
-            e, _ = parity.floored_rel(out, mlp.output(ref_t[-1], w.dims, acts, Xh))
-            if not e <= parity.OUT_TOL:
-                fails.append(f"inference: floored relative error {e:.3e}")
-    print(f"[parity] {name}: worst step-along param error {worst['step_p']:.2e}, "
-          f"worst free-running param error {worst['free_p']:.2e}", file=sys.stderr, flush=True)
+            ro = parity.tensor_report(out, mlp.output(ref_t[-1], w.dims, acts, Xh))
+            parity.emit(f"{name} inference", ro)
+            if not ro["gated"] <= parity.OUT_TOL:
+                fails.append(f"inference: floored relative error {ro['gated']:.3e}")
+    msg = (f"[parity] {name}: step-along worst params {worst['along_params']:.2e}, tendencies "
+           f"{worst['along_grads']:.2e}, update {worst['along_update']:.2e}; free-running worst "
+           f"params {worst['free_params']:.2e}")
+    if kinked and steps >= 10:
+        # the plain reference against itself with the other side taken for
+        # the band units: how far the undetermined decisions alone move it
+        alt_t, _ = _reference(w, X, Y, theta0, steps, shards, parity.KINK_BAND)
+        spread = []
+        for t in range(steps):
+            rep = {}
+            parity.check_params(alt_t[t + 1], ref_t[t + 1], w.dims, report=rep)
+            spread.append(parity.worst(rep))
+        parity.emit(f"{name} free-running after 10 steps",
+                    {"gpu_vs_reference_with_gpu_decisions": free_dec[9], "gpu_vs_plain_reference":
+                     free_plain[9], "plain_reference_spread": spread[9],
+                     "per_step_vs_plain": free_plain, "per_step_spread": spread})
+        msg += (f"; after 10 steps: {free_dec[9]:.2e} (gated), vs the plain reference "
+                f"{free_plain[9]:.2e}, the plain reference's own spread {spread[9]:.2e}")
+    print(msg, file=sys.stderr, flush=True)
     assert not fails, "\n".join(fails[:30])
-    return w, X, Y, theta0, final
+    return w, X, Y, theta0
 
 
 def test_c1_784_30_10_batch100():
@@ -128,19 +167,23 @@ def test_c1_784_30_10_batch100():
 
 
 def test_c2_784_30_10_epoch_and_inference():
-    w, X, Y, theta, final = _run("c2")
+    w, X, Y, theta = _run("c2")
     # the whole epoch in one call gives the same bits as step-by-step calls
     note("c2: nf_train_epoch")
-    with GpuNet(w.dims, list(w.acts), theta) as net:
-        net.train_epoch(to_dev(X), to_dev(Y), w.batch, w.eta, w.shards)
-        assert np.array_equal(net.params(), final)
+    with GpuNet(w.dims, list(w.acts), theta) as a, GpuNet(w.dims, list(w.acts), theta) as b:
+        xd, yd = to_dev(X), to_dev(Y)
+        a.train_epoch(xd, yd, w.batch, w.eta, w.shards)
+        for t in range(w.steps):
+            b.train_batch(xd[t * w.batch:(t + 1) * w.batch], yd[t * w.batch:(t + 1) * w.batch],
+                          w.eta, w.shards)
+        assert np.array_equal(a.params(), b.params())
 
 
 def test_c3_784_100_100_10_sixteen_shards():
     _run("c3")
 
 
-@pytest.mark.timeout(600)
+@pytest.mark.timeout(900)
 def test_c4_784_1024x3_10():
     _run("c4")
 

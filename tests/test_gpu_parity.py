@@ -28,15 +28,30 @@ def _problem(dims, seed, n, init_scale=None, x_lo=0.0, x_hi=1.0):
 
 
 def _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, steps):
-    acts_full = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+    """The GPU's free-running trajectory against the reference's, step by step.
+    For networks with relu units the reference takes the GPU's decisions for
+    the units within the kink band (tests/parity.py); where the GPU keeps no
+    decisions (per-sample kernels), the seed must leave every unit clear of
+    the kink."""
+    acts_full = parity.full_acts(dims, acts)
+    kinked = "relu" in acts_full
     ref = [theta]
     fails = []
 
-    def each(t, p, g):
+    def each(t, p, g, net):
         sl = slice(t * batch, (t + 1) * batch)
-        new, G = mlp.train_batch(ref[0], dims, acts_full, X[sl], Y[sl], eta, shards)
+        sides = parity.gpu_kink_sides(net.nf, net.h, dims, acts, batch) if kinked else None
+        if sides is not None:
+            fails.extend(f"step {t}: {m}"
+                         for m in parity.check_kink_sides(sides, ref[0], dims, acts, X[sl]))
+            new, G = mlp.train_batch(ref[0], dims, acts_full, X[sl], Y[sl], eta, shards,
+                                     kink_tol=parity.KINK_BAND, kink_given=sides)
+        else:
+            if kinked and not parity.relu_clear(ref[0], dims, acts, X[sl], rel=parity.KINK_BAND):
+                fails.append(f"step {t}: relu units near the kink and no GPU decisions")
+            new, G = mlp.train_batch(ref[0], dims, acts_full, X[sl], Y[sl], eta, shards)
         fails.extend(f"step {t}: {m}" for m in parity.check_params(p, new, dims))
-        fails.extend(f"step {t}: {m}" for m in parity.check_grads(g, G, dims, acts_full))
+        fails.extend(f"step {t}: {m}" for m in parity.check_grads(g, G, dims))
         ref[0] = new
 
     note(f"trajectory dims={dims} acts={acts} batch={batch} shards={shards} steps={steps}")
@@ -279,6 +294,68 @@ def test_activation_ulp(act, d0):
     err = np.abs(out - ref) / ulp
     i = int(np.argmax(err))
     assert err[i] <= 4.0, (act, float(err[i]), float(z[i]))
+
+
+# pre-activations of the derivative test: saturated (the survey's +-8, +-15,
+# +-30), moderate, and the kink
+SAT_Z = np.array([-30, -15, -8, -2, -0.3, 0.0, 0.3, 2, 8, 15, 30], np.float64)
+# the kernel families, by the shape and sharding that selects them: the narrow
+# per-sample kernels (<= 32 units, input width % 4 == 0, one shard), the medium
+# per-sample kernel (<= 128 units in 2 to 4 layers; two shards keep the narrow
+# path out) and the contraction epilogues (a layer over 128 units)
+FAMILIES = {"narrow": (len(SAT_Z), 1, 1), "medium": (len(SAT_Z), 2, 2),
+            "general": (160, 1, 1)}
+
+
+def _fprime_case(act, family, hidden):
+    """A two-layer network whose pre-activations z of the tested layer are
+    exactly SAT_Z (the rest of a wide layer at z = 0.25), with x = e_1.
+    hidden: layer 1 holds z (z_1 = W_1 x, W_2 = 0.05, sigmoid output, y = 0),
+    so the bias tendency of layer 1 is 0.05 delta_2 f'(z_1) per sample;
+    otherwise layer 2 holds z (W_2 = 0, b_2 = z) and the target is
+    fp32(f(z)) + 1, so the bias tendency of layer 2 is (f(z) - y) f'(z) with
+    f(z) - y close to -1."""
+    n, shards, batch = FAMILIES[family]
+    z = np.full(n, 0.25)
+    z[:len(SAT_Z)] = SAT_Z
+    d0 = 4
+    if hidden:
+        dims, acts = (d0, n, 1), (act, "sigmoid")
+        W1 = np.zeros((n, d0))
+        W1[:, 0] = z
+        parts = [W1.ravel(), np.zeros(n), np.full(n, 0.05), np.zeros(1)]
+        Y = np.zeros((batch, 1))
+    else:
+        dims, acts = (d0, 1, n), ("sigmoid", act)
+        parts = [np.zeros(d0), np.zeros(1), np.zeros(n), z]
+        Y = np.tile(np.asarray(mlp.act(act, z) + 1.0, np.float32), (batch, 1))
+    theta = np.concatenate(parts).astype(np.float32)
+    X = np.zeros((batch, d0), np.float32)
+    X[:, 0] = 1.0
+    return dims, acts, theta, X, Y.astype(np.float32), shards
+
+
+@pytest.mark.parametrize("family", sorted(FAMILIES))
+@pytest.mark.parametrize("act", ["sigmoid", "tanh", "gaussian", "relu"])
+@pytest.mark.parametrize("hidden", [True, False], ids=["hidden", "output"])
+def test_derivative_in_saturation(act, family, hidden):
+    """f'(z) of every kernel family at saturated pre-activations, through the
+    bias tendency of the layer that holds them, against the fp64 reference:
+    relative error at most 2e-6 per element (about 16 fp32 ulp; a derivative
+    formed as s (1 - s) from an fp32 sigmoid s is wrong by orders of
+    magnitude at z = 15), or an absolute 1e-37 where the fp64 value is below
+    fp32's normal range (the Gaussian past |z| = 9)."""
+    dims, acts, theta, X, Y, shards = _fprime_case(act, family, hidden)
+    new, G = mlp.train_batch(theta, dims, list(acts), X, Y, 0.0, shards)
+    note(f"f' in saturation act={act} family={family} hidden={hidden}")
+    with GpuNet(dims, acts, theta) as net:
+        net.train_batch(to_dev(X), to_dev(Y), 0.0, shards)
+        g = net.grads().astype(np.float64)
+    sl = dict(parity.tensor_slices(dims))["b1" if hidden else "b2"]
+    got, ref = g[sl][:len(SAT_Z)], G[sl][:len(SAT_Z)]
+    bad = np.abs(got - ref) > 2e-6 * np.abs(ref) + 1e-37
+    assert not bad.any(), [(float(SAT_Z[i]), float(got[i]), float(ref[i]))
+                           for i in np.flatnonzero(bad)]
 
 
 @pytest.mark.parametrize("dims,acts,n", [
