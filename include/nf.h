@@ -227,32 +227,60 @@ nf_status nf_load(const char* path, nf_net** out);
 
 /* Per-kernel timing, for measuring the method's computational performance the
  * way section 5 reports it (elapsed time), one kernel at a time.  While
- * recording is on, every kernel the net launches is bracketed by a pair of HIP
- * events on its stream, and the library notes the algorithmic bytes the
- * kernel must move (inputs read once, outputs written once) and the flops of
- * its contraction (2 per multiply-add, no padding).  Recording costs time;
- * leave it off for throughput runs. */
+ * recording is on, every kernel the net launches is timed with a pair of HIP
+ * events, and the library notes the algorithmic bytes the kernel must move
+ * (inputs read once, outputs written once) and the flops of its contraction
+ * (2 per multiply-add, no padding). */
 typedef struct {
   char name[64];      /* kernel family, e.g. "gemm_fwd_stash_128x128" */
   int64_t launches;   /* launches recorded since the last read             */
   double total_ms;    /* sum of the measured durations (ms)                */
   double bytes;       /* algorithmic bytes, summed over the launches       */
   double flops;       /* algorithmic flops, summed over the launches       */
+  double min_ms;      /* shortest and longest single measured duration (ms) */
+  double max_ms;
 } nf_kernel_stat;
 
-/* repeats = 0 turns recording off.  repeats = R >= 1 turns it on (discarding
- * anything recorded and not yet read): each launch is then run R times in a
- * row between its two events and charged the average of the R runs, which
- * keeps the fixed cost of the event pair out of short kernels.  Repeating is
- * harmless because no kernel writes a buffer it reads: a training step reads
- * the parameters from one buffer and writes the updated ones to another.
- * repeats must be in 0 .. 1000. */
+/* repeats = 0 turns recording off.  repeats = 1 turns it on (discarding
+ * anything recorded and not yet read) with the two events of a launch bound
+ * to that kernel's dispatch, so each launch is charged its own start-to-end
+ * time and nothing is added between launches.  repeats = R >= 2 instead runs
+ * each launch R times in a row between two events recorded on its stream and
+ * charges it the average of the R runs; repeating is harmless because no
+ * kernel writes a buffer it reads (a training step reads the parameters from
+ * one buffer and writes the updated ones to another), but the repeats find
+ * their inputs in cache.  repeats must be in 0 .. 1000. */
 nf_status nf_profile(nf_net* net, int32_t repeats);
 
 /* Wait for the recorded work, then write one entry per kernel name (at most
  * cap entries, ordered by total time, largest first) to out[] and their number
  * to *count; the records are then cleared. */
 nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t* count);
+
+/* Measurement aids: the device's own peaks, against which the roofline
+ * fractions of the kernels above are read (the published peaks are quoted
+ * beside them).  Each runs one kernel on `stream` (void* hipStream_t), waits
+ * for it, and returns the kernel's own start-to-end time in *host_ms.
+ * nf_calib_read: a streaming read of `bytes` bytes at d_src (a positive
+ * multiple of 16 at a 16-byte aligned device address), 4 workgroups of 256
+ * threads per compute unit, 16-byte loads; d_sink is device scratch of at
+ * least NF_CALIB_SINK_BYTES bytes.
+ * nf_calib_copy: the same access pattern copying d_src to d_dst.
+ * nf_calib_mfma: a loop of independent matrix-core instructions, `iters`
+ * rounds of 8 per wave on 2 workgroups of 4 waves per compute unit
+ * (v_mfma_f32_32x32x2f32 for dtype NF_F32, v_mfma_f64_16x16x4f64 for
+ * NF_F64); *host_flops receives the flops it performed (2 per multiply-add)
+ * and *host_clock_ghz the mean shader clock of its waves, from the shader
+ * cycle counter against the 100 MHz constant clock.  d_sink as above.
+ * Errors: NF_EINVAL for NULL pointers, bad sizes or alignment; NF_EDEVICE
+ * when there is no device or a HIP call fails. */
+#define NF_CALIB_SINK_BYTES (1 << 20)
+nf_status nf_calib_read(const void* d_src, int64_t bytes, void* d_sink, void* stream,
+                        double* host_ms);
+nf_status nf_calib_copy(void* d_dst, const void* d_src, int64_t bytes, void* stream,
+                        double* host_ms);
+nf_status nf_calib_mfma(int32_t dtype, int64_t iters, void* d_sink, void* stream,
+                        double* host_ms, double* host_flops, double* host_clock_ghz);
 
 /* Message for the last failed call on this thread ("" if none).  The pointer
  * stays valid until the next nf_* call on the same thread. */

@@ -17,8 +17,18 @@
 #include "nf_split.h"
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
+
+namespace nf {
+LaunchEvents& launch_events() {
+  thread_local LaunchEvents ev;
+  return ev;
+}
+void set_error_message(const char* msg) { g_err = msg; }
+}  // namespace nf
+
+namespace {
 
 nf_status fail(nf_status st, const std::string& msg) {
   g_err = msg;
@@ -225,42 +235,48 @@ void clear_recs(nf_net* n) {
   n->recs.clear();
 }
 
-// Runs `enqueue` on stream s.  With recording on, the launch is bracketed by a
-// pair of events and, for R > 1, repeated R times in a row between them (every
-// kernel reads only buffers it does not write, so a repeat recomputes the same
-// values); the record is charged the average of the R runs.
+// Runs `enqueue` (one kernel launch) on stream s.  With recording on, the
+// launch is timed by a pair of events: for R = 1 the events are bound to the
+// kernel's own dispatch (its start and end timestamps, no marker between
+// launches); for R > 1 they are recorded on the stream around R back-to-back
+// runs of the launch (every kernel reads only buffers it does not write, so
+// a repeat recomputes the same values) and the record is charged the average.
 template <class F>
 nf_status timed(nf_net* n, const char* name, double bytes, double flops, hipStream_t s,
                 F&& enqueue) {
   nf_net::Rec r{name, nullptr, nullptr, bytes, flops, n->prof};
+  auto drop = [&] {
+    if (r.a) (void)hipEventDestroy(r.a);
+    if (r.b) (void)hipEventDestroy(r.b);
+  };
   if (n->prof) {
     hipError_t e = hipEventCreate(&r.a);
     if (e == hipSuccess) e = hipEventCreate(&r.b);
-    if (e == hipSuccess) e = hipEventRecord(r.a, s);
+    if (e == hipSuccess && n->prof > 1) e = hipEventRecord(r.a, s);
     if (e != hipSuccess) {
-      if (r.a) (void)hipEventDestroy(r.a);
-      if (r.b) (void)hipEventDestroy(r.b);
+      drop();
       return hip_fail(e, "profiling event");
     }
   }
   const int reps = n->prof > 1 ? n->prof : 1;
+  nf::LaunchEvents& ev = nf::launch_events();
   for (int i = 0; i < reps; ++i) {
+    if (n->prof == 1) ev = {r.a, r.b};
     hipError_t e = enqueue();
+    ev = {};
     if (e != hipSuccess) {
-      if (r.a) (void)hipEventDestroy(r.a);
-      if (r.b) (void)hipEventDestroy(r.b);
+      drop();
       return hip_fail(e, "kernel launch");
     }
   }
-  if (n->prof) {
+  if (n->prof > 1) {
     hipError_t e = hipEventRecord(r.b, s);
     if (e != hipSuccess) {
-      (void)hipEventDestroy(r.a);
-      (void)hipEventDestroy(r.b);
+      drop();
       return hip_fail(e, "profiling event");
     }
-    n->recs.push_back(r);
   }
+  if (n->prof) n->recs.push_back(r);
   return NF_OK;
 }
 
@@ -1512,8 +1528,11 @@ nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t
         k = &agg.back();
         std::snprintf(k->name, sizeof(k->name), "%s", r.name);
       }
+      const double one = ms / (r.repeats > 1 ? r.repeats : 1);
+      k->min_ms = k->launches == 0 ? one : std::min(k->min_ms, one);
+      k->max_ms = k->launches == 0 ? one : std::max(k->max_ms, one);
       k->launches += 1;
-      k->total_ms += ms / (r.repeats > 1 ? r.repeats : 1);
+      k->total_ms += one;
       k->bytes += r.bytes;
       k->flops += r.flops;
     }

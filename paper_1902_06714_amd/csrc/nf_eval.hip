@@ -79,8 +79,8 @@ hipError_t launch_count_correct(const T* out, int64_t ldo, const T* y, int64_t l
   if (n <= 0 || d <= 0) return hipErrorInvalidValue;
   const int64_t want = (n + EVAL_WAVES - 1) / EVAL_WAVES;
   const int blocks = (int)(want < 2048 ? want : 2048);
-  count_correct_kernel<T><<<blocks, 64 * EVAL_WAVES, 0, s>>>(out, ldo, y, ldy, n, d, count);
-  return hipGetLastError();
+  return launch_k(count_correct_kernel<T>, blocks, 64 * EVAL_WAVES, 0, s, out, ldo, y, ldy, n, d,
+                  count);
 }
 
 template hipError_t launch_count_correct<float>(const float*, int64_t, const float*, int64_t,

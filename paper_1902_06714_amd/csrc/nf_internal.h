@@ -1,10 +1,40 @@
 // Internal declarations shared by the host runtime and the kernel launchers.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace nf {
+
+// Every kernel of the library is launched through launch_k.  While the host
+// runtime times one launch by the kernel's own start and end (nf_profile with
+// repeats = 1) it sets launch_events to a pair of HIP events, which the
+// launch binds to that kernel's dispatch; otherwise both are null and the
+// launch is a plain one.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+// Sets the message nf_last_error returns on this thread.
+void set_error_message(const char* msg);
+
+template <class T>
+struct same_type {
+  using type = T;
+};
+
+// args convert to the kernel's parameter types (which alone fix P...); each
+// is passed by the address of that converted copy
+template <typename... P>
+inline hipError_t launch_k(void (*kernel)(P...), dim3 grid, dim3 block, unsigned shmem,
+                           hipStream_t s, const typename same_type<P>::type&... args) {
+  void* argv[] = {const_cast<void*>(static_cast<const void*>(&args))..., nullptr};
+  const LaunchEvents& ev = launch_events();
+  return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, shmem, s,
+                            ev.start, ev.stop, 0);
+}
 
 // Epilogue of the tiled MFMA contraction C = A(m,k) * B(k,n).
 enum Epilogue : int {

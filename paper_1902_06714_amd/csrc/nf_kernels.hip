@@ -458,8 +458,8 @@ template <class T, int BM, int BN, int BK, int WM, int WN, int PD, bool AKC, boo
 static hipError_t launch_one(int nsplit, const GemmParamsT<T>& p, hipStream_t s) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, nsplit);
-  gemm_kernel<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, EPI><<<grid, NT, 0, s>>>(p);
-  return hipGetLastError();
+  return launch_k(gemm_kernel<T, BM, BN, BK, WM, WN, PD, AKC, BKC, AV, BV, EPI>, grid, NT, 0, s,
+                  p);
 }
 
 template <class T, int BM, int BN, int BK, int WM, int WN, int PD>
@@ -569,14 +569,12 @@ hipError_t launch_fwd_fold(int epi, const FwdFoldParamsT<T>& f, hipStream_t s) {
   if (total <= 0 || f.nsplit < 1) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((total + 255) / 256));
   if (epi == EPI_FWD_STASH)
-    fwd_fold_kernel<T, EPI_FWD_STASH><<<grid, 256, 0, s>>>(f);
+    return launch_k(fwd_fold_kernel<T, EPI_FWD_STASH>, grid, 256, 0, s, f);
   else if (epi == EPI_FWD_DELTA)
-    fwd_fold_kernel<T, EPI_FWD_DELTA><<<grid, 256, 0, s>>>(f);
+    return launch_k(fwd_fold_kernel<T, EPI_FWD_DELTA>, grid, 256, 0, s, f);
   else if (epi == EPI_FWD_OUT)
-    fwd_fold_kernel<T, EPI_FWD_OUT><<<grid, 256, 0, s>>>(f);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+    return launch_k(fwd_fold_kernel<T, EPI_FWD_OUT>, grid, 256, 0, s, f);
+  return hipErrorInvalidValue;
 }
 
 template hipError_t launch_fwd_fold<float>(int, const FwdFoldParamsT<float>&, hipStream_t);
@@ -592,8 +590,7 @@ hipError_t launch_fold_sgd(FoldGroupT<T> g, hipStream_t s) {
     g.start[q + 1] = g.start[q] + (int)((elems + threads - 1) / threads);
   }
   for (int q = g.n + 1; q <= FOLD_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
-  fold_sgd_kernel<T><<<dim3((unsigned)g.start[g.n]), threads, 0, s>>>(g);
-  return hipGetLastError();
+  return launch_k(fold_sgd_kernel<T>, dim3((unsigned)g.start[g.n]), threads, 0, s, g);
 }
 
 template hipError_t launch_fold_sgd<float>(FoldGroupT<float>, hipStream_t);
@@ -608,9 +605,9 @@ static hipError_t launch_group(GemmGroupT<T> g, const int* nsplit, hipStream_t s
     g.start[q + 1] = g.start[q] + mt * nt * nsplit[q];
   }
   for (int q = g.n + 1; q <= GEMM_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
-  gemm_group_kernel<T, BM, BN, 16, WM, WN, PD, false, false, true, BV, EPI_DW_PARTIAL>
-      <<<dim3((unsigned)g.start[g.n]), NT, 0, s>>>(g);
-  return hipGetLastError();
+  return launch_k(
+      gemm_group_kernel<T, BM, BN, 16, WM, WN, PD, false, false, true, BV, EPI_DW_PARTIAL>,
+      dim3((unsigned)g.start[g.n]), NT, 0, s, g);
 }
 
 template <class T>

@@ -444,11 +444,11 @@ static int medium_tile_blocks(int B, int ncu, int esz) {
 }
 
 template <class T, int NSB>
-static void launch_nsb(const MediumParamsT<T>& p, dim3 grid, hipStream_t s) {
+static hipError_t launch_nsb(const MediumParamsT<T>& p, dim3 grid, hipStream_t s) {
   switch (p.L) {
-    case 2: medium_kernel<T, NSB, 2><<<grid, M_THREADS, 0, s>>>(p); break;
-    case 3: medium_kernel<T, NSB, 3><<<grid, M_THREADS, 0, s>>>(p); break;
-    default: medium_kernel<T, NSB, 4><<<grid, M_THREADS, 0, s>>>(p); break;
+    case 2: return launch_k(medium_kernel<T, NSB, 2>, grid, M_THREADS, 0, s, p);
+    case 3: return launch_k(medium_kernel<T, NSB, 3>, grid, M_THREADS, 0, s, p);
+    default: return launch_k(medium_kernel<T, NSB, 4>, grid, M_THREADS, 0, s, p);
   }
 }
 
@@ -459,15 +459,14 @@ hipError_t launch_medium(const MediumParamsT<T>& p, int ncu, hipStream_t s) {
   const int ntiles = (p.B + 16 * nsb - 1) / (16 * nsb);
   const dim3 grid(ntiles < ncu ? ntiles : ncu);
   if constexpr (sizeof(T) == 8) {
-    launch_nsb<T, 1>(p, grid, s);
+    return launch_nsb<T, 1>(p, grid, s);
   } else {
     switch (nsb) {
-      case 1: launch_nsb<T, 1>(p, grid, s); break;
-      case 2: launch_nsb<T, 2>(p, grid, s); break;
-      default: launch_nsb<T, 3>(p, grid, s); break;
+      case 1: return launch_nsb<T, 1>(p, grid, s);
+      case 2: return launch_nsb<T, 2>(p, grid, s);
+      default: return launch_nsb<T, 3>(p, grid, s);
     }
   }
-  return hipGetLastError();
 }
 
 template hipError_t launch_medium<float>(const MediumParamsT<float>&, int, hipStream_t);

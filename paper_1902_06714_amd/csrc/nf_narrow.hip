@@ -761,35 +761,32 @@ hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s
     case NK_FWD4: {
       const dim3 grid((p.B + N4_T - 1) / N4_T);
       if (train)
-        narrow_fwd4_kernel<true><<<grid, block, 0, s>>>(p);
+        return launch_k(narrow_fwd4_kernel<true>, grid, block, 0, s, p);
       else
-        narrow_fwd4_kernel<false><<<grid, block, 0, s>>>(p);
-      break;
+        return launch_k(narrow_fwd4_kernel<false>, grid, block, 0, s, p);
     }
     case NK_FWD16: {
       const dim3 grid((p.B + NARROW_TILE - 1) / NARROW_TILE);
       if (train)
-        narrow_fwd16_kernel<true, N1_PRE_TRAIN><<<grid, block, 0, s>>>(p);
+        return launch_k(narrow_fwd16_kernel<true, N1_PRE_TRAIN>, grid, block, 0, s, p);
       else
-        narrow_fwd16_kernel<false, N1_PRE_INFER><<<grid, block, 0, s>>>(p);
-      break;
+        return launch_k(narrow_fwd16_kernel<false, N1_PRE_INFER>, grid, block, 0, s, p);
     }
     case NK_INFER: {
       const dim3 grid(narrow_infer_grid(p));
       // chunks per wave
       switch (((p.d0 + NI_CH - 1) / NI_CH + N1_WAVES - 1) / N1_WAVES) {
-        case 1: narrow_infer_kernel<1><<<grid, block, 0, s>>>(p); break;
-        case 2: narrow_infer_kernel<2><<<grid, block, 0, s>>>(p); break;
-        case 3: narrow_infer_kernel<3><<<grid, block, 0, s>>>(p); break;
-        case 4: narrow_infer_kernel<4><<<grid, block, 0, s>>>(p); break;
-        case 5: narrow_infer_kernel<5><<<grid, block, 0, s>>>(p); break;
-        case 6: narrow_infer_kernel<6><<<grid, block, 0, s>>>(p); break;
-        default: narrow_infer_kernel<NI_MC_MAX><<<grid, block, 0, s>>>(p); break;
+        case 1: return launch_k(narrow_infer_kernel<1>, grid, block, 0, s, p);
+        case 2: return launch_k(narrow_infer_kernel<2>, grid, block, 0, s, p);
+        case 3: return launch_k(narrow_infer_kernel<3>, grid, block, 0, s, p);
+        case 4: return launch_k(narrow_infer_kernel<4>, grid, block, 0, s, p);
+        case 5: return launch_k(narrow_infer_kernel<5>, grid, block, 0, s, p);
+        case 6: return launch_k(narrow_infer_kernel<6>, grid, block, 0, s, p);
+        default: return launch_k(narrow_infer_kernel<NI_MC_MAX>, grid, block, 0, s, p);
       }
-      break;
     }
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 const char* narrow_fwd_name(bool train, const NarrowFwdParams& p) {
@@ -804,8 +801,7 @@ const char* narrow_fwd_name(bool train, const NarrowFwdParams& p) {
 }
 
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s) {
-  narrow_dw_kernel<<<dim3(p.ntiles), N2_WAVES * 64, 0, s>>>(p);
-  return hipGetLastError();
+  return launch_k(narrow_dw_kernel, dim3(p.ntiles), N2_WAVES * 64, 0, s, p);
 }
 
 }  // namespace nf

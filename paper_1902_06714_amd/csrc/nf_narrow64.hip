@@ -503,17 +503,15 @@ hipError_t launch_narrow64_fwd(bool train, const NarrowFwdParamsT<double>& p, hi
   if (p.B <= NARROW_SMALL_BATCH) {
     const dim3 grid((p.B + D4_T - 1) / D4_T);
     if (train)
-      narrow64_fwd4_kernel<true><<<grid, D_WAVES * 64, 0, s>>>(p);
+      return launch_k(narrow64_fwd4_kernel<true>, grid, D_WAVES * 64, 0, s, p);
     else
-      narrow64_fwd4_kernel<false><<<grid, D_WAVES * 64, 0, s>>>(p);
-    return hipGetLastError();
+      return launch_k(narrow64_fwd4_kernel<false>, grid, D_WAVES * 64, 0, s, p);
   }
   const dim3 grid((p.B + D_T - 1) / D_T);
   if (train)
-    narrow64_fwd_kernel<true><<<grid, D_WAVES * 64, 0, s>>>(p);
+    return launch_k(narrow64_fwd_kernel<true>, grid, D_WAVES * 64, 0, s, p);
   else
-    narrow64_fwd_kernel<false><<<grid, D_WAVES * 64, 0, s>>>(p);
-  return hipGetLastError();
+    return launch_k(narrow64_fwd_kernel<false>, grid, D_WAVES * 64, 0, s, p);
 }
 
 const char* narrow64_fwd_name(bool train, const NarrowFwdParamsT<double>& p) {
@@ -522,8 +520,7 @@ const char* narrow64_fwd_name(bool train, const NarrowFwdParamsT<double>& p) {
 }
 
 hipError_t launch_narrow64_dw(const NarrowDwParamsT<double>& p, hipStream_t s) {
-  narrow64_dw_kernel<<<dim3(p.ntiles), D2_WAVES * 64, 0, s>>>(p);
-  return hipGetLastError();
+  return launch_k(narrow64_dw_kernel, dim3(p.ntiles), D2_WAVES * 64, 0, s, p);
 }
 
 }  // namespace nf

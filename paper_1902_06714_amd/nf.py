@@ -50,7 +50,8 @@ _net_p = ctypes.c_void_p
 class nf_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 64), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("bytes", ctypes.c_double),
-                ("flops", ctypes.c_double)]
+                ("flops", ctypes.c_double), ("min_ms", ctypes.c_double),
+                ("max_ms", ctypes.c_double)]
 
 
 _sig = {
@@ -105,6 +106,14 @@ _sig = {
     "nf_profile": (ctypes.c_int, [_net_p, ctypes.c_int32]),
     "nf_profile_read": (ctypes.c_int, [_net_p, ctypes.POINTER(nf_kernel_stat), ctypes.c_int32,
                                        ctypes.POINTER(ctypes.c_int32)]),
+    "nf_calib_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
+    "nf_calib_copy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                     ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
+    "nf_calib_mfma": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_double)]),
     "nf_last_error": (ctypes.c_char_p, []),
 }
 for _name, (_res, _args) in _sig.items():
@@ -329,13 +338,42 @@ def nf_profile(net, repeats: int) -> None:
 
 
 def nf_profile_read(net, cap: int = 64) -> list:
-    """[{name, launches, total_ms, bytes, flops}], largest total time first."""
+    """[{name, launches, total_ms, bytes, flops, min_ms, max_ms}], largest
+    total time first."""
     buf = (nf_kernel_stat * cap)()
     n = ctypes.c_int32()
     _check(_lib.nf_profile_read(net, buf, cap, ctypes.byref(n)), "nf_profile_read")
     return [{"name": buf[i].name.decode(), "launches": buf[i].launches,
-             "total_ms": buf[i].total_ms, "bytes": buf[i].bytes, "flops": buf[i].flops}
+             "total_ms": buf[i].total_ms, "bytes": buf[i].bytes, "flops": buf[i].flops,
+             "min_ms": buf[i].min_ms, "max_ms": buf[i].max_ms}
             for i in range(n.value)]
+
+
+NF_CALIB_SINK_BYTES = 1 << 20
+
+
+def nf_calib_read(src, sink, stream=None) -> float:
+    """ms of one streaming read of the GPU tensor src (sink: a GPU tensor of at
+    least NF_CALIB_SINK_BYTES bytes)."""
+    ms = ctypes.c_double()
+    _check(_lib.nf_calib_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(),
+                              _stream(stream), ctypes.byref(ms)), "nf_calib_read")
+    return ms.value
+
+
+def nf_calib_copy(dst, src, stream=None) -> float:
+    ms = ctypes.c_double()
+    _check(_lib.nf_calib_copy(dst.data_ptr(), src.data_ptr(), src.numel() * src.element_size(),
+                              _stream(stream), ctypes.byref(ms)), "nf_calib_copy")
+    return ms.value
+
+
+def nf_calib_mfma(dtype: int, iters: int, sink, stream=None):
+    """(ms, flops, shader clock GHz) of the matrix-core loop."""
+    ms, fl, ghz = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(_lib.nf_calib_mfma(dtype, iters, sink.data_ptr(), _stream(stream), ctypes.byref(ms),
+                              ctypes.byref(fl), ctypes.byref(ghz)), "nf_calib_mfma")
+    return ms.value, fl.value, ghz.value
 
 
 def nf_last_error() -> str:

@@ -19,6 +19,12 @@ as the reference decides it.  The free-running reference takes the free
 GPU run's decisions step by step in the same way; the distance to the plain
 reference (which decides every unit itself) and the spread of the plain
 reference under the other choice for the band units are reported beside it.
+
+The 784-1024^3-10 schedule is chaotic in its last steps: the reference run
+from theta_0 moved by one ulp per parameter separates from itself by 1.7e-5
+after 10 steps but 8e-4 after 16.  The free-running gate after step t is
+therefore max(1e-4, that one-ulp spread at t), computed here from the
+reference alone; after 10 steps it is the fixed 1e-4.
 """
 
 import sys
@@ -46,22 +52,48 @@ def _reference(w, X, Y, theta, steps, shards, kink_tol=0.0):
     return thetas, grads
 
 
-def _kink_step(w, theta, X, Y, shards, sides):
+def _kink_step(w, theta, X, Y, shards, sides, band=parity.KINK_BAND):
     if sides is None:       # already a failure; the plain step keeps the rest meaningful
         return mlp.train_batch(theta, w.dims, list(w.acts), X, Y, w.eta, shards)
     return mlp.train_batch(theta, w.dims, list(w.acts), X, Y, w.eta, shards,
-                           kink_tol=parity.KINK_BAND, kink_given=sides)
+                           kink_tol=band, kink_given=sides)
 
 
-def _sides(net, w, theta, X, fails, what):
+def _sides(net, w, theta, X, fails, what, band=parity.KINK_BAND):
     sides = parity.gpu_kink_sides(net.nf, net.h, w.dims, w.acts, X.shape[0])
     if sides is None:
         fails.append(f"{what}: the GPU step kept no relu decisions")
         return None, {}
     stats = {}
     fails += [f"{what}: {m}" for m in parity.check_kink_sides(sides, theta, w.dims, w.acts, X,
-                                                              stats=stats)]
+                                                              band=band, stats=stats)]
     return sides, stats
+
+
+def _ulp_spread(w, X, Y, theta0, ref_t, steps, shards):
+    """The reference's own sensitivity to the last bit of its state: its
+    trajectory from theta_0 moved by one fp32 ulp per parameter (seeded random
+    signs), taking the unmoved trajectory's relu decisions inside the kink
+    band, against the unmoved trajectory.  Worst floored parameter error after
+    each step.  Every fp32 step rounds the parameters, so no fp32 computation
+    can be held closer to the reference than this after t steps."""
+    rng = np.random.default_rng(20260)
+    b = (theta0 + np.where(rng.random(theta0.size) < 0.5, -1.0, 1.0)
+         * np.spacing(np.abs(theta0))).astype(np.float32)
+    acts = parity.full_acts(w.dims, w.acts)
+    L = len(w.dims) - 1
+    out = []
+    for t in range(steps):
+        sl = slice(t * w.batch, (t + 1) * w.batch)
+        Za, _ = mlp.forward(ref_t[t], w.dims, acts, X[sl])
+        sides = [(Za[l] > 0).astype(np.float32) if acts[l - 1] == "relu" and l < L else None
+                 for l in range(1, L + 1)]
+        b, _ = mlp.train_batch(b, w.dims, acts, X[sl], Y[sl], w.eta, shards,
+                               kink_tol=parity.KINK_BAND, kink_given=sides)
+        rep = {}
+        parity.check_params(b, ref_t[t + 1], w.dims, report=rep)
+        out.append(parity.worst(rep))
+    return out
 
 
 def _run(name, steps=None, shards=None):
@@ -74,6 +106,11 @@ def _run(name, steps=None, shards=None):
     X, Y = W.make_data(w, w.batch * steps)
     theta0 = W.make_params(w)
     ref_t, ref_g = _reference(w, X, Y, theta0, steps, shards)
+    # free-running gate after step t: max(PARAM_TOL, the reference's own
+    # one-ulp spread at t); the kink band widens the same way, since two
+    # trajectories that far apart may decide units that far from the kink
+    # differently.  Networks without kinks keep the fixed gate.
+    ulp_spread = _ulp_spread(w, X, Y, theta0, ref_t, steps, shards) if kinked else [0.0] * steps
     xd, yd = to_dev(X), to_dev(Y)
     fails = []
     worst = {"along_params": 0.0, "along_grads": 0.0, "along_update": 0.0, "free_params": 0.0}
@@ -110,17 +147,21 @@ def _run(name, steps=None, shards=None):
             net.train_batch(xd[sl], yd[sl], w.eta, shards)
             p, g = net.params(), net.grads()
             kstats = {}
+            tol_p = max(parity.PARAM_TOL, ulp_spread[t])
+            band = max(parity.KINK_BAND, ulp_spread[t])
             if kinked:
-                sides, kstats = _sides(net, w, th_o, X[sl], fails, f"free {t}")
-                th_new, G_o = _kink_step(w, th_o, X[sl], Y[sl], shards, sides)
+                sides, kstats = _sides(net, w, th_o, X[sl], fails, f"free {t}", band)
+                th_new, G_o = _kink_step(w, th_o, X[sl], Y[sl], shards, sides, band)
             else:
                 th_new, G_o = ref_t[t + 1], ref_g[t]
             rp, rg = {}, {}
-            fails += [f"free {t}: {m}" for m in parity.check_params(p, th_new, w.dims, report=rp)]
+            fails += [f"free {t}: {m}" for m in parity.check_params(p, th_new, w.dims, tol=tol_p,
+                                                                    report=rp)]
             gfails = parity.check_grads(g, G_o, w.dims, report=rg)
             if not kinked:
                 fails += [f"free {t}: {m}" for m in gfails]
-            rec = {"params": rp, "grads": rg, "kinks": kstats}
+            rec = {"params": rp, "grads": rg, "kinks": kstats, "gate": tol_p,
+                   "reference_ulp_spread": ulp_spread[t]}
             if kinked:
                 plain = {}
                 parity.check_params(p, ref_t[t + 1], w.dims, report=plain)
@@ -154,9 +195,14 @@ def _run(name, steps=None, shards=None):
         parity.emit(f"{name} free-running after 10 steps",
                     {"gpu_vs_reference_with_gpu_decisions": free_dec[9], "gpu_vs_plain_reference":
                      free_plain[9], "plain_reference_spread": spread[9],
-                     "per_step_vs_plain": free_plain, "per_step_spread": spread})
-        msg += (f"; after 10 steps: {free_dec[9]:.2e} (gated), vs the plain reference "
-                f"{free_plain[9]:.2e}, the plain reference's own spread {spread[9]:.2e}")
+                     "reference_ulp_spread": ulp_spread[9],
+                     "per_step_gated": free_dec, "per_step_vs_plain": free_plain,
+                     "per_step_spread": spread, "per_step_ulp_spread": ulp_spread})
+        gate10 = max(parity.PARAM_TOL, ulp_spread[9])
+        msg += (f"; after 10 steps: {free_dec[9]:.2e} (gated at {gate10:.1e}), "
+                f"vs the plain reference {free_plain[9]:.2e}, the plain reference's spread "
+                f"over the band's decisions {spread[9]:.2e}, over one ulp {ulp_spread[9]:.2e}; "
+                f"at the end {free_dec[-1]:.2e} (gated at {max(parity.PARAM_TOL, ulp_spread[-1]):.1e})")
     print(msg, file=sys.stderr, flush=True)
     assert not fails, "\n".join(fails[:30])
     return w, X, Y, theta0
