@@ -12,9 +12,11 @@ line on stdout; per-kernel timings go to stderr.  `value` is the warm rate
 write larger than the 256 MB memory-side cache, each from the initial
 parameters.
 
-Per-kernel durations come from a pass over one more step with every launch
-timed by its own start and end (nf_profile with repeats 1: HIP events bound
-to the kernel's dispatch on the stream it runs on).  `roofline` is the
+Per-kernel durations come from the timed steps run once more (up to five)
+with every launch timed by its own start and end (nf_profile with repeats 1:
+HIP events bound to the kernel's dispatch on the stream it runs on), behind a
+spin kernel that holds the stream while the host enqueues them, so that they
+run back to back as in the timed region.  `roofline` is the
 kernel with the most time per step, its achieved rate being the compulsory
 bytes (inputs, targets and parameters read once, parameters written once:
 per sample d_0 + d_L elements, per SGD step twice the parameter count) or
@@ -51,6 +53,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 FP64_MFMA_PEAK_TFS = 78.6      # MI355X dense fp64 matrix, TFLOP/s
+PROFILE_SPIN_US = 60000.0      # stream held while the profiled steps are enqueued
 
 METRIC = "training samples/sec (fwd+bwd+SGD) at 784-30-10 and wide MLP; % HBM/MFMA roofline"
 
@@ -176,7 +179,7 @@ def measure_peaks(torch, nf, dev):
     out["method"] = ("nf_calib_read / nf_calib_copy over 1 GiB (best of 3; the copy counts its "
                      "reads and writes), nf_calib_read over 31.36 MB back to back (best of 4 "
                      "after one), nf_calib_mfma 8 independent 32x32x2 fp32 / 16x16x4 fp64 chains "
-                     "per wave, 8 waves per CU (best of 3); kernel timestamps")
+                     "per wave, 8 (fp32) or 16 (fp64) waves per CU (best of 3); kernel timestamps")
     return out
 
 
@@ -259,16 +262,23 @@ def run_workload(args, w, f64: bool, steps: int, warmup: int, cold_reps: int, lo
                 + ", ".join(f"{c:.3f}" for c in cold) + " ms per step")
         res["cold"] = cold
 
-        # one more step, every launch timed by its own start and end; the
-        # step as a whole is timed too, to show what the timing costs
+        # the timed steps once more with every launch timed by its own start
+        # and end (events bound to each kernel's dispatch).  Such a launch
+        # costs the host more than the kernel runs, so a spin kernel holds the
+        # stream while the host enqueues the steps; they then run back to
+        # back as in the timed region (whose own time these steps report too)
+        psteps = min(steps, 5)
         nf.nf_profile(net, 1)
+        nf.nf_calib_spin(PROFILE_SPIN_US)
         evs[0].record(stream)
-        step()
-        evs[1].record(stream)
+        for i in range(psteps):
+            step()
+            evs[i + 1].record(stream)
         stats = nf.nf_profile_read(net)
         nf.nf_profile(net, 0)
         torch.cuda.synchronize()
-        res["profiled_step_ms"] = evs[0].elapsed_time(evs[1])
+        res["profiled_ms_per_step"] = evs[0].elapsed_time(evs[psteps]) / psteps
+        res["profiled_steps"] = psteps
         res["stats"] = stats
         res["finite"] = bool(np.all(np.isfinite(nf.nf_get_params_f64(net) if f64
                                                 else nf.nf_get_params(net))))
@@ -299,10 +309,11 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
         avg_s = k["total_ms"] / k["launches"] / 1e3
         design_b = k["bytes"] / k["launches"]
         flops_l = k["flops"] / k["launches"]
+        per_step = k["launches"] / res["profiled_steps"]
         if is_inference_kernel(k["name"]):
-            comp = infer_bytes / k["launches"] if infer_bytes else design_b
+            comp = infer_bytes / per_step if infer_bytes else design_b
         else:
-            comp = step_bytes * w.steps / k["launches"]
+            comp = step_bytes * w.steps / per_step
         if flops_l / design_b < ridge:
             achieved = comp / avg_s / 1e9
             r = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -316,7 +327,8 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
         r["avg_us"] = avg_s * 1e6
         r["min_us"] = k["min_ms"] * 1e3
         r["max_us"] = k["max_ms"] * 1e3
-        r["launches_per_step"] = k["launches"]
+        r["launches_per_step"] = per_step
+        r["launches_timed"] = k["launches"]
         r["bytes_per_launch"] = comp
         r["design_bytes_per_launch"] = design_b
         r["flops_per_launch"] = flops_l
@@ -327,7 +339,7 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
     ms = res["ms"]
     ms_step = ms / steps
     n_train = w.batch * w.steps
-    step_flops = sum(k["flops"] for k in stats)
+    step_flops = sum(k["flops"] for k in stats) / res["profiled_steps"]
     whole_bytes = step_bytes * w.steps + infer_bytes
     if kernels[0]["bound"] == "hbm":
         ach = whole_bytes / (ms_step / 1e3) / 1e9
@@ -337,9 +349,9 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
         ach = step_flops / (ms_step / 1e3) / 1e12
         step_roof = {"bound": "mfma", "achieved": ach, "peak": mfma_peak, "unit": "TFLOP/s",
                      "frac": ach / mfma_peak, "flops_per_step": step_flops}
-    busy = sum(k["total_ms"] for k in stats)
-    step_roof["kernel_busy_ms"] = busy
-    step_roof["profiled_step_ms"] = res["profiled_step_ms"]
+    psteps = res["profiled_steps"]
+    step_roof["kernel_busy_ms_per_step"] = sum(k["total_ms"] for k in stats) / psteps
+    step_roof["profiled_ms_per_step"] = res["profiled_ms_per_step"]
     per_step = res["per_step"]
     out = {
         "value": n_train * steps / (ms / 1e3),

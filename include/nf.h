@@ -267,14 +267,21 @@ nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t
  * least NF_CALIB_SINK_BYTES bytes.
  * nf_calib_copy: the same access pattern copying d_src to d_dst.
  * nf_calib_mfma: a loop of independent matrix-core instructions, `iters`
- * rounds of 8 per wave on 2 workgroups of 4 waves per compute unit
+ * rounds of 8 per wave on 2 (fp32) or 4 (fp64) workgroups of 4 waves per compute unit
  * (v_mfma_f32_32x32x2f32 for dtype NF_F32, v_mfma_f64_16x16x4f64 for
  * NF_F64); *host_flops receives the flops it performed (2 per multiply-add)
  * and *host_clock_ghz the mean shader clock of its waves, from the shader
  * cycle counter against the 100 MHz constant clock.  d_sink as above.
  * Errors: NF_EINVAL for NULL pointers, bad sizes or alignment; NF_EDEVICE
  * when there is no device or a HIP call fails. */
+/* nf_calib_spin: enqueue on `stream` one kernel that returns after `us`
+ * microseconds (0 .. 1e6; one wave polling the 100 MHz constant clock) and
+ * return at once.  Work the host enqueues behind it meanwhile starts back to
+ * back when it ends, so kernels timed with nf_profile(net, 1), whose launches
+ * cost the host more than their run time, still run as in an untimed
+ * sequence. */
 #define NF_CALIB_SINK_BYTES (1 << 20)
+nf_status nf_calib_spin(void* stream, double us);
 nf_status nf_calib_read(const void* d_src, int64_t bytes, void* d_sink, void* stream,
                         double* host_ms);
 nf_status nf_calib_copy(void* d_dst, const void* d_src, int64_t bytes, void* stream,

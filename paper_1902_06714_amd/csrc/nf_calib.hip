@@ -74,7 +74,9 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_copy_kernel(float4* dst, co
 // (s_memtime) and the 100 MHz constant clock (s_memrealtime) at its start and
 // end, so the host can tell the clock the matrix cores ran at
 constexpr int CAL_CHAINS = 8;
-constexpr int CAL_MFMA_WG = 2;   // workgroups of 4 waves per CU: two waves per SIMD
+// workgroups of 4 waves per CU: two waves per SIMD for fp32 (128 accumulator
+// registers each), four for fp64 (64 each), whose chains need more in flight
+constexpr int CAL_MFMA_WG32 = 2, CAL_MFMA_WG64 = 4;
 
 template <bool F64>
 __global__ void __launch_bounds__(CAL_THREADS) calib_mfma_kernel(int64_t iters, float* sink,
@@ -113,7 +115,7 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_mfma_kernel(int64_t iters, 
 #pragma unroll
     for (int c = 0; c < CAL_CHAINS; ++c) total += (float)acc[c][lane & 3];
   }
-  sink[(int64_t)blockIdx.x * CAL_THREADS + threadIdx.x] = total;
+  if (lane == 0) sink[(int64_t)blockIdx.x * (CAL_THREADS / 64) + (threadIdx.x >> 6)] = total;
   if (threadIdx.x == 0) {
     const uint64_t c1 = __builtin_amdgcn_s_memtime();
     const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
@@ -123,6 +125,13 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_mfma_kernel(int64_t iters, 
     st[2] = r0;
     st[3] = r1;
   }
+}
+
+// One wave that returns once `ticks` of the 100 MHz constant clock have
+// passed since it started (bounded by the caller to one second).
+__global__ void __launch_bounds__(64) calib_spin_kernel(uint64_t ticks) {
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  while (__builtin_amdgcn_s_memrealtime() - t0 < ticks) __builtin_amdgcn_s_sleep(8);
 }
 
 }  // namespace nf
@@ -212,8 +221,8 @@ nf_status nf_calib_mfma(int32_t dtype, int64_t iters, void* d_sink, void* stream
   if (iters < 1 || iters > ((int64_t)1 << 30)) return cfail(NF_EINVAL, "iters out of range");
   const int ncu = device_cus();
   if (ncu <= 0) return cfail(NF_EDEVICE, "no usable HIP device");
-  const int grid = nf::CAL_MFMA_WG * ncu;
-  const int64_t sink_floats = (int64_t)grid * nf::CAL_THREADS;
+  const int grid = (dtype == NF_F64 ? nf::CAL_MFMA_WG64 : nf::CAL_MFMA_WG32) * ncu;
+  const int64_t sink_floats = (int64_t)grid * (nf::CAL_THREADS / 64);
   const int64_t need = sink_floats * 4 + (int64_t)grid * 32;
   if (need > NF_CALIB_SINK_BYTES) return cfail(NF_ESHAPE, "sink too small for this device");
   float* sink = static_cast<float*>(d_sink);
@@ -245,6 +254,18 @@ nf_status nf_calib_mfma(int32_t dtype, int64_t iters, void* d_sink, void* stream
     }
   }
   *host_clock_ghz = used ? sum / used : 0.0;
+  return NF_OK;
+}
+
+nf_status nf_calib_spin(void* stream, double us) {
+  nf::set_error_message("");
+  if (!(us >= 0.0 && us <= 1e6)) return cfail(NF_EINVAL, "us must be in 0 .. 1e6");
+  const hipError_t e = nf::launch_k(nf::calib_spin_kernel, dim3(1), dim3(64), 0,
+                                    static_cast<hipStream_t>(stream), (uint64_t)(us * 100.0));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return cfail(NF_EDEVICE, std::string("spin kernel: ") + hipGetErrorString(e));
+  }
   return NF_OK;
 }
 

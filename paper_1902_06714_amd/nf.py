@@ -114,6 +114,7 @@ _sig = {
                                      ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_double)]),
+    "nf_calib_spin": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_double]),
     "nf_last_error": (ctypes.c_char_p, []),
 }
 for _name, (_res, _args) in _sig.items():
@@ -374,6 +375,11 @@ def nf_calib_mfma(dtype: int, iters: int, sink, stream=None):
     _check(_lib.nf_calib_mfma(dtype, iters, sink.data_ptr(), _stream(stream), ctypes.byref(ms),
                               ctypes.byref(fl), ctypes.byref(ghz)), "nf_calib_mfma")
     return ms.value, fl.value, ghz.value
+
+
+def nf_calib_spin(us: float, stream=None) -> None:
+    """Hold the stream for `us` microseconds (returns at once)."""
+    _check(_lib.nf_calib_spin(_stream(stream), float(us)), "nf_calib_spin")
 
 
 def nf_last_error() -> str:

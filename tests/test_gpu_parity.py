@@ -310,8 +310,10 @@ FAMILIES = {"narrow": (len(SAT_Z), 1, 1), "medium": (len(SAT_Z), 2, 2),
 def _fprime_case(act, family, hidden):
     """A two-layer network whose pre-activations z of the tested layer are
     exactly SAT_Z (the rest of a wide layer at z = 0.25), with x = e_1.
-    hidden: layer 1 holds z (z_1 = W_1 x, W_2 = 0.05, sigmoid output, y = 0),
-    so the bias tendency of layer 1 is 0.05 delta_2 f'(z_1) per sample;
+    hidden: layer 1 holds z (z_1 = W_1 x, W_2 = 2^-10, a sigmoid output whose
+    bias cancels the weighted sum, so z_2 is about 0, where sigma' is flat,
+    and y = 1.5), so the bias tendency of layer 1 is 2^-10 delta_2 f'(z_1) per
+    sample with delta_2 close to -1/4 and insensitive to the rounding of z_2;
     otherwise layer 2 holds z (W_2 = 0, b_2 = z) and the target is
     fp32(f(z)) + 1, so the bias tendency of layer 2 is (f(z) - y) f'(z) with
     f(z) - y close to -1."""
@@ -323,8 +325,10 @@ def _fprime_case(act, family, hidden):
         dims, acts = (d0, n, 1), (act, "sigmoid")
         W1 = np.zeros((n, d0))
         W1[:, 0] = z
-        parts = [W1.ravel(), np.zeros(n), np.full(n, 0.05), np.zeros(1)]
-        Y = np.zeros((batch, 1))
+        w2 = np.float32(2.0 ** -10)
+        b2 = -float(w2) * float(np.sum(mlp.act(act, z.astype(np.float32))))
+        parts = [W1.ravel(), np.zeros(n), np.full(n, w2), np.array([b2])]
+        Y = np.full((batch, 1), 1.5)
     else:
         dims, acts = (d0, 1, n), ("sigmoid", act)
         parts = [np.zeros(d0), np.zeros(1), np.zeros(n), z]
