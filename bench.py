@@ -20,8 +20,9 @@ run back to back as in the timed region.  `roofline` is the
 kernel with the most time per step, its achieved rate being the compulsory
 bytes (inputs, targets and parameters read once, parameters written once:
 per sample d_0 + d_L elements, per SGD step twice the parameter count) or
-the flops of its launches over its average duration; `step_roofline` does
-the same for the whole step.  `wide` repeats the measurement on the widest
+the flops of its launches over its average share of the timed step (its own
+duration, run_avg_us, scaled so that the kernels of a step add up to the
+measured step time); `step_roofline` does the same for the whole step.  `wide` repeats the measurement on the widest
 workload (4096^4-10 by default), the matrix-core half of the metric, with
 its own CPU-reference timing.  `peaks_measured` holds the device's streaming
 read and copy rates and its matrix-core loop rate, beside the published
@@ -303,10 +304,19 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
             f"{k['bytes'] / k['launches'] / 1e6:11.6f} MB/launch  "
             f"{k['flops'] / k['launches'] / 1e9:9.4f} GFLOP/launch")
 
+    # a launch timed by its own dispatch runs from its first wave to its
+    # last; in the timed steps the launches also share the gaps between them.
+    # Each kernel is charged its own duration scaled so that the kernels of a
+    # step add up to the measured step (its share of the step), which is what
+    # the roofline divides by; the unscaled duration is reported beside it
+    busy_ms = sum(k["total_ms"] for k in stats) / res["profiled_steps"]
+    in_step = (res["ms"] / steps) / busy_ms if busy_ms > 0 else 1.0
+
     def roofline(k):
-        """Roofline of one timed kernel over its average launch time: the
+        """Roofline of one timed kernel over its share of the step: the
         compulsory bytes its launches carry, or its flops above the ridge."""
-        avg_s = k["total_ms"] / k["launches"] / 1e3
+        run_s = k["total_ms"] / k["launches"] / 1e3
+        avg_s = run_s * in_step
         design_b = k["bytes"] / k["launches"]
         flops_l = k["flops"] / k["launches"]
         per_step = k["launches"] / res["profiled_steps"]
@@ -325,8 +335,9 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
         r["traffic"] = read_traffic(k["name"], w.name + ("_f64" if f64 else ""), sha)
         r["kernel"] = k["name"]
         r["avg_us"] = avg_s * 1e6
-        r["min_us"] = k["min_ms"] * 1e3
-        r["max_us"] = k["max_ms"] * 1e3
+        r["run_avg_us"] = run_s * 1e6
+        r["run_min_us"] = k["min_ms"] * 1e3
+        r["run_max_us"] = k["max_ms"] * 1e3
         r["launches_per_step"] = per_step
         r["launches_timed"] = k["launches"]
         r["bytes_per_launch"] = comp
@@ -349,8 +360,8 @@ def summarize(w, f64: bool, res, steps: int, sha: str, log):
         ach = step_flops / (ms_step / 1e3) / 1e12
         step_roof = {"bound": "mfma", "achieved": ach, "peak": mfma_peak, "unit": "TFLOP/s",
                      "frac": ach / mfma_peak, "flops_per_step": step_flops}
-    psteps = res["profiled_steps"]
-    step_roof["kernel_busy_ms_per_step"] = sum(k["total_ms"] for k in stats) / psteps
+    step_roof["kernel_run_ms_per_step"] = busy_ms
+    step_roof["in_step_scale"] = in_step
     step_roof["profiled_ms_per_step"] = res["profiled_ms_per_step"]
     per_step = res["per_step"]
     out = {
