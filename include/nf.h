@@ -153,6 +153,29 @@ nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out,
 nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_t batch,
                          float eta, int32_t n_shards, void* stream);
 
+/* nf_train_batch for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * The same step, bit for bit, with the per-sample buffers and the tendency
+ * pieces placed in a scratch array that the library holds on each device
+ * (NF_NOALLOC_SCRATCH_BYTES, a device variable of the library: the runtime
+ * maps it with the library's code on that device, and it stays until the
+ * process ends) instead of the net's own workspace; the call allocates
+ * nothing (no hipMalloc or hipFree, no memset node: the array is cleared by
+ * a kernel) and leaves the net's own workspace as it was.  fp32 nets only.
+ * Errors as nf_train_batch, plus NF_ESHAPE (nothing enqueued, the net
+ * unchanged) when the step needs more than NF_NOALLOC_SCRATCH_BYTES: about
+ * 3 * batch * (sum of the layer widths, each rounded up to 4; 32 for
+ * networks of at most 32 units per layer) floats of per-sample buffers, plus
+ * the tendency pieces of sharded or split batches.  Every such call on a
+ * device uses the same array and starts by clearing what it needs: calls
+ * that can overlap on one device (different streams, or threads) race and
+ * must be ordered by the caller.  The step's f'(z) is not kept afterwards
+ * (nf_get_fprime reports none), and nf_profile recording is suspended for
+ * the call. */
+#define NF_NOALLOC_SCRATCH_BYTES (48 << 20)
+nf_status nf_train_batch_noalloc(nf_net* net, const float* d_x, const float* d_y, int64_t batch,
+                                 float eta, int32_t n_shards, void* stream);
+
 /* Consecutive mini-batches: samples [t*batch, (t+1)*batch) for
  * t = 0 .. n_samples/batch - 1, one nf_train_batch step each, in order
  * (the epoch loop of section 4 without the random window).  n_samples must be

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <exception>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -110,6 +111,9 @@ struct nf_net {
   // samples whose f'(z_l), l < L, the last training step left in fbuf (0 when
   // that step kept f' in registers, or the workspace has been replaced since)
   int64_t stash_batch = 0;
+  // true while a step runs on the shared scratch (nf_train_batch_noalloc):
+  // the workspace pointers then point into it and nothing may be allocated
+  bool borrowed = false;
   // per-kernel timing (nf_profile)
   struct Rec {
     const char* name;
@@ -156,26 +160,51 @@ void free_ws(nf_net* n) {
   n->dbuf.assign(n->dims.size(), nullptr);
 }
 
-// Make room for `batch` samples.  Growing waits for the net's earlier work,
-// which may still read the old buffers.
-nf_status ensure_ws(nf_net* n, int64_t batch) {
-  if (batch <= n->ws_batch) return NF_OK;
-  nf_status st = sync_net(n);
-  if (st != NF_OK) return st;
+// The per-sample workspace of `batch` samples: for l < L, f(z_l) and f'(z_l),
+// and delta_l for every l, each [batch][lda_l], at the element offsets
+// written to aoff/foff/doff (-1 where a layer has none).  Returns the total.
+int64_t ws_layout(const nf_net* n, int64_t batch, std::vector<int64_t>* aoff,
+                  std::vector<int64_t>* foff, std::vector<int64_t>* doff) {
   const int L = num_layers(n);
+  aoff->assign(L + 1, -1);
+  foff->assign(L + 1, -1);
+  doff->assign(L + 1, -1);
   int64_t total = 0;
-  std::vector<int64_t> aoff(L + 1, -1), foff(L + 1, -1), doff(L + 1, -1);
   for (int l = 1; l <= L; ++l) {
     const int64_t sz = round_up(batch * n->layers[l].lda, kAlign);
     if (l < L) {
-      aoff[l] = total;
+      (*aoff)[l] = total;
       total += sz;
-      foff[l] = total;
+      (*foff)[l] = total;
       total += sz;
     }
-    doff[l] = total;
+    (*doff)[l] = total;
     total += sz;
   }
+  return total;
+}
+
+// points the net's per-sample buffers at base (element offsets as above)
+void ws_assign(nf_net* n, char* base, const std::vector<int64_t>& aoff,
+               const std::vector<int64_t>& foff, const std::vector<int64_t>& doff) {
+  const int L = num_layers(n);
+  for (int l = 1; l <= L; ++l) {
+    n->actv[l] = aoff[l] >= 0 ? base + aoff[l] * n->esz : nullptr;
+    n->fbuf[l] = foff[l] >= 0 ? base + foff[l] * n->esz : nullptr;
+    n->dbuf[l] = base + doff[l] * n->esz;
+  }
+}
+
+// Make room for `batch` samples.  Growing waits for the net's earlier work,
+// which may still read the old buffers.  A net borrowing the shared scratch
+// (nf_train_batch_noalloc) never grows: its room was checked beforehand.
+nf_status ensure_ws(nf_net* n, int64_t batch) {
+  if (batch <= n->ws_batch) return NF_OK;
+  if (n->borrowed) return fail(NF_EINVAL, "internal: the scratch workspace is too small");
+  nf_status st = sync_net(n);
+  if (st != NF_OK) return st;
+  std::vector<int64_t> aoff, foff, doff;
+  const int64_t total = ws_layout(n, batch, &aoff, &foff, &doff);
   void* buf = nullptr;
   hipError_t e = hipMalloc(&buf, (size_t)total * n->esz);
   if (e != hipSuccess) {
@@ -191,17 +220,13 @@ nf_status ensure_ws(nf_net* n, int64_t batch) {
   free_ws(n);
   n->ws = buf;
   n->ws_batch = batch;
-  char* base = static_cast<char*>(buf);
-  for (int l = 1; l <= L; ++l) {
-    n->actv[l] = aoff[l] >= 0 ? base + aoff[l] * n->esz : nullptr;
-    n->fbuf[l] = foff[l] >= 0 ? base + foff[l] * n->esz : nullptr;
-    n->dbuf[l] = base + doff[l] * n->esz;
-  }
+  ws_assign(n, static_cast<char*>(buf), aoff, foff, doff);
   return NF_OK;
 }
 
 nf_status ensure_partial(nf_net* n, int64_t elems) {
   if (elems <= n->partial_elems) return NF_OK;
+  if (n->borrowed) return fail(NF_EINVAL, "internal: the scratch piece buffer is too small");
   nf_status st = sync_net(n);
   if (st != NF_OK) return st;
   void* buf = nullptr;
@@ -306,6 +331,57 @@ nf_status launch(nf_net* n, int epi, bool akc, bool bkc, bool av, bool bv, int n
                [&] { return nf::launch_gemm<T>(epi, tile, akc, bkc, av, bv, nsplit, p, s); });
 }
 
+// The cut of a forward contraction (M samples, N units, K inputs) over its
+// k range: one piece unless the 64 x 64 tile grid is under twice the CU count
+// and K >= 256 (general nets take it only when the grid would use the
+// 64 x 64 tile anyway).  Pieces start on whole 16-input stages, so a vector
+// load never reaches into the next piece and every piece start stays 16-byte
+// aligned (nf_split.h).
+nf::KSplit fwd_split(const nf_net* n, int64_t M, int64_t N, int64_t K, bool small_tile_only) {
+  const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  const int64_t want = 2 * (int64_t)(n->ncu > 0 ? n->ncu : 256);
+  if ((small_tile_only && pick_tile(M, N, 1) != nf::TILE_64x64) || tiles >= want || K < 256)
+    return nf::KSplit{1, (int)K};
+  const int64_t nsplit = std::min<int64_t>({(want + tiles - 1) / tiles, K / 128, 16});
+  return nf::k_split(K, nsplit);
+}
+
+// elements of the pieces of a forward contraction cut into nsplit pieces
+int64_t fwd_piece_elems(int64_t M, int64_t N, int nsplit) {
+  return nsplit <= 1 ? 0 : nsplit * round_up(M * round_up(N, 4), kAlign);
+}
+
+// The tendency pieces of a step: each layer whose batch is split (shards, or
+// sub-pieces when the tile grid alone would leave most compute units idle)
+// gets a region of the piece buffer, the weights' pieces [pieces][d_l][ldw_l]
+// followed by the biases' pieces.  Returns the elements of all the regions.
+struct DwPiece {
+  int l, nsub;
+  int64_t pstride, off;                  // weights' pitch per piece, region offset
+};
+
+int64_t dw_plan(const nf_net* n, int64_t batch, int shards, std::vector<DwPiece>* pieces) {
+  const int L = num_layers(n);
+  const int64_t shard_len = batch / shards;
+  int64_t total = 0;
+  pieces->clear();
+  for (int l = L; l >= 1; --l) {
+    const LayerLayout& ly = n->layers[l];
+    const int64_t M = ly.out, N = ly.in;
+    int nsub = 1;
+    const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    while (tiles * shards * nsub < 256 && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
+           (int64_t)shards * nsub * 2 <= 65535)
+      nsub *= 2;
+    if (shards * nsub == 1) continue;
+    const int64_t pstride = round_up(M * ly.ldw, kAlign);
+    const int64_t nsplit = (int64_t)shards * nsub;
+    pieces->push_back({l, nsub, pstride, total});
+    total += round_up(nsplit * (pstride + round_up(M, kAlign)), kAlign);
+  }
+  return total;
+}
+
 // Forward propagation of `batch` samples through every layer (section 3.2).
 // train: keep f(z_l) and f'(z_l) for back-propagation and finish with the
 // output delta; otherwise write f(z_L) to `out`.
@@ -355,22 +431,13 @@ nf_status run_forward(nf_net* n, const T* x, const T* y, int64_t batch, T* out, 
     // A contraction with too few 64 x 64 tiles to fill the chip and a long k
     // range is split over the k range; a fold adds the pieces in order and
     // applies the epilogue.
-    const int64_t tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
-    const int64_t want = 2 * (int64_t)(n->ncu > 0 ? n->ncu : 256);
-    int nsplit = 1;
-    if (pick_tile(p.M, p.N, 1) == nf::TILE_64x64 && tiles < want && p.K >= 256) {
-      nsplit = (int)std::min<int64_t>({(want + tiles - 1) / tiles, p.K / 128, 16});
-    }
+    const nf::KSplit ks = fwd_split(n, p.M, p.N, p.K, true);
+    int nsplit = ks.nsplit;
     nf_status st;
     if (nsplit <= 1) {
       st = launch<T>(n, epi, true, true, av, true, 1, p, s);
     } else {
-      // pieces start on whole 16-input stages, so a vector load never
-      // reaches into the next piece and every piece start stays 16-byte
-      // aligned (nf_split.h)
-      const nf::KSplit ks = nf::k_split(p.K, nsplit);
       const int sub_len = ks.sub_len;
-      nsplit = ks.nsplit;
       const int64_t ldp = round_up(p.N, 4);
       const int64_t pstride = round_up((int64_t)p.M * ldp, kAlign);
       st = ensure_partial(n, nsplit * pstride);
@@ -429,26 +496,9 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
   // after every layer's pieces are in.  Each layer's pieces get their own
   // region of the workspace, so the piece kernels of several layers share a
   // launch and one fold serves them all.
-  struct Piece {
-    int l, nsub;
-    int64_t pstride, off;                  // weights' pitch per piece, region offset
-  };
+  using Piece = DwPiece;
   std::vector<Piece> pieces;
-  int64_t total = 0;
-  for (int l = L; l >= 1; --l) {
-    const LayerLayout& ly = n->layers[l];
-    const int64_t M = ly.out, N = ly.in;
-    int nsub = 1;
-    const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    while (tiles * shards * nsub < 256 && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
-           (int64_t)shards * nsub * 2 <= 65535)
-      nsub *= 2;
-    if (shards * nsub == 1) continue;
-    const int64_t pstride = round_up(M * ly.ldw, kAlign);
-    const int64_t nsplit = (int64_t)shards * nsub;
-    pieces.push_back({l, nsub, pstride, total});
-    total += round_up(nsplit * (pstride + round_up(M, kAlign)), kAlign);
-  }
+  const int64_t total = dw_plan(n, batch, shards, &pieces);
   if (total > 0) {
     nf_status st = ensure_partial(n, total);
     if (st != NF_OK) return st;
@@ -758,15 +808,9 @@ nf_status medium_forward_deltas(nf_net* n, const T* x, const T* y, int64_t batch
   p.M = (int)batch;
   p.N = l1.out;
   p.K = l1.in;
-  const int64_t tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
-  const int64_t want = 2 * (int64_t)(n->ncu > 0 ? n->ncu : 256);
-  int nsplit = 1;
-  if (tiles < want && p.K >= 256)
-    nsplit = (int)std::min<int64_t>({(want + tiles - 1) / tiles, p.K / 128, 16});
-  // pieces start on whole 16-input stages (nf_split.h)
-  const nf::KSplit ks = nf::k_split(p.K, nsplit);
+  const nf::KSplit ks = fwd_split(n, p.M, p.N, p.K, false);
   const int sub_len = ks.sub_len;
-  nsplit = ks.nsplit;
+  const int nsplit = ks.nsplit;
   const int64_t ldz = round_up(p.N, 4);
   const int64_t zstride = round_up((int64_t)p.M * ldz, kAlign);
   nf_status st = ensure_partial(n, nsplit * zstride);
@@ -1099,6 +1143,134 @@ nf_status train_batch(nf_net* net, const T* d_x, const T* d_y, int64_t batch, do
   });
 }
 
+// ---------------------------------------------------------------------------
+// the training step on the shared scratch array (nf_train_batch_noalloc)
+// ---------------------------------------------------------------------------
+// The most the piece buffer is asked for by one training step of `batch`
+// samples in `shards` shards: the forward pieces (consumed before the
+// backward pass starts) or the tendency pieces, whichever is larger.
+template <class T>
+int64_t partial_need(const nf_net* n, const T* x, int64_t batch, int shards) {
+  if (shards == 1 && narrow_rows_ok<T>(n, x)) return 0;
+  std::vector<DwPiece> pieces;
+  int64_t need = dw_plan(n, batch, shards, &pieces);
+  nf::MediumParamsT<T> mp{};
+  if (medium_layout<T>(n, batch, &mp)) {
+    // the medium path always writes layer 1 as pieces, one or more
+    const LayerLayout& l1 = n->layers[1];
+    const nf::KSplit ks = fwd_split(n, batch, l1.out, l1.in, false);
+    need = std::max(need, ks.nsplit * round_up(batch * round_up(l1.out, 4), kAlign));
+  } else {
+    for (int l = 1; l <= num_layers(n); ++l) {
+      const LayerLayout& ly = n->layers[l];
+      const nf::KSplit ks = fwd_split(n, batch, ly.out, ly.in, true);
+      need = std::max(need, fwd_piece_elems(batch, ly.out, ks.nsplit));
+    }
+  }
+  return need;
+}
+
+}  // namespace
+
+namespace nf {
+// clears n16 16-byte units at p (the workspace's row padding must read as
+// zero; a kernel, not hipMemsetAsync, so that the call can be captured)
+__global__ void __launch_bounds__(256) zero16_kernel(float4* p, int64_t n16) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride)
+    p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+}  // namespace nf
+
+// The scratch memory of nf_train_batch_noalloc: one array per device, shared
+// by every such call on that device.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[NF_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// the device address of the scratch array on device dev, which is current
+nf_status scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(NF_EDEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* a = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return hip_fail(e, "hipGetSymbolAddress of the scratch array");
+    }
+    g_scratch_addr[dev] = a;
+  }
+  *out = g_scratch_addr[dev];
+  return NF_OK;
+}
+
+// One nf_train_batch step whose per-sample buffers and piece buffer are carved
+// out of the scratch array: the net's own workspace is set aside for the call
+// and restored after it, and nothing is allocated.
+nf_status train_batch_noalloc(nf_net* net, const float* d_x, const float* d_y, int64_t batch,
+                              double eta, int32_t n_shards, void* stream) {
+  return guarded([&]() -> nf_status {
+    nf_status st = check_net_t<float>(net);
+    if (st != NF_OK) return st;
+    st = check_train_args(d_x, d_y, batch, eta, n_shards);
+    if (st != NF_OK) return st;
+    DeviceGuard g(net->device);
+    if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
+    void* base = nullptr;
+    st = scratch_address(net->device, &base);
+    if (st != NF_OK) return st;
+    std::vector<int64_t> aoff, foff, doff;
+    const int64_t ws = round_up(ws_layout(net, batch, &aoff, &foff, &doff), kAlign);
+    const int64_t part = partial_need<float>(net, d_x, batch, n_shards);
+    const double need = (double)(ws + part) * (double)net->esz;
+    if (need > (double)NF_NOALLOC_SCRATCH_BYTES)
+      return fail(NF_ESHAPE, "this step needs " + std::to_string((int64_t)need) +
+                                 " bytes of scratch; nf_train_batch_noalloc has " +
+                                 std::to_string((int64_t)NF_NOALLOC_SCRATCH_BYTES));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* sbase = static_cast<char*>(base);
+    // the per-sample buffers' row padding must read as zero, and the array
+    // holds whatever the last call left there
+    hipError_t e = nf::launch_k(nf::zero16_kernel, dim3(1024), dim3(256), 0, s,
+                                reinterpret_cast<float4*>(sbase),
+                                ws * (int64_t)net->esz / 16);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return hip_fail(e, "kernel launch");
+    }
+    // set the net's own buffers aside for the call
+    const std::vector<void*> actv = net->actv, fbuf = net->fbuf, dbuf = net->dbuf;
+    const int64_t ws_batch = net->ws_batch, partial_elems = net->partial_elems;
+    void* partial = net->partial;
+    const int prof = net->prof;
+    ws_assign(net, sbase, aoff, foff, doff);
+    net->ws_batch = batch;
+    net->partial = sbase + ws * (int64_t)net->esz;
+    net->partial_elems = part;
+    net->borrowed = true;
+    net->prof = 0;
+    st = train_step<float>(net, d_x, d_y, batch, eta, n_shards, s);
+    net->actv = actv;
+    net->fbuf = fbuf;
+    net->dbuf = dbuf;
+    net->ws_batch = ws_batch;
+    net->partial = partial;
+    net->partial_elems = partial_elems;
+    net->borrowed = false;
+    net->prof = prof;
+    net->stash_batch = 0;   // the stash lived in the shared array
+    net->last = s;
+    net->used = true;
+    return st;
+  });
+}
+
 template <class T>
 nf_status train_epoch(nf_net* net, const T* d_x, const T* d_y, int64_t n_samples, int64_t batch,
                       double eta, int32_t n_shards, void* stream) {
@@ -1425,6 +1597,10 @@ nf_status nf_forward(nf_net* net, const float* d_x, int64_t batch, float* d_out,
 nf_status nf_train_batch(nf_net* net, const float* d_x, const float* d_y, int64_t batch, float eta,
                          int32_t n_shards, void* stream) {
   return train_batch<float>(net, d_x, d_y, batch, (double)eta, n_shards, stream);
+}
+nf_status nf_train_batch_noalloc(nf_net* net, const float* d_x, const float* d_y, int64_t batch,
+                                 float eta, int32_t n_shards, void* stream) {
+  return train_batch_noalloc(net, d_x, d_y, batch, eta, n_shards, stream);
 }
 nf_status nf_train_epoch(nf_net* net, const float* d_x, const float* d_y, int64_t n_samples,
                          int64_t batch, float eta, int32_t n_shards, void* stream) {

@@ -69,6 +69,9 @@ _sig = {
                                   ctypes.c_void_p]),
     "nf_train_batch": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_float, ctypes.c_int32, ctypes.c_void_p]),
+    "nf_train_batch_noalloc": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int64, ctypes.c_float, ctypes.c_int32,
+                                              ctypes.c_void_p]),
     "nf_train_epoch": (ctypes.c_int, [_net_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_float, ctypes.c_int32,
                                       ctypes.c_void_p]),
@@ -230,6 +233,16 @@ def nf_forward(net, x, out, stream=None) -> None:
 def nf_train_batch(net, x, y, eta: float, n_shards: int = 1, stream=None) -> None:
     _check(_lib.nf_train_batch(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0], float(eta),
                                int(n_shards), _stream(stream)), "nf_train_batch")
+
+
+NF_NOALLOC_SCRATCH_BYTES = 48 << 20
+
+
+def nf_train_batch_noalloc(net, x, y, eta: float, n_shards: int = 1, stream=None) -> None:
+    """nf_train_batch on the library's scratch array (allocates nothing)."""
+    _check(_lib.nf_train_batch_noalloc(net, _dev_ptr(x, "x"), _dev_ptr(y, "y"), x.shape[0],
+                                       float(eta), int(n_shards), _stream(stream)),
+           "nf_train_batch_noalloc")
 
 
 def nf_train_epoch(net, x, y, batch: int, eta: float, n_shards: int = 1, stream=None) -> None:
