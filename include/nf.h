@@ -290,7 +290,8 @@ nf_status nf_profile_read(nf_net* net, nf_kernel_stat* out, int32_t cap, int32_t
  * least NF_CALIB_SINK_BYTES bytes.
  * nf_calib_copy: the same access pattern copying d_src to d_dst.
  * nf_calib_mfma: a loop of independent matrix-core instructions, `iters`
- * rounds of 8 per wave on 2 (fp32) or 4 (fp64) workgroups of 4 waves per compute unit
+ * (rounded up to a multiple of 8) rounds of 8 per wave on 2 (fp32) or 4
+ * (fp64) workgroups of 4 waves per compute unit
  * (v_mfma_f32_32x32x2f32 for dtype NF_F32, v_mfma_f64_16x16x4f64 for
  * NF_F64); *host_flops receives the flops it performed (2 per multiply-add)
  * and *host_clock_ghz the mean shader clock of its waves, from the shader

@@ -106,6 +106,12 @@ struct nf_net {
   // narrow nets: offset of a zero block (NARROW_WIDTH^2 weights, then
   // NARROW_WIDTH biases) that stands in for the layers past the last one
   int64_t zero_off = 0;
+  // fp32 narrow nets: W_1 packed in the per-sample kernels' operand layouts
+  // (W1f, then W1i; see NarrowFwdParamsT), valid for the parameters of
+  // version packver; pver counts every change of the current parameters
+  void* w1pack = nullptr;
+  int64_t w1f_elems = 0;
+  uint64_t pver = 1, packver = 0;
   hipStream_t last = nullptr;
   bool used = false;
   // samples whose f'(z_l), l < L, the last training step left in fbuf (0 when
@@ -148,6 +154,18 @@ nf_status sync_net(nf_net* n) {
   hipError_t e = hipStreamSynchronize(n->last);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   return NF_OK;
+}
+
+// the parameter buffers, the tendencies and the packed copies of W_1
+void free_params(nf_net* n) {
+  for (void*& b : n->pbuf) {
+    if (b) (void)hipFree(b);
+    b = nullptr;
+  }
+  if (n->grads) (void)hipFree(n->grads);
+  if (n->w1pack) (void)hipFree(n->w1pack);
+  n->grads = nullptr;
+  n->w1pack = nullptr;
 }
 
 void free_ws(nf_net* n) {
@@ -681,7 +699,27 @@ nf::NarrowFwdParamsT<T> narrow_fwd_params(const nf_net* n, const T* x, const T* 
   p.dout = n->dims[L];
   p.out = out;
   p.ncu = n->ncu;
+  if constexpr (sizeof(T) == 4) {
+    p.W1f = as<T>(n->w1pack);
+    p.W1i = as<T>(n->w1pack) + n->w1f_elems;
+  }
   return p;
+}
+
+// The packed copies of W_1 for the current parameters (fp32 narrow nets):
+// rewritten from W_1 unless the last step's SGD kernel wrote them
+nf_status ensure_packed(nf_net* n, hipStream_t s) {
+  if (!n->w1pack || n->packver == n->pver) return NF_OK;
+  const LayerLayout& l1 = n->layers[1];
+  float* P = cur_params<float>(n);
+  float* W1f = as<float>(n->w1pack);
+  nf_status st = timed(n, "narrow_pack_w1", 8.0 * (double)(n->w1f_elems + nf::narrow_pack_w1i_elems(l1.in)),
+                       0.0, s, [&] {
+                         return nf::launch_narrow_pack_w1(P + l1.w_off, l1.ldw, l1.out, l1.in, W1f,
+                                                          W1f + n->w1f_elems, s);
+                       });
+  if (st == NF_OK) n->packver = n->pver;
+  return st;
 }
 
 // Algorithmic work of the per-sample pass: inputs, targets and weights read,
@@ -713,9 +751,12 @@ nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, do
   narrow_fwd_work(n, batch, true, &by, &fl);
   const nf::NarrowFwdParamsT<T> fp = narrow_fwd_params<T>(n, x, y, batch, nullptr);
   nf_status st;
-  if constexpr (sizeof(T) == 4)
+  if constexpr (sizeof(T) == 4) {
+    st = ensure_packed(n, s);
+    if (st != NF_OK) return st;
     st = timed(n, nf::narrow_fwd_name(true, fp), by, fl, s,
                [&] { return nf::launch_narrow_fwd(true, fp, s); });
+  }
   else
     st = timed(n, nf::narrow64_fwd_name(true, fp), by, fl, s,
                [&] { return nf::launch_narrow64_fwd(true, fp, s); });
@@ -753,6 +794,10 @@ nf_status narrow_train_step(nf_net* n, const T* x, const T* y, int64_t batch, do
   }
   for (int l = L; l <= nf::NARROW_MAX_LAYERS; ++l) dp.tile_base[l] = base;
   dp.ntiles = base;
+  if constexpr (sizeof(T) == 4) {
+    dp.W1f = as<T>(n->w1pack);
+    dp.W1i = as<T>(n->w1pack) + n->w1f_elems;
+  }
   if constexpr (sizeof(T) == 4)
     return timed(n, "narrow_dw_sgd", dby, dfl, s, [&] { return nf::launch_narrow_dw(dp, s); });
   else
@@ -871,8 +916,13 @@ nf_status train_step(nf_net* n, const T* x, const T* y, int64_t batch, double et
   }
   n->stash_batch = (!narrow && !medium_layout<T>(n, batch, &mp) && st == NF_OK) ? batch : 0;
   // the updated parameters are in the other buffer from here on (a failed
-  // launch leaves the net in an undefined state, reported as NF_EDEVICE)
-  if (st == NF_OK) n->cur ^= 1;
+  // launch leaves the net in an undefined state, reported as NF_EDEVICE);
+  // the narrow step's SGD kernel has packed its W_1 as well
+  if (st == NF_OK) {
+    n->cur ^= 1;
+    ++n->pver;
+    if (narrow) n->packver = n->pver;
+  }
   return st;
 }
 
@@ -885,9 +935,12 @@ nf_status infer(nf_net* n, const T* x, int64_t batch, T* out, hipStream_t s) {
     double by, fl;
     narrow_fwd_work(n, batch, false, &by, &fl);
     const nf::NarrowFwdParamsT<T> fp = narrow_fwd_params<T>(n, x, nullptr, batch, out);
-    if constexpr (sizeof(T) == 4)
+    if constexpr (sizeof(T) == 4) {
+      st = ensure_packed(n, s);
+      if (st != NF_OK) return st;
       return timed(n, nf::narrow_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow_fwd(false, fp, s); });
+    }
     else
       return timed(n, nf::narrow64_fwd_name(false, fp), by, fl, s,
                    [&] { return nf::launch_narrow64_fwd(false, fp, s); });
@@ -1011,11 +1064,14 @@ nf_status create(const int32_t* dims, int32_t n_dims, const int32_t* acts, int32
   if (e == hipSuccess) e = hipMemset(n->pbuf[0], 0, bytes);
   if (e == hipSuccess) e = hipMemset(n->pbuf[1], 0, bytes);
   if (e == hipSuccess) e = hipMemset(n->grads, 0, bytes);
+  if (e == hipSuccess && n->narrow && n->dtype == nf::DT_F32) {
+    n->w1f_elems = nf::narrow_pack_w1f_elems(dims[0]);
+    const size_t pbytes = (size_t)(n->w1f_elems + nf::narrow_pack_w1i_elems(dims[0])) * sizeof(float);
+    e = hipMalloc(&n->w1pack, pbytes);
+  }
   if (e != hipSuccess) {
     (void)hipGetLastError();
-    if (n->pbuf[0]) (void)hipFree(n->pbuf[0]);
-    if (n->pbuf[1]) (void)hipFree(n->pbuf[1]);
-    if (n->grads) (void)hipFree(n->grads);
+    free_params(n);
     delete n;
     return fail(e == hipErrorOutOfMemory ? NF_ENOMEM : NF_EDEVICE,
                 std::string("device allocation failed: ") + hipGetErrorString(e));
@@ -1031,6 +1087,7 @@ nf_status copy_params(nf_net* n, void* dev, const void* host_src, void* host_dst
   if (!g.ok) return fail(NF_EDEVICE, "cannot select the net's device");
   nf_status st = sync_net(n);
   if (st != NF_OK) return st;
+  if (host_src) ++n->pver;   // the packed copies of W_1 no longer match
   const size_t es = n->esz;
   char* d = static_cast<char*>(dev);
   int64_t canon = 0;
@@ -1522,9 +1579,7 @@ nf_status load(const char* path, nf_net** out) {
   st = copy_params(n, n->pbuf[n->cur], buf.data() + pos, nullptr, np);
   if (st != NF_OK) {
     const std::string msg = g_err;
-    (void)hipFree(n->pbuf[0]);
-    (void)hipFree(n->pbuf[1]);
-    (void)hipFree(n->grads);
+    free_params(n);
     delete n;
     return fail(st, msg);
   }
@@ -1572,9 +1627,7 @@ nf_status nf_net_destroy(nf_net* net) {
     if (net->partial) (void)hipFree(net->partial);
     if (net->evalbuf) (void)hipFree(net->evalbuf);
     if (net->dcount) (void)hipFree(net->dcount);
-    if (net->pbuf[0]) (void)hipFree(net->pbuf[0]);
-    if (net->pbuf[1]) (void)hipFree(net->pbuf[1]);
-    if (net->grads) (void)hipFree(net->grads);
+    free_params(net);
     delete net;
     return st;
   });

@@ -74,6 +74,7 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_copy_kernel(float4* dst, co
 // (s_memtime) and the 100 MHz constant clock (s_memrealtime) at its start and
 // end, so the host can tell the clock the matrix cores ran at
 constexpr int CAL_CHAINS = 8;
+constexpr int CAL_GROUP = 8;     // rounds per loop trip; iters is rounded up to a multiple
 // workgroups of 4 waves per CU: two waves per SIMD for fp32 (128 accumulator
 // registers each), four for fp64 (64 each), whose chains need more in flight
 constexpr int CAL_MFMA_WG32 = 2, CAL_MFMA_WG64 = 4;
@@ -95,10 +96,14 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_mfma_kernel(int64_t iters, 
     for (int c = 0; c < CAL_CHAINS; ++c)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[c][v] = 0.0f;
-    for (int64_t it = 0; it < iters; ++it)
+    // whole groups of CAL_GROUP rounds per trip: the compiler moves the
+    // accumulators between register files at the loop's back edge
+    for (int64_t it = 0; it < iters; it += CAL_GROUP)
 #pragma unroll
-      for (int c = 0; c < CAL_CHAINS; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[c], 0, 0, 0);
+      for (int r = 0; r < CAL_GROUP; ++r)
+#pragma unroll
+        for (int c = 0; c < CAL_CHAINS; ++c)
+          acc[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[c], 0, 0, 0);
 #pragma unroll
     for (int c = 0; c < CAL_CHAINS; ++c) total += acc[c][lane & 15];
   } else {
@@ -108,10 +113,12 @@ __global__ void __launch_bounds__(CAL_THREADS) calib_mfma_kernel(int64_t iters, 
     for (int c = 0; c < CAL_CHAINS; ++c)
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc[c][v] = 0.0;
-    for (int64_t it = 0; it < iters; ++it)
+    for (int64_t it = 0; it < iters; it += CAL_GROUP)
 #pragma unroll
-      for (int c = 0; c < CAL_CHAINS; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc[c], 0, 0, 0);
+      for (int r = 0; r < CAL_GROUP; ++r)
+#pragma unroll
+        for (int c = 0; c < CAL_CHAINS; ++c)
+          acc[c] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc[c], 0, 0, 0);
 #pragma unroll
     for (int c = 0; c < CAL_CHAINS; ++c) total += (float)acc[c][lane & 3];
   }
@@ -219,6 +226,7 @@ nf_status nf_calib_mfma(int32_t dtype, int64_t iters, void* d_sink, void* stream
     return cfail(NF_EINVAL, "NULL pointer");
   if (dtype != NF_F32 && dtype != NF_F64) return cfail(NF_EINVAL, "unknown dtype");
   if (iters < 1 || iters > ((int64_t)1 << 30)) return cfail(NF_EINVAL, "iters out of range");
+  iters = (iters + nf::CAL_GROUP - 1) / nf::CAL_GROUP * nf::CAL_GROUP;
   const int ncu = device_cus();
   if (ncu <= 0) return cfail(NF_EDEVICE, "no usable HIP device");
   const int grid = (dtype == NF_F64 ? nf::CAL_MFMA_WG64 : nf::CAL_MFMA_WG32) * ncu;

@@ -186,6 +186,23 @@ constexpr unsigned NARROW_OOB = 0x40000000u;
 // is [NARROW_WIDTH][NARROW_WIDTH]; biases are NARROW_WIDTH long; rows, columns
 // and entries past the layer sizes are zero.  The per-sample kernel reads the
 // layers past the last one (up to NARROW_MAX_LAYERS) from a zero block.
+//
+// fp32 narrow nets also keep W_1 packed twice, in the register layouts the
+// matrix-core operands of the per-sample kernels take, so that each wave
+// reads its share of W_1 with 16-byte loads of 1 KiB contiguous per
+// instruction (the vector memory pipeline spends a fixed time per
+// instruction that grows with the rows it touches):
+//   W1f (4x4x1 operands): block (t, q) of 64 lanes x float4, t < ceil(d0 / 64),
+//       q < 8; lane 4 b + i holds W_1[4 q + i][64 t + 4 b .. 64 t + 4 b + 3];
+//   W1i (16x16x4 operands): block (c, h), c < ceil(d0 / 16), h < 2; lane
+//       r + 16 g holds W_1[16 h + r][16 c + 4 g .. 16 c + 4 g + 3];
+// blocks in index order, entries past d_1 or d_0 zero.  The SGD kernel
+// writes both with the updated W_1; after any other change of the
+// parameters the host rewrites them (narrow_pack_w1) before the next pass.
+constexpr int NARROW_PACK_W1F_BLOCK = 8 * 64 * 4;   // floats per step t (8 blocks)
+constexpr int NARROW_PACK_W1I_BLOCK = 2 * 64 * 4;   // floats per chunk c (2 blocks)
+inline int64_t narrow_pack_w1f_elems(int d0) { return (int64_t)((d0 + 63) / 64) * NARROW_PACK_W1F_BLOCK; }
+inline int64_t narrow_pack_w1i_elems(int d0) { return (int64_t)((d0 + 15) / 16) * NARROW_PACK_W1I_BLOCK; }
 template <class T>
 struct NarrowFwdParamsT {
   const T* X;                              // [B][d0], d0 % (16 / sizeof(T)) == 0, 16-byte aligned
@@ -201,6 +218,8 @@ struct NarrowFwdParamsT {
   T* D[NARROW_MAX_LAYERS];                 // delta_l [B][32], l = 1..L
   T* out;                                  // inference: f(z_L) [B][d_L]
   int ncu;                                 // compute units of the device
+  const T* W1f;                            // packed W_1 (fp32 only), see above
+  const T* W1i;
 };
 using NarrowFwdParams = NarrowFwdParamsT<float>;
 
@@ -222,6 +241,8 @@ struct NarrowDwParamsT {
                                            // ntiles for the layers past the last one
   int ntiles;                              // tiles of all layers
   T scale;
+  T* W1f;                                  // packed copies of the updated W_1 (fp32 only)
+  T* W1i;
 };
 using NarrowDwParams = NarrowDwParamsT<float>;
 
@@ -233,6 +254,10 @@ hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s
 // Name of the kernel launch_narrow_fwd picks for this pass.
 const char* narrow_fwd_name(bool train, const NarrowFwdParams& p);
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s);
+// Writes both packed copies of W_1 ([d1][ldw] fp32, rows and columns past
+// d1 and d0 taken as zero) into W1f and W1i.
+hipError_t launch_narrow_pack_w1(const float* W1, int64_t ldw, int d1, int d0, float* W1f,
+                                 float* W1i, hipStream_t s);
 
 // The fp64 counterparts (16-sample tiles for every batch; no persistent
 // inference kernel).  Input rows need an even width.

@@ -17,6 +17,8 @@
 //   the tendency and writes W' = W - (eta/B) G itself (into the other
 //   parameter buffer), so no workgroup waits on another.
 // The order of every sum is fixed, so results are reproducible bit for bit.
+#include <type_traits>
+
 #include "nf_act.h"
 #include "nf_internal.h"
 
@@ -28,6 +30,21 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // type itself is lowered through private memory)
 __device__ __forceinline__ float4 keep_if(bool c, float4 v) {
   return make_float4(c ? v.x : 0.0f, c ? v.y : 0.0f, c ? v.z : 0.0f, c ? v.w : 0.0f);
+}
+
+// The float4 of lane src_byte / 4, by one backward permute per dword.  The
+// vector memory pipeline takes a 16-byte load at full rate only when each
+// quad of lanes (4 consecutive lanes) reads 64 consecutive bytes; where the
+// lanes of a quad read four different rows, as the matrix-core operand
+// layouts would have them, it delivers about a third of that.  So inputs are
+// loaded quad-contiguous and moved across lanes to the operand layout.
+__device__ __forceinline__ float4 lane_permute4(int src_byte, float4 v) {
+  float4 o;
+  o.x = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src_byte, __builtin_bit_cast(int, v.x)));
+  o.y = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src_byte, __builtin_bit_cast(int, v.y)));
+  o.z = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src_byte, __builtin_bit_cast(int, v.z)));
+  o.w = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src_byte, __builtin_bit_cast(int, v.w)));
+  return o;
 }
 
 // A buffer offset past every range the narrow kernels read through buffer
@@ -382,20 +399,27 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
 
   {
     const int b = lane >> 2, q = lane & 3;
-    // the tile's input rows and W_1's d_1 rows through buffer resources that
-    // end at the last row: rows past the batch, W_1's padding rows and inputs
-    // past the width (given an offset past the end) read as zeros without a
-    // memory access, so no bytes go to loads whose values are not used
+    // the tile's input rows through a buffer resource that ends at the last
+    // row, and W_1 packed in this kernel's operand layout (W1f: lane 4 b + q
+    // of block (t, ug) holds W_1[4 ug + q][64 t + 4 b ..], one contiguous 1 KiB
+    // per instruction); rows past the batch, inputs past the width and steps
+    // past the last (given an offset past the end) read as zeros without a
+    // memory access, so no bytes go to loads whose values are not used.  The
+    // inputs are loaded with lane 16 qx + bx taking sample qx, inputs
+    // 64 t + 4 bx .. (each quad of lanes 64 consecutive bytes, which the vector
+    // memory pipeline takes at full rate) and moved to the operand layout
+    // (lane 4 b + q: sample q, inputs 64 t + 4 b ..) by a backward permute.
+    const int qx = lane >> 4, bx = lane & 15;
+    const int src_byte = 4 * (16 * q + b);
     const int nrows = p.B - s0 < T ? p.B - s0 : T;
     const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(p.X + (int64_t)s0 * p.d0), (short)0, nrows * p.d0 * 4, 0x00020000);
-    const int ldw1 = (int)p.ldw[0];
+    const int nsteps = (p.d0 + N4_KS - 1) / N4_KS;
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)p.W[0], (short)0, p.dims[1] * ldw1 * 4, 0x00020000);
+        (void*)p.W1f, (short)0, nsteps * NARROW_PACK_W1F_BLOCK * 4, 0x00020000);
     floatx4 acc[N4_UG];
 #pragma unroll
     for (int ug = 0; ug < N4_UG; ++ug) acc[ug] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int nsteps = (p.d0 + N4_KS - 1) / N4_KS;
     // workgroups start at different steps (rotated by the tile index), so the
     // workgroups that start together do not all ask for the same W_1 lines
     const int rot = (int)(blockIdx.x % (unsigned)nsteps);
@@ -409,19 +433,22 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
 #pragma unroll
       for (int u = 0; u < N4_PRE; ++u) {
         int t = t0 + u * N1_WAVES;
-        if (t < nsteps) t = t + rot < nsteps ? t + rot : t + rot - nsteps;
-        const int k = t * N4_KS + 4 * b;
-        const bool ok = k < p.d0;
+        const bool tin = t < nsteps;
+        if (tin) t = t + rot < nsteps ? t + rot : t + rot - nsteps;
+        const int kx = t * N4_KS + 4 * bx;
+        const bool okx = tin && kx < p.d0;
         xr[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
-                                               xres, ok ? 4 * (q * p.d0 + k) : (int)NB_OOB, 0, 0));
+                                               xres, okx ? 4 * (qx * p.d0 + kx) : (int)NB_OOB, 0, 0));
 #pragma unroll
         for (int ug = 0; ug < N4_UG; ++ug)
           wr[u][ug] = __builtin_bit_cast(
               float4, __builtin_amdgcn_raw_buffer_load_b128(
-                          wres, ok ? 4 * ((4 * ug + q) * ldw1 + k) : (int)NB_OOB, 0, 0));
+                          wres, tin ? 16 * ((t * 8 + ug) * 64 + lane) : (int)NB_OOB, 0, 0));
       }
       // keep every load of the block ahead of the first matrix instruction
       __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < N4_PRE; ++u) xr[u] = lane_permute4(src_byte, xr[u]);
 #pragma unroll
       for (int u = 0; u < N4_PRE; ++u) {
 #pragma unroll
@@ -468,33 +495,102 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_fwd4_kernel(const Narrow
   narrow_tail<TRAIN, T>(p, s0, tid, z1, ytg, hs, ws, wsT, sl.b);
 }
 
+// one of four per-layer arguments, picked by value (so that an argument load
+// does not wait on the index)
+template <class V>
+__device__ __forceinline__ V pick(int l, V a0, V a1, V a2, V a3) {
+  return l == 0 ? a0 : (l == 1 ? a1 : (l == 2 ? a2 : a3));
+}
+
 // ---------------------------------------------------------------------------
-// Inference over large batches.  One persistent workgroup per CU walks a
-// contiguous run of 16-sample tiles.  W_1 stays in registers for the whole
-// launch (wave w holds the 16-wide input chunks w, w + 8, ... of all 32 units),
-// so a CU reads it once instead of once per tile, and the inputs of the tile
-// two ahead are requested before the matrix work of the current one.  The
-// inputs are read through a buffer resource: rows past the batch and inputs
-// past the width come back as zeros without touching memory, so every load is
-// unconditional.  The waves' layer-1 sums are added in wave order and the tail
-// is that of the per-sample kernels, its outputs staged in LDS and written out
-// once per round of tiles: a global store inside the tile loop would make the
-// compiler wait for every outstanding load at the next use (stores and loads
-// share one wait counter), draining the loads of the tiles ahead.
+// Inference over large batches.  One persistent workgroup of 8 waves per CU
+// walks a contiguous, balanced run of 16-sample tiles; every wave does both
+// parts of the work.
+//
+// Layer 1: W_1 stays in the waves' registers for the whole launch, the wave
+// of chunk group q holding the 16-wide input chunks q, q + 8, ... of all 32
+// units (a CU reads W_1 once, from its packed copy in the operand layout, a
+// contiguous KiB per load, requested before any input: a CU keeps a bounded
+// number of loads in flight and they complete in order, so W_1 behind inputs
+// from HBM would arrive only at the inputs' pace); the groups are dealt to the waves rotated by
+// the workgroup index, so the workgroups that start together ask for
+// different lines of W_1 first.  Layer 1 runs as z^T = W_1 x^T on the
+// 16x16x4 matrix instruction, units as rows and samples as columns; each
+// wave leaves its partial sums of a tile in one of NI_NB LDS buffers and
+// counts them there.  The inputs of later tiles are requested before the
+// matrix work of the current one, through a buffer resource: rows past the
+// batch and inputs past the width come back as zeros without touching
+// memory, so every load is unconditional.
+//
+// The rest of the network, one tile behind: wave w takes samples 2w and
+// 2w + 1 of the tile, lane (s, u) = (lane / 32, lane % 32) unit u of one of
+// them.  It adds the 8 partial sums in group order, adds the bias and applies
+// f, then runs each later layer as a 32-term dot product over the previous
+// layer's values of its sample (a per-wave LDS row) with the weights in LDS.
+// One value per lane keeps the dependent instruction chains of the
+// activations short and spreads them over all SIMDs; running a tile late
+// lets a wave start the next tile without waiting for the slowest wave.  The
+// outputs collect in LDS and are written every NI_OUT tiles and at the end:
+// a store in flight would make every later use of a prefetched input wait
+// for all outstanding loads (loads and stores share one wait counter).
+//
+// Counters in LDS: zst[b] counts the partial-sum stores into buffer b and
+// zrd[b] the waves that have read it, each growing by 8 per use of the
+// buffer.  A wave writes tile t into buffer t % NI_NB once all 8 have read
+// tile t - NI_NB from it, and reads tile t once all 8 have stored it.  A
+// wave's LDS operations complete in order; counts are release additions after
+// the accesses they cover, and waits are acquire loads polled with a short
+// sleep.  Every wait is bounded (NI_SPIN polls): correct code never comes
+// near the bound, and a wave that reached it would go on rather than hang.
 // ---------------------------------------------------------------------------
 constexpr int NI_CH = 16;                  // inputs per chunk: a float4 per lane group
 constexpr int NI_SLOTS = 3;                // tiles of inputs held: the current one + two ahead
-constexpr int NI_ROUND = 5 * NI_SLOTS;     // tiles whose outputs are staged in LDS
+constexpr int NI_QWAIT = 7;                // loads of the current tile left in flight when the next is requested
+constexpr int NI_MW = N1_WAVES;            // chunk groups: one per wave
+constexpr int NI_NB = 3;                   // partial-sum buffers
+constexpr int NI_ZS = NARROW_TILE + 1;     // partial-sum row stride: conflict-free reads
+constexpr int NI_OUT = 16;                 // tiles of outputs held before they are written
 constexpr unsigned NI_OOB = NB_OOB;
+constexpr int NI_SPIN = 1 << 22;           // polls before a wait gives up (about 0.1 s)
+static_assert(2 * N1_WAVES == NARROW_TILE, "two samples of a tile per wave");
 
-template <int MC>
+// waits until at most N of the wave's vector memory operations are in flight
+// (they complete in order, so the oldest ones have landed)
+template <int N>
+__device__ __forceinline__ void ni_wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// waits until the LDS counter c reaches at least v (acquire), at most NI_SPIN polls
+__device__ __forceinline__ void ni_wait_at_least(unsigned* c, unsigned v) {
+  for (int k = 0; k < NI_SPIN; ++k) {
+    if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+__device__ __forceinline__ float ni_act(int act, float z) {
+  float f, fp;
+  act_eval(act, z, f, fp);
+  return f;
+}
+
+template <int MC, int NS = NI_SLOTS, int NQ = NI_QWAIT>
 __global__ void __launch_bounds__(N1_WAVES * 64) narrow_infer_kernel(const NarrowFwdParams p) {
+  static_assert(NS == 2 || NS == 3, "two or three input slots");
+  static_assert(NQ >= 0, "loads left in flight");
+  constexpr int Q = NQ < MC ? NQ : MC;
   constexpr int T = NARROW_TILE;
   constexpr int NW = NARROW_WIDTH;
-  __shared__ float zp[N1_WAVES][T][NW + 1];                   // the waves' layer-1 sums
-  __shared__ __attribute__((aligned(16))) float hs[2][T][NWP];
+  // layer-1 partial sums [buffer][chunk group][unit][sample]
+  __shared__ float zq[NI_NB][NI_MW][NW][NI_ZS];
+  __shared__ unsigned zst[NI_NB], zrd[NI_NB];
   __shared__ __attribute__((aligned(16))) float ws[NARROW_MAX_LAYERS - 1][NW][NWP];
-  __shared__ float ob[NI_ROUND * T][NW];                      // f(z_L) of a round's samples
+  __shared__ float bs[NARROW_MAX_LAYERS][NW];
+  // a layer's values of each wave's two samples, and the outputs held
+  __shared__ __attribute__((aligned(16))) float hs[N1_WAVES][2][NWP];
+  __shared__ float os[N1_WAVES][NI_OUT][2][NW];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -505,138 +601,217 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_infer_kernel(const Narro
   const int t0 = (int)((int64_t)blockIdx.x * ntiles / gridDim.x);
   const int t1 = (int)((int64_t)(blockIdx.x + 1) * ntiles / gridDim.x);
   const int nt = t1 - t0;
+  if (tid < NI_NB) {
+    zst[tid] = 0u;
+    zrd[tid] = 0u;
+  }
+  __syncthreads();
+
+  // the small layers' weights and every bias: requested first and staged in
+  // LDS once the big loads are issued (a store waits for its load, and loads
+  // complete in order); each wave stages its share before it counts its first
+  // tile, and a wave reads them only after every wave has counted that tile.
+  // Every entry of the padded 32 x 32 blocks is readable, so the loads are
+  // unconditional (clamped indices).
+  constexpr int NSMALL = (NW * NW + N1_WAVES * 64 - 1) / (N1_WAVES * 64);
+  float wv[NARROW_MAX_LAYERS - 1][NSMALL];
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < NSMALL; ++u) {
+      const int e = tid + u * N1_WAVES * 64;
+      wv[li][u] = p.W[li + 1][e < NW * NW ? e : NW * NW - 1];
+    }
+  const int bl = (tid >> 5) & (NARROW_MAX_LAYERS - 1);
+  const float bv = pick(bl, p.bias[0], p.bias[1], p.bias[2], p.bias[3])[tid & (NW - 1)];
+  // issued before every later load, so that staging them waits for them alone
+  __builtin_amdgcn_sched_barrier(0);
   const int nch = (p.d0 + NI_CH - 1) / NI_CH;
-  // chunks of this wave: MC or MC - 1 (MC is the launch's ceil(nch / 8))
-  const bool last_mine = (wave + N1_WAVES * (MC - 1)) < nch;
-
-  SmallLayers sl;
-  load_small_layers(p, tid, sl);
-
-  // lane (r, g) feeds sample r and units r, 16 + r with inputs 16 c + 4 g ..
-  // 16 c + 4 g + 3 of chunk c = wave + 8 i, one per MFMA (as in the 16-sample
-  // kernel).  W_1 and the inputs are read through buffer resources.  Chunks
-  // i < MC - 1 lie wholly inside the input width (byte offset kofs + 512 i);
-  // the last one may be partial or absent, and its inputs past the width are
-  // read at an offset past the buffers.
-  const unsigned kofs = 4u * (unsigned)(wave * NI_CH + 4 * g);
-  const int klast = (wave + N1_WAVES * (MC - 1)) * NI_CH + 4 * g;
+  const int grp = (int)((wave + blockIdx.x) % NI_MW);
+  // chunks of this group: MC or MC - 1 (MC is the launch's ceil(nch / NI_MW))
+  const bool last_mine = (grp + NI_MW * (MC - 1)) < nch;
+  // lane (r, g) feeds unit r (and 16 + r) and sample r with inputs 16 c + 4 g
+  // .. 16 c + 4 g + 3 of chunk c = grp + NI_MW i, one per instruction; it
+  // loads the inputs of row m = lane / 4 and group e = lane % 4 and takes its
+  // own from lane 4 r + g.  Chunks i < MC - 1 lie wholly inside the input
+  // width; the last one may be partial or absent, and its inputs past the
+  // width are read at an offset past the buffer.
+  const int m = lane >> 2, e = lane & 3;
+  const int src_byte = 4 * (4 * r + g);
+  const unsigned kofs = 4u * (unsigned)(grp * NI_CH + 4 * e);
+  const int klast = (grp + NI_MW * (MC - 1)) * NI_CH + 4 * e;
   const unsigned kofs_last = klast < p.d0 ? 4u * (unsigned)klast : NI_OOB;
   auto koff = [&](int i) {
-    return i < MC - 1 ? kofs + 4u * N1_WAVES * NI_CH * i : kofs_last;
+    return i < MC - 1 ? kofs + 4u * NI_MW * NI_CH * i : kofs_last;
   };
-  const unsigned wrow = 4u * (unsigned)(r * p.ldw[0]);
-  const unsigned whalf = 4u * (unsigned)(16 * p.ldw[0]);
+  // W_1 packed in this kernel's operand layout (W1i: lane r + 16 g of block
+  // (c, h) holds W_1[16 h + r][16 c + 4 g ..]): one contiguous 1 KiB per
+  // instruction, no permute; chunks past the last read as zeros
   const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)p.W[0], (short)0, (int)(4 * NW * p.ldw[0]), 0x00020000);
-  float4 wlo[MC], whi[MC];
-#pragma unroll
-  for (int i = 0; i < MC; ++i) {
-    wlo[i] = __builtin_bit_cast(
-        float4, __builtin_amdgcn_raw_buffer_load_b128(wres, wrow + koff(i), 0, 0));
-    whi[i] = __builtin_bit_cast(
-        float4, __builtin_amdgcn_raw_buffer_load_b128(wres, wrow + whalf + koff(i), 0, 0));
-  }
-
+      (void*)p.W1i, (short)0, nch * NARROW_PACK_W1I_BLOCK * 4, 0x00020000);
+  auto wload = [&](int i, int h) {
+    const int c = grp + NI_MW * i;
+    const unsigned off = c < nch ? 16u * (unsigned)((2 * c + h) * 64 + lane) : NI_OOB;
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0));
+  };
   // the rows of this workgroup's tiles (fewer than NI_OOB bytes: the host
   // picks another kernel otherwise)
   const int row0 = t0 * T;
   const int nrows = (p.B < t1 * T ? p.B : t1 * T) - row0;
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.X + (int64_t)row0 * p.d0), (short)0, nrows * p.d0 * 4, 0x00020000);
-  auto load_tile = [&](float4(&dst)[MC], int tt) {
-    const unsigned roff = 4u * (unsigned)((tt * T + r) * p.d0);
-#pragma unroll
-    for (int i = 0; i < MC; ++i)
-      dst[i] = __builtin_bit_cast(
-          float4, __builtin_amdgcn_raw_buffer_load_b128(xres, roff + koff(i), 0, 0));
+  auto xload = [&](int tt, int i) {
+    const unsigned roff = 4u * (unsigned)((tt * T + m) * p.d0);
+    return __builtin_bit_cast(
+        float4, __builtin_amdgcn_raw_buffer_load_b128(xres, roff + koff(i), 0, 0));
   };
-
-  float4 x[NI_SLOTS][MC];
+  auto load_tile = [&](float4(&dst)[MC], int tt) {
+#pragma unroll
+    for (int i = 0; i < MC; ++i) dst[i] = xload(tt, i);
+  };
+  float4 wlo[MC], whi[MC];
+  float4 x[NS][MC];
+#pragma unroll
+  for (int i = 0; i < MC; ++i) {
+    wlo[i] = wload(i, 0);
+    whi[i] = wload(i, 1);
+  }
   load_tile(x[0], 0);
-  load_tile(x[1], 1);
+  if constexpr (NS == 3) load_tile(x[1], 1);
   // every load of the prologue is issued before the first wait
   __builtin_amdgcn_sched_barrier(0);
-  store_small_layers<false>(sl, tid, ws, ws);
+#pragma unroll
+  for (int li = 0; li < NARROW_MAX_LAYERS - 1; ++li)
+#pragma unroll
+    for (int u = 0; u < NSMALL; ++u) {
+      const int e2 = tid + u * N1_WAVES * 64;
+      if (e2 < NW * NW) ws[li][e2 / NW][e2 % NW] = wv[li][u];
+    }
+  if (tid < NARROW_MAX_LAYERS * NW) bs[bl][tid & (NW - 1)] = bv;
 
-  // layer 1 of tile tt from its inputs xc, then the tail, whose outputs go to
-  // row block obi of the round's staging area
-  auto tile = [&](const float4(&xc)[MC], int tt, int obi) {
+  // layer 1 of tile tt from its inputs xc; the partial sums go to buffer
+  // tt % NI_NB once every wave has read the tile that used it before
+  auto tile = [&](const float4(&xc)[MC], int tt) {
     floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < MC; ++i) {
       if (i < MC - 1 || last_mine) {
-        const float4 v = xc[i];
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, wlo[i].x, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.x, whi[i].x, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, wlo[i].y, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.y, whi[i].y, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, wlo[i].z, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.z, whi[i].z, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, wlo[i].w, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(v.w, whi[i].w, acc1, 0, 0, 0);
+        const float4 v = lane_permute4(src_byte, xc[i]);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(wlo[i].x, v.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(whi[i].x, v.x, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(wlo[i].y, v.y, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(whi[i].y, v.y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(wlo[i].z, v.z, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(whi[i].z, v.z, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(wlo[i].w, v.w, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(whi[i].w, v.w, acc1, 0, 0, 0);
       }
     }
-    // accumulator register v of lane (r, g): sample 4 g + v, unit r (+16)
+    const int b = tt % NI_NB;
+    if (tt >= NI_NB) ni_wait_at_least(&zrd[b], (unsigned)(NI_MW * (tt / NI_NB)));
+    // accumulator register v: unit 4 g + v (+ 16) of sample r
+    float* zrow = &zq[b][grp][4 * g][r];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      zp[wave][4 * g + v][r] = acc0[v];
-      zp[wave][4 * g + v][16 + r] = acc1[v];
+      zrow[v * NI_ZS] = acc0[v];
+      zrow[(16 + v) * NI_ZS] = acc1[v];
     }
-    __syncthreads();
-    // z_1 of (sample tid / 32, unit tid % 32): the waves' sums in wave order;
-    // the tail's first barrier comes before the next tile rewrites zp
-    const int s = tid >> 5, j = tid & 31;
-    float z1 = zp[0][s][j];
-#pragma unroll
-    for (int w = 1; w < N1_WAVES; ++w) z1 += zp[w][s][j];
-    narrow_tail<false, T, true>(p, (t0 + tt) * T, tid, z1, 0.0f, hs, ws, ws, sl.b,
-                                ob + obi * T);
+    if (lane == 0) __hip_atomic_fetch_add(&zst[b], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
   };
 
-  // Tile tt is in slot tt % 3 (rounds are whole multiples of 3 tiles).  The
-  // loop runs whole groups of three tiles, each requesting the inputs of the
-  // tile two ahead before its matrix work (past the last tile: zeros, no
-  // traffic); the last one or two tiles follow the loop, their inputs already
-  // requested.  (With a loop exit or a guard inside the group the compiler
-  // could no longer tell which loads a use waits for, and would wait for all.)
-  for (int rb = 0; rb < nt; rb += NI_ROUND) {
-    const int rn = nt - rb < NI_ROUND ? nt - rb : NI_ROUND;
-    int tb = 0;
-    for (; tb + NI_SLOTS <= rn; tb += NI_SLOTS) {
-      load_tile(x[2], rb + tb + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      tile(x[0], rb + tb, tb);
-      load_tile(x[0], rb + tb + 3);
-      __builtin_amdgcn_sched_barrier(0);
-      tile(x[1], rb + tb + 1, tb + 1);
-      load_tile(x[1], rb + tb + 4);
-      __builtin_amdgcn_sched_barrier(0);
-      tile(x[2], rb + tb + 2, tb + 2);
+  // layers 1 (the rest of it) to L for this wave's two samples of tile tt
+  const int sl = lane >> 5, u = lane & (NW - 1);
+  const int js = 2 * wave + sl;  // sample within the tile
+  auto flush = [&](int tt) {     // outputs of tiles (tt / NI_OUT) * NI_OUT .. tt
+    const int tf = tt - tt % NI_OUT;
+    for (int q = tf; q <= tt; ++q) {
+      const int smp = (t0 + q) * T + js;
+      if (u < p.dout && smp < p.B) p.out[(int64_t)smp * p.dout + u] = os[wave][q % NI_OUT][sl][u];
     }
-    if (tb < rn) tile(x[0], rb + tb, tb);
-    if (tb + 1 < rn) tile(x[1], rb + tb + 1, tb + 1);
-    // the round's outputs, rows [(t0 + rb) T, ..) of out [B][d_L], contiguous;
-    // the tail ended on a barrier, and the next round's first barrier comes
-    // before ob is written again
-    const int d = p.dout;
-    const int rs = (t0 + rb) * T;
-    const int re = (t0 + rb + rn) * T < p.B ? (t0 + rb + rn) * T : p.B;
-    float* o = p.out + (int64_t)rs * d;
-    for (int e = tid; e < (re - rs) * d; e += N1_WAVES * 64) o[e] = ob[e / d][e % d];
-    // let the stores drain here, once per round, so that the loads of the
-    // next round are tracked on their own
-    __builtin_amdgcn_s_waitcnt(0);
+  };
+  auto rest = [&](int tt) {
+    const int b = tt % NI_NB;
+    ni_wait_at_least(&zst[b], (unsigned)(NI_MW * (tt / NI_NB + 1)));
+    float z = zq[b][0][u][js];
+#pragma unroll
+    for (int q = 1; q < NI_MW; ++q) z += zq[b][q][u][js];
+    if (lane == 0) __hip_atomic_fetch_add(&zrd[b], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    float h = ni_act(p.acts[0], z + bs[0][u]);
+    for (int l = 2; l <= p.L; ++l) {
+      hs[wave][sl][u] = h;
+      const float* wr = &ws[l - 2][u][0];
+      const float* hr = &hs[wave][sl][0];
+      float a0 = bs[l - 1][u], a1 = 0.0f;
+#pragma unroll
+      for (int k = 0; k < NW; k += 8) {
+        const float4 w0 = *reinterpret_cast<const float4*>(wr + k);
+        const float4 h0 = *reinterpret_cast<const float4*>(hr + k);
+        const float4 w1 = *reinterpret_cast<const float4*>(wr + k + 4);
+        const float4 h1 = *reinterpret_cast<const float4*>(hr + k + 4);
+        a0 = fmaf(w0.x, h0.x, a0);
+        a1 = fmaf(w1.x, h1.x, a1);
+        a0 = fmaf(w0.y, h0.y, a0);
+        a1 = fmaf(w1.y, h1.y, a1);
+        a0 = fmaf(w0.z, h0.z, a0);
+        a1 = fmaf(w1.z, h1.z, a1);
+        a0 = fmaf(w0.w, h0.w, a0);
+        a1 = fmaf(w1.w, h1.w, a1);
+      }
+      h = ni_act(pick(l - 1, p.acts[0], p.acts[1], p.acts[2], p.acts[3]), a0 + a1);
+    }
+    os[wave][tt % NI_OUT][sl][u] = h;
+    if (tt % NI_OUT == NI_OUT - 1 || tt == nt - 1) flush(tt);
+  };
+
+  // Tile tt is in slot tt % NS.  Before its matrix work a wave requests the
+  // inputs of tile tt + NS - 1 (past the last tile: zeros, no traffic), once
+  // at most Q loads of tile tt are still in flight; after it, the wave
+  // finishes tile tt - 1.  The loop runs whole groups of NS tiles (slot
+  // indices must be constants); the last tiles follow it, their inputs
+  // already requested.
+  auto step = [&](auto cur, auto nxt, int tt) {
+    ni_wait_loads<Q + (NS - 2) * MC>();
+    __builtin_amdgcn_sched_barrier(0);
+    load_tile(x[decltype(nxt)::value], tt + NS - 1);
+    __builtin_amdgcn_sched_barrier(0);
+    tile(x[decltype(cur)::value], tt);
+    if (tt > 0) rest(tt - 1);
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  int tb = 0;
+  if constexpr (NS == 2) {
+    for (; tb + 2 <= nt; tb += 2) {
+      step(S0{}, S1{}, tb);
+      step(S1{}, S0{}, tb + 1);
+    }
+    if (tb < nt) {
+      tile(x[0], tb);
+      if (tb > 0) rest(tb - 1);
+    }
+  } else {
+    for (; tb + 3 <= nt; tb += 3) {
+      step(S0{}, S2{}, tb);
+      step(S1{}, S0{}, tb + 1);
+      step(S2{}, S1{}, tb + 2);
+    }
+    if (tb < nt) {
+      tile(x[0], tb);
+      if (tb > 0) rest(tb - 1);
+    }
+    if (tb + 1 < nt) {
+      tile(x[1], tb + 1);
+      rest(tb);
+    }
   }
+  if (nt > 0) rest(nt - 1);
 }
 
 // Workgroup = 8 waves, one (layer, 16-column tile, 16-unit half) over the whole
 // batch: G[16 h + u][c0 + r] = sum over samples of delta[s][16 h + u] a_prev[s][c0 + r]
 // on the 16x16x4 matrix cores.  Wave w takes every 8th group of 4 samples; the
 // waves' sums are added in wave order, then the tile applies the SGD step.
-template <class V>
-__device__ __forceinline__ V pick(int l, V a0, V a1, V a2, V a3) {
-  return l == 0 ? a0 : (l == 1 ? a1 : (l == 2 ? a2 : a3));
-}
 
 constexpr int N2_WAVES = 8;
 constexpr int N2_UNROLL = 32;  // groups of 4 samples loaded before use
@@ -714,12 +889,22 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   if (c == 0) bred[wave][g][r] = bsum;
   __syncthreads();
 
+  float wn = 0.0f;
   if (w_mine) {
     float gsum = red[0][ui][uj];
 #pragma unroll
     for (int w = 1; w < N2_WAVES; ++w) gsum += red[w][ui][uj];
     G[wo] = gsum;
-    W[wo] = fmaf(-p.scale, gsum, w_old);
+    wn = fmaf(-p.scale, gsum, w_old);
+    W[wo] = wn;
+  }
+  // layer 1: the tile's 16 x 16 block of the updated W_1 (zeros past d_1 and
+  // d_0) into both packed copies; it is one whole block of W1i and a quarter
+  // of four blocks of W1f
+  if (l == 0 && tid < 256 && p.W1f) {
+    const int u = u0 + ui, k = c0 + uj;
+    p.W1i[((2 * c + h) * 64 + ui + 16 * (uj >> 2)) * 4 + (uj & 3)] = wn;
+    p.W1f[(((k >> 6) * 8 + (u >> 2)) * 64 + 4 * ((k & 63) >> 2) + (u & 3)) * 4 + (k & 3)] = wn;
   }
   if (b_mine) {
     float gsum = 0.0f;
@@ -733,11 +918,41 @@ __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDw
   }
 }
 
+// Both packed copies of W_1, one thread per packed element.
+__global__ void __launch_bounds__(256) narrow_pack_w1_kernel(const float* W1, int64_t ldw, int d1,
+                                                              int d0, float* W1f, float* W1i,
+                                                              int64_t nf, int64_t ni) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < nf) {
+    // W1f: block (t, q) = e / 256, lane 4 b + i, component v
+    const int64_t blk = e >> 8;
+    const int ln = (int)(e >> 2) & 63, v = (int)e & 3;
+    const int t = (int)(blk >> 3), q = (int)blk & 7;
+    const int u = 4 * q + (ln & 3), k = 64 * t + 4 * (ln >> 2) + v;
+    W1f[e] = (u < d1 && k < d0) ? W1[(int64_t)u * ldw + k] : 0.0f;
+  } else if (e < nf + ni) {
+    // W1i: block (c, h) = (e - nf) / 256, lane r + 16 g, component v
+    const int64_t f = e - nf;
+    const int64_t blk = f >> 8;
+    const int ln = (int)(f >> 2) & 63, v = (int)f & 3;
+    const int c = (int)(blk >> 1), h = (int)blk & 1;
+    const int u = 16 * h + (ln & 15), k = 16 * c + 4 * (ln >> 4) + v;
+    W1i[f] = (u < d1 && k < d0) ? W1[(int64_t)u * ldw + k] : 0.0f;
+  }
+}
+
+hipError_t launch_narrow_pack_w1(const float* W1, int64_t ldw, int d1, int d0, float* W1f,
+                                 float* W1i, hipStream_t s) {
+  const int64_t nf = narrow_pack_w1f_elems(d0), ni = narrow_pack_w1i_elems(d0);
+  const dim3 grid((unsigned)((nf + ni + 255) / 256)), block(256);
+  return launch_k(narrow_pack_w1_kernel, grid, block, 0, s, W1, ldw, d1, d0, W1f, W1i, nf, ni);
+}
+
 // The per-sample kernel for this pass: inference over batches above
-// NARROW_SMALL_BATCH takes the persistent kernel when W_1 fits its registers
-// (d0 <= 8 waves x NI_MC_MAX chunks x 16 = 896; eight chunks per wave would
-// spill) and every workgroup's input rows fit below NI_OOB bytes.
-constexpr int NI_MC_MAX = 7;
+// NARROW_SMALL_BATCH takes the persistent kernel when W_1 fits its matrix
+// waves' registers (d0 <= 8 waves x NI_MC_MAX chunks x 16 = 1024) and every
+// workgroup's input rows fit below NI_OOB bytes.
+constexpr int NI_MC_MAX = 8;
 
 int narrow_infer_grid(const NarrowFwdParams& p) {
   const int ntiles = (p.B + NARROW_TILE - 1) / NARROW_TILE;
@@ -746,7 +961,7 @@ int narrow_infer_grid(const NarrowFwdParams& p) {
 
 NarrowKernel narrow_fwd_kernel(bool train, const NarrowFwdParams& p) {
   if (p.B <= NARROW_SMALL_BATCH) return NK_FWD4;
-  if (!train && p.ncu > 0 && p.d0 <= N1_WAVES * NI_MC_MAX * NI_CH) {
+  if (!train && p.ncu > 0 && p.d0 <= NI_MW * NI_MC_MAX * NI_CH) {
     const int64_t ntiles = (p.B + NARROW_TILE - 1) / NARROW_TILE;
     const int64_t grid = narrow_infer_grid(p);
     const int64_t rows = (ntiles + grid - 1) / grid * NARROW_TILE;
@@ -774,14 +989,15 @@ hipError_t launch_narrow_fwd(bool train, const NarrowFwdParams& p, hipStream_t s
     }
     case NK_INFER: {
       const dim3 grid(narrow_infer_grid(p));
-      // chunks per wave
-      switch (((p.d0 + NI_CH - 1) / NI_CH + N1_WAVES - 1) / N1_WAVES) {
+      // chunks per matrix wave
+      switch (((p.d0 + NI_CH - 1) / NI_CH + NI_MW - 1) / NI_MW) {
         case 1: return launch_k(narrow_infer_kernel<1>, grid, block, 0, s, p);
         case 2: return launch_k(narrow_infer_kernel<2>, grid, block, 0, s, p);
         case 3: return launch_k(narrow_infer_kernel<3>, grid, block, 0, s, p);
         case 4: return launch_k(narrow_infer_kernel<4>, grid, block, 0, s, p);
         case 5: return launch_k(narrow_infer_kernel<5>, grid, block, 0, s, p);
         case 6: return launch_k(narrow_infer_kernel<6>, grid, block, 0, s, p);
+        case 7: return launch_k(narrow_infer_kernel<7>, grid, block, 0, s, p);
         default: return launch_k(narrow_infer_kernel<NI_MC_MAX>, grid, block, 0, s, p);
       }
     }

@@ -244,6 +244,45 @@ def test_narrow_and_general_paths_agree():
     assert not parity.check_params(res[0][1], res[1][1], dims, tol=1e-5, what="grads")
 
 
+@pytest.mark.parametrize("dims,acts", [
+    ((784, 30, 10), ("sigmoid",)),
+    ((40, 12, 5), ("tanh", "sigmoid")),      # one unit half: W1i and W1f half empty
+    ((100, 32, 7), ("sigmoid",)),            # 1.5625 input steps of 64
+])
+def test_packed_w1_follows_every_parameter_change(dims, acts):
+    """Narrow fp32 nets read W_1 from packed copies that the SGD kernel of the
+    narrow step rewrites and the host rebuilds after any other change.  After
+    set_params, a step on the general path (two shards), a narrow step and a
+    second set_params, the 4-sample kernel (100 samples) and the persistent
+    inference kernel (3000 samples) must give the network outputs of the
+    parameters the library holds at that point."""
+    acts_full = parity.full_acts(dims, acts)
+    theta, X, Y = _problem(dims, 91, 3000, x_lo=-1.0)
+    theta2, _, _ = _problem(dims, 92, 1)
+    xd, yd = to_dev(X), to_dev(Y)
+    fails = []
+
+    def check(net, what):
+        p = net.params()
+        for n in (100, 3000):
+            out = net.forward(xd[:n])
+            ref = mlp.output(p.astype(np.float64), dims, acts_full, X[:n].astype(np.float64))
+            e, i = parity.floored_rel(out, ref)
+            if e > parity.OUT_TOL:
+                fails.append(f"{what}, {n} samples: {e:.3g} at {i}")
+
+    note(f"packed W_1 dims={dims}")
+    with GpuNet(dims, acts, theta) as net:
+        check(net, "after set_params")
+        net.train_batch(xd[:200], yd[:200], 0.5, 2)
+        check(net, "after a general-path step")
+        net.train_batch(xd[200:400], yd[200:400], 0.5, 1)
+        check(net, "after a narrow step")
+        net.nf.nf_set_params(net.h, theta2)
+        check(net, "after a second set_params")
+    assert not fails, "\n".join(fails)
+
+
 def test_hand_worked_networks_on_gpu():
     """The hand-worked tiny networks: integer relu cases come out exactly."""
     for c in pins.load_hand_worked():
@@ -371,11 +410,12 @@ def test_derivative_in_saturation(act, family, hidden):
     # narrow inference past 2048 samples: persistent workgroups holding W_1
     ((40, 17, 9, 5), ("tanh", "sigmoid", "gaussian"), 4100),   # width 2.5 chunks
     ((4, 3), ("tanh",), 3000),                                 # one partial chunk
-    ((896, 32), ("sigmoid",), 3000),                           # widest input held, one layer
+    ((1024, 32), ("sigmoid",), 3000),                          # widest input held, one layer
+    ((1012, 30, 10), ("tanh", "sigmoid"), 2500),               # 63.25 chunks: a partial last chunk
     ((128, 32, 32, 32, 10), ("tanh", "relu", "gaussian", "sigmoid"), 2049),  # 1-sample tail
     ((784, 30, 10), ("sigmoid",), 65541),    # 16 or 17 tiles per workgroup: 1 or 2 after the loop
     ((784, 30, 10), ("sigmoid",), 70001),    # 17 or 18 tiles per workgroup
-    ((900, 30, 10), ("sigmoid",), 3000),     # input too wide to hold: 16-sample tiles
+    ((1040, 30, 10), ("sigmoid",), 3000),    # input too wide to hold: 16-sample tiles
 ])
 def test_inference_matches_reference(dims, acts, n):
     theta, X, _ = _problem(dims, 77, n, x_lo=-1.0)
