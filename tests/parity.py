@@ -4,16 +4,19 @@ GPU library through its C ABI binding.
 Gates (fp32 GPU against the fp64 reference, same seeded inputs):
 
 * parameters, every tensor t, every element i:
-      |gpu_i - ref_i| <= 1e-4 * max(|ref_i|, rms(ref_t))
-  a relative error of 1e-4 with the tensor's rms as the floor of the
-  denominator.  The error of a weight that lands near zero after a step is
-  the fp32 error of its update (eta/B) * G, not a fraction of its own value,
-  so a floor is needed; with the smaller floor 1e-3 * rms(ref_t) an
-  independent fp32 computation of the same step (numpy float32 products on
-  the CPU) already reaches 1.0-1.7e-4 on the first layer of the 784-30-10
-  and 784-100-100-10 workloads.  Every comparison also reports the error
-  under that smaller floor and the unfloored largest relative error with the
-  element that holds it (tensor_report).
+      |gpu_i - ref_i| <= 1e-4 * max(|ref_i|, f * rms(ref_t))
+  a relative error of 1e-4 with a floor on the denominator.  The error of a
+  weight that lands near zero after a step is the fp32 error of its update
+  (eta/B) * G, not a fraction of its own value, so a floor is needed.  The
+  full-size workloads are gated with f = 1e-3 (SMALL_FLOOR), in every
+  step-along comparison and in the free-running ones of networks without
+  kinks; the chaotic free-running relu schedule and the small edge-case
+  networks use f = 1 (an independent fp32 computation of the same step,
+  numpy float32 products on the CPU, reaches 1.0-1.7e-4 under f = 1e-3 on
+  the first layer of the 784-30-10 and 784-100-100-10 workloads, so f = 1e-3
+  holds only for an implementation whose sums are that accurate).  Every
+  comparison reports the error under both floors and the unfloored largest
+  relative error with the element that holds it (tensor_report).
 * update, every tensor, in the step-along comparisons (both sides start from
   the same theta_t): with d_gpu = theta_gpu - theta_t and the exact
   d_ref = -(eta/B) G_ref,
@@ -97,16 +100,19 @@ def tensor_report(got, ref) -> Dict:
     return {"gated": e, "at": i, "floor_1e-3": e3, "floor_1e-3_at": i3, "unfloored": raw}
 
 
-def check_params(got, ref, dims, tol=PARAM_TOL, what="params", report=None) -> List[str]:
-    """Elementwise gate per tensor; report (a dict) collects tensor_report."""
+def check_params(got, ref, dims, tol=PARAM_TOL, what="params", report=None,
+                 floor: float = 1.0) -> List[str]:
+    """Elementwise gate per tensor, the denominator floored at floor * rms of
+    the tensor (1: the rms floor; SMALL_FLOOR: the 1e-3 * rms floor); report
+    (a dict) collects tensor_report."""
     fails = []
     for name, sl in tensor_slices(dims):
         rep = tensor_report(got[sl], ref[sl])
         if report is not None:
             report[name] = rep
-        if not rep["gated"] <= tol:
-            i = rep["at"]
-            fails.append(f"{what} {name}: floored relative error {rep['gated']:.3e} > {tol:g} "
+        e, i = (rep["gated"], rep["at"]) if floor == 1.0 else floored_rel(got[sl], ref[sl], floor)
+        if not e <= tol:
+            fails.append(f"{what} {name}: relative error {e:.3e} (floor {floor:g} rms) > {tol:g} "
                          f"at {i} (gpu {got[sl][i]!r}, ref {ref[sl][i]!r})")
     return fails
 

@@ -1,7 +1,10 @@
 """GPU library against the CPU reference on the five benchmark workloads at
 their full sizes, in the launch configuration bench.py times.
 
-Two comparisons per workload (the gates are those of tests/parity.py):
+Two comparisons per workload (the gates are those of tests/parity.py; the
+parameters, and the held-out outputs of the 784-30-10 workload, are gated at
+1e-4 with the 1e-3 * rms floor of the denominator, except the free-running
+relu trajectories below, which keep the rms floor):
 
 * step along the reference: before every step the GPU net is loaded with the
   reference's parameters theta_t for that step (data flows from the
@@ -139,7 +142,8 @@ def _run(name, steps=None, shards=None):
             else:
                 new, G = ref_t[t + 1], ref_g[t]
             rp, rg, ru = {}, {}, {}
-            fails += [f"step-along {t}: {m}" for m in parity.check_params(p, new, w.dims, report=rp)]
+            fails += [f"step-along {t}: {m}" for m in parity.check_params(
+                p, new, w.dims, report=rp, floor=parity.SMALL_FLOOR)]
             fails += [f"step-along {t}: {m}" for m in parity.check_grads(g, G, w.dims, report=rg)]
             fails += [f"step-along {t}: {m}" for m in parity.check_update(p, ref_t[t], G, scale,
                                                                           w.dims, report=ru)]
@@ -164,8 +168,12 @@ def _run(name, steps=None, shards=None):
             else:
                 th_new, G_o = ref_t[t + 1], ref_g[t]
             rp, rg = {}, {}
-            fails += [f"free {t}: {m}" for m in parity.check_params(p, th_new, w.dims, tol=tol_p,
-                                                                    report=rp)]
+            # without kinks the free-running trajectory is held to the same floor
+            # as the step-along one; the relu schedules to the rms floor and the
+            # envelope of the reference's own one-ulp spread
+            fails += [f"free {t}: {m}" for m in parity.check_params(
+                p, th_new, w.dims, tol=tol_p, report=rp,
+                floor=1.0 if kinked else parity.SMALL_FLOOR)]
             gfails = parity.check_grads(g, G_o, w.dims, report=rg)
             if not kinked:
                 fails += [f"free {t}: {m}" for m in gfails]
@@ -187,8 +195,8 @@ def _run(name, steps=None, shards=None):
             out = net.forward(to_dev(Xh))
             ro = parity.tensor_report(out, mlp.output(ref_t[-1], w.dims, acts, Xh))
             parity.emit(f"{name} inference", ro)
-            if not ro["gated"] <= parity.OUT_TOL:
-                fails.append(f"inference: floored relative error {ro['gated']:.3e}")
+            if not ro["floor_1e-3"] <= parity.OUT_TOL:
+                fails.append(f"inference: relative error {ro['floor_1e-3']:.3e} (floor 1e-3 rms)")
     msg = (f"[parity] {name}: step-along worst params {worst['along_params']:.2e}, tendencies "
            f"{worst['along_grads']:.2e}, update {worst['along_update']:.2e}; free-running worst "
            f"params {worst['free_params']:.2e}")
