@@ -815,20 +815,22 @@ __global__ void __launch_bounds__(N1_WAVES * 64) narrow_infer_kernel(const Narro
 
 constexpr int N2_WAVES = 8;
 constexpr int N2_UNROLL = 32;  // groups of 4 samples loaded before use
+constexpr int N2_RUN_ALIGN = 4;  // tiles per XCD run: a multiple of two column tiles x two halves
 
 __global__ void __launch_bounds__(N2_WAVES * 64) narrow_dw_kernel(const NarrowDwParams p) {
   __shared__ float red[N2_WAVES][16][17];
   __shared__ float bred[N2_WAVES][4][16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // consecutive workgroups land on different XCDs (round robin over 8); give
-  // each XCD a contiguous run of tiles so that the two unit halves of a column
-  // tile, and neighbouring column tiles, share the input rows in one L2
-  const int nwg = p.ntiles;
-  const int per = (nwg + 7) / 8;
-  const int full = nwg - 8 * (per - 1);       // XCDs that get `per` tiles
+  // consecutive workgroups land on different XCDs (round robin over 8); the
+  // grid is 8 runs of N2_RUN_ALIGN-aligned length, and XCD x takes the run of
+  // tiles [x * per, (x + 1) * per), so the four tiles of two neighbouring
+  // column tiles (both unit halves), whose 64-byte input slices share 128-byte
+  // lines, meet in one L2; the grid's padding workgroups have no tile
+  const int per = (int)gridDim.x >> 3;
   const int xcd = (int)blockIdx.x & 7, slot = (int)blockIdx.x >> 3;
-  const int tile = xcd < full ? xcd * per + slot : full * per + (xcd - full) * (per - 1) + slot;
+  const int tile = xcd * per + slot;
+  if (tile >= p.ntiles) return;
   // the layer of this tile (tile_base of the layers past the last is ntiles);
   // every per-layer argument is picked by value from constant indices, so
   // the argument loads all issue at kernel start
@@ -1017,7 +1019,9 @@ const char* narrow_fwd_name(bool train, const NarrowFwdParams& p) {
 }
 
 hipError_t launch_narrow_dw(const NarrowDwParams& p, hipStream_t s) {
-  return launch_k(narrow_dw_kernel, dim3(p.ntiles), N2_WAVES * 64, 0, s, p);
+  if (p.ntiles <= 0) return hipErrorInvalidValue;
+  const int per = ((p.ntiles + 7) / 8 + N2_RUN_ALIGN - 1) / N2_RUN_ALIGN * N2_RUN_ALIGN;
+  return launch_k(narrow_dw_kernel, dim3(8 * per), N2_WAVES * 64, 0, s, p);
 }
 
 }  // namespace nf
