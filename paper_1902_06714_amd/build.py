@@ -25,7 +25,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnf.so")
 SOURCES = ["nf_api.hip", "nf_kernels.hip", "nf_narrow.hip", "nf_narrow64.hip", "nf_medium.hip",
-           "nf_eval.hip", "nf_calib.hip"]
+           "nf_eval.hip", "nf_calib.hip", "nf_skinny.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -582,9 +582,44 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
   if (pieces.empty()) return NF_OK;
 
   // the piece kernels, grouped by tile shape and B-row vector loads (layer
-  // order within a group), up to GEMM_GROUP_MAX layers per launch
+  // order within a group), up to GEMM_GROUP_MAX layers per launch; fp32
+  // layers of at most SKINNY_MAX_UNITS units with 16-byte operand rows take
+  // the kernel that holds all of a layer's units in one workgroup
   const int dtype = dtype_of<T>();
   std::vector<bool> done(pieces.size(), false);
+  auto piece_params = [&](const Piece& pc) {
+    const LayerLayout& lj = n->layers[pc.l];
+    nf::GemmParamsT<T> p = dw_params(pc.l);
+    p.nsub = pc.nsub;
+    p.sub_len = (int)((shard_len + pc.nsub - 1) / pc.nsub);
+    p.partial = as<T>(n->partial) + pc.off;
+    p.pstride = pc.pstride;
+    p.ld0 = lj.ldw;
+    p.pbias = p.partial + (int64_t)shards * pc.nsub * pc.pstride;
+    return p;
+  };
+  if constexpr (sizeof(T) == 4) {
+    {
+      nf::SkinnyGroup g{};
+      double bytes = 0.0, flops = 0.0;
+      for (size_t j = 0; j < pieces.size() && g.n < nf::GEMM_GROUP_MAX; ++j) {
+        const Piece& pj = pieces[j];
+        const nf::GemmParamsT<T> p = piece_params(pj);
+        if (p.M > nf::SKINNY_MAX_UNITS || !vec_ok(p.A, p.lda) || !vec_ok(p.B, p.ldb)) continue;
+        const int nsplit = shards * pj.nsub;
+        g.npieces[g.n] = nsplit;
+        g.p[g.n++] = p;
+        bytes += gemm_bytes(nf::EPI_DW_PARTIAL, p.M, p.N, p.K, nsplit, (double)sizeof(T));
+        flops += 2.0 * p.M * (double)p.N * p.K;
+        done[j] = true;
+      }
+      if (g.n > 0) {
+        nf_status st = timed(n, "dw_skinny", bytes, flops, s,
+                             [&] { return nf::launch_dw_skinny_group(g, s); });
+        if (st != NF_OK) return st;
+      }
+    }
+  }
   for (size_t i = 0; i < pieces.size(); ++i) {
     if (done[i]) continue;
     const Piece& pi = pieces[i];
@@ -601,13 +636,7 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
       const int tj = pick_tile(lj.out, lj.in, (int64_t)shards * pj.nsub);
       const bool bvj = pj.l == 1 ? vec_ok(x, n->dims[0]) : true;
       if (tj != tile || bvj != bv) continue;
-      nf::GemmParamsT<T> p = dw_params(pj.l);
-      p.nsub = pj.nsub;
-      p.sub_len = (int)((shard_len + pj.nsub - 1) / pj.nsub);
-      p.partial = as<T>(n->partial) + pj.off;
-      p.pstride = pj.pstride;
-      p.ld0 = lj.ldw;
-      p.pbias = p.partial + (int64_t)shards * pj.nsub * pj.pstride;
+      nf::GemmParamsT<T> p = piece_params(pj);
       nsplit[g.n] = shards * pj.nsub;
       g.p[g.n++] = p;
       bytes += gemm_bytes(nf::EPI_DW_PARTIAL, p.M, p.N, p.K, nsplit[g.n - 1], (double)sizeof(T));

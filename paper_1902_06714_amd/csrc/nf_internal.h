@@ -132,6 +132,22 @@ template <class T>
 hipError_t launch_dw_partial_group(int tile, bool b_vec, const GemmGroupT<T>& g,
                                    const int* nsplit, hipStream_t s);
 
+// The tendency pieces of up to GEMM_GROUP_MAX fp32 layers of at most
+// SKINNY_MAX_UNITS units in one launch, operands loaded straight into the
+// matrix cores (csrc/nf_skinny.hip); same piece layout as
+// launch_dw_partial_group.  Problem q has npieces[q] pieces; start[] is
+// filled by the launcher.  Both operands and the piece buffer need 16-byte
+// aligned rows with pitches of whole 16-byte vectors.
+constexpr int SKINNY_MAX_UNITS = 128;
+constexpr int SKINNY_PD = 4;    // k-steps of operand loads in flight
+struct SkinnyGroup {
+  GemmParamsT<float> p[GEMM_GROUP_MAX];
+  int start[GEMM_GROUP_MAX + 1];
+  int npieces[GEMM_GROUP_MAX];
+  int n;
+};
+hipError_t launch_dw_skinny_group(SkinnyGroup g, hipStream_t s);
+
 // Fold the per-piece tendencies of up to FOLD_GROUP_MAX layers in piece order,
 // store each sum as the tendency, and write the SGD step W = Win - scale * G,
 // b = bin - scale * g (W [M][ldw], b [M]).  Layer q's pieces: nshards shards
