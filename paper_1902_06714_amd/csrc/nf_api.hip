@@ -364,6 +364,41 @@ nf::KSplit fwd_split(const nf_net* n, int64_t M, int64_t N, int64_t K, bool smal
   return nf::k_split(K, nsplit);
 }
 
+// The k pieces of the skinny forward kernel (layers of at most
+// SKINNY_MAX_UNITS units): one workgroup per (128 samples, piece) holding the
+// piece's slice of W in LDS, one workgroup per CU.  Among the piece counts
+// whose slice fits in LDS, the one with the fewest k-groups on the busiest
+// CU wins, the smaller on ties; nsplit 0 when none fits.
+nf::KSplit fwd_skinny_split(const nf_net* n, int64_t M, int64_t N, int64_t K) {
+  const int64_t ncu = n->ncu > 0 ? n->ncu : 256;
+  const int64_t groups = (M + 127) / 128;
+  nf::KSplit best{0, 0};
+  int64_t best_cost = -1;
+  for (int want = 1; want <= 16; ++want) {
+    const nf::KSplit ks = nf::k_split(K, want);
+    if (nf::fwd_skinny_lds_bytes((int)N, ks.sub_len) > nf::SKINNY_FWD_LDS) continue;
+    const int64_t per_cu = (groups * ks.nsplit + ncu - 1) / ncu;
+    const int64_t cost = per_cu * ((ks.sub_len + 15) / 16);
+    if (best_cost < 0 || cost < best_cost) {
+      best = ks;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+// layer 1 of the medium path goes to the skinny forward kernel
+template <class T>
+bool medium_fwd_skinny(const nf_net* n, const T* x, int64_t batch) {
+  if constexpr (sizeof(T) != 4) {
+    return false;
+  } else {
+    const LayerLayout& l1 = n->layers[1];
+    return l1.out <= nf::SKINNY_MAX_UNITS && vec_ok(x, n->dims[0]) &&
+           fwd_skinny_split(n, batch, l1.out, l1.in).nsplit > 0;
+  }
+}
+
 // elements of the pieces of a forward contraction cut into nsplit pieces
 int64_t fwd_piece_elems(int64_t M, int64_t N, int nsplit) {
   return nsplit <= 1 ? 0 : nsplit * round_up(M * round_up(N, 4), kAlign);
@@ -882,7 +917,8 @@ nf_status medium_forward_deltas(nf_net* n, const T* x, const T* y, int64_t batch
   p.M = (int)batch;
   p.N = l1.out;
   p.K = l1.in;
-  const nf::KSplit ks = fwd_split(n, p.M, p.N, p.K, false);
+  const bool skinny = medium_fwd_skinny<T>(n, x, batch);
+  const nf::KSplit ks = skinny ? fwd_skinny_split(n, p.M, p.N, p.K) : fwd_split(n, p.M, p.N, p.K, false);
   const int sub_len = ks.sub_len;
   const int nsplit = ks.nsplit;
   const int64_t ldz = round_up(p.N, 4);
@@ -895,9 +931,18 @@ nf_status medium_forward_deltas(nf_net* n, const T* x, const T* y, int64_t batch
   p.partial = as<T>(n->partial);
   p.pstride = zstride;
   p.ld0 = ldz;
-  const bool av = vec_ok(x, n->dims[0]);
-  st = launch<T>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, p, s, nf::TILE_64x64);
-  if (st != NF_OK) return st;
+  if constexpr (sizeof(T) == 4) {
+    if (skinny) {
+      st = timed(n, "fwd_skinny", gemm_bytes(nf::EPI_FWD_PIECE, p.M, p.N, p.K, nsplit, 4.0),
+                 2.0 * p.M * (double)p.N * p.K, s, [&] { return nf::launch_fwd_skinny(p, s); });
+      if (st != NF_OK) return st;
+    }
+  }
+  if (!skinny) {
+    const bool av = vec_ok(x, n->dims[0]);
+    st = launch<T>(n, nf::EPI_FWD_PIECE, true, true, av, true, nsplit, p, s, nf::TILE_64x64);
+    if (st != NF_OK) return st;
+  }
 
   mp.B = (int)batch;
   mp.L = L;
@@ -1244,8 +1289,12 @@ int64_t partial_need(const nf_net* n, const T* x, int64_t batch, int shards) {
   if (medium_layout<T>(n, batch, &mp)) {
     // the medium path always writes layer 1 as pieces, one or more
     const LayerLayout& l1 = n->layers[1];
+    // either kernel may take layer 1, depending on the input rows
     const nf::KSplit ks = fwd_split(n, batch, l1.out, l1.in, false);
-    need = std::max(need, ks.nsplit * round_up(batch * round_up(l1.out, 4), kAlign));
+    int np = ks.nsplit;
+    if (n->dtype == nf::DT_F32 && l1.out <= nf::SKINNY_MAX_UNITS)
+      np = std::max(np, fwd_skinny_split(n, batch, l1.out, l1.in).nsplit);
+    need = std::max(need, np * round_up(batch * round_up(l1.out, 4), kAlign));
   } else {
     for (int l = 1; l <= num_layers(n); ++l) {
       const LayerLayout& ly = n->layers[l];

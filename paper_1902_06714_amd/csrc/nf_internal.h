@@ -148,6 +148,18 @@ struct SkinnyGroup {
 };
 hipError_t launch_dw_skinny_group(SkinnyGroup g, hipStream_t s);
 
+// Forward pieces of a fp32 layer of at most SKINNY_MAX_UNITS units (N),
+// operands loaded straight into the matrix cores (csrc/nf_skinny.hip):
+// partial[piece][m][ld0] = sum over k in piece of A[m][k] B[n][k], pieces
+// of sub_len inputs (a multiple of 16 when nsub > 1), nsub of them; A rows
+// (lda) and B rows (ldb) 16-byte aligned with K and both pitches multiples
+// of 4.  A workgroup holds the piece's slice of B in LDS:
+// fwd_skinny_lds_bytes(N, sub_len) must not exceed SKINNY_FWD_LDS.
+constexpr int SKINNY_FWD_PD = 8;          // k-groups of sample loads in flight
+constexpr int SKINNY_FWD_LDS = 160 * 1024;
+int64_t fwd_skinny_lds_bytes(int N, int sub_len);
+hipError_t launch_fwd_skinny(const GemmParamsT<float>& p, hipStream_t s);
+
 // Fold the per-piece tendencies of up to FOLD_GROUP_MAX layers in piece order,
 // store each sum as the tendency, and write the SGD step W = Win - scale * G,
 // b = bin - scale * g (W [M][ldw], b [M]).  Layer q's pieces: nshards shards

@@ -209,6 +209,130 @@ __global__ void __launch_bounds__(SK_NT, 2) skinny_dw_kernel(const SkinnyGroup g
     skinny_tile<1>(p, piece, tile, red, bred);
 }
 
+// ---------------------------------------------------------------------------
+// Forward pieces of a layer of at most SKINNY_MAX_UNITS units (section 3.2:
+// z[s][u] = sum over inputs n of x[s][n] W[u][n], over one piece of the
+// input range).  The k index is contiguous in both operands, so lane (r, g)
+// takes inputs k0 + 4 g .. + 3 of a row in one 16-byte access and uses them
+// in the 4 products of a k-group of 16 inputs.
+//
+// A workgroup of 8 waves owns one piece and 8 blocks of 16 samples.  It
+// first copies the piece's slice of W (every unit, the piece's inputs) into
+// LDS, at a row pitch of 4 (odd) floats so that the 16 rows of a fragment
+// read fall on distinct banks; after that one barrier each wave runs its
+// own sample block: the sample rows come from global memory, SKINNY_FWD_PD
+// k-groups ahead, the unit rows from LDS.
+// ---------------------------------------------------------------------------
+constexpr int SKF_NT = 512;   // 8 waves
+
+template <int NUB>
+__device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int sblk, int piece,
+                                                const float* ws, int pk) {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, gq = lane >> 4;
+  const int M = p.M, N = p.N;
+  const int s0 = 16 * sblk;
+  const int kbeg = piece * p.sub_len;
+  const int kend = min(kbeg + p.sub_len, p.K);
+  const int ngr = kend > kbeg ? (kend - kbeg + 15) >> 4 : 0;   // k-groups of 16 inputs
+  const bool xok = s0 + r < M;
+  const __amdgpu_buffer_rsrc_t ra = sk_rsrc(p.A + (int64_t)s0 * p.lda);
+  const int lda = (int)p.lda;
+
+  floatx4 acc[NUB];
+#pragma unroll
+  for (int u = 0; u < NUB; ++u) acc[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // k-group t: inputs kbeg + 16 t + 4 gq .. + 3 (whole vectors: the pieces
+  // start on multiples of 16 and the row length is a multiple of 4)
+  auto load = [&](int t) {
+    const int k = kbeg + 16 * t + 4 * gq;
+    return sk_load(ra, k < kend && xok ? 4u * (unsigned)(r * lda + k) : SK_OOB);
+  };
+  const float* wl = ws + r * pk + 4 * gq;
+  auto step = [&](const floatx4& xv, int t) {
+    floatx4 wv[NUB];
+#pragma unroll
+    for (int u = 0; u < NUB; ++u)
+      wv[u] = *reinterpret_cast<const floatx4*>(wl + 16 * u * pk + 16 * t);
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int u = 0; u < NUB; ++u)
+        acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt], wv[u][tt], acc[u], 0, 0, 0);
+  };
+  constexpr int PD = SKINNY_FWD_PD;
+  floatx4 xv[PD];
+#pragma unroll
+  for (int d = 0; d < PD; ++d) xv[d] = load(d);
+  int t = 0;
+  for (; t + PD <= ngr; t += PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      step(xv[d], t + d);
+      xv[d] = load(t + d + PD);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < PD - 1; ++d)
+    if (t + d < ngr) step(xv[d], t + d);
+
+  // accumulator register v of lane (r, gq): sample s0 + 4 gq + v, unit 16 u + r
+  float* out = p.partial + (int64_t)piece * p.pstride;
+#pragma unroll
+  for (int u = 0; u < NUB; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = s0 + 4 * gq + v;
+      if (m < M && 16 * u + r < N) out[(int64_t)m * p.ld0 + 16 * u + r] = acc[u][v];
+    }
+}
+
+__global__ void __launch_bounds__(SKF_NT) fwd_skinny_kernel(const GemmParamsT<float> p, int pk) {
+  extern __shared__ floatx4 ws4[];
+  float* ws = reinterpret_cast<float*>(ws4);
+  // workgroup b: piece b % nsub, sample blocks 8 (b / nsub) .. + 7
+  const int piece = blockIdx.x % p.nsub;
+  const int sblk = 8 * (blockIdx.x / p.nsub) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+  // the piece's slice of W: row u, inputs kbeg .. kend - 1 at ws[u * pk + ..],
+  // zeros up to the end of the last k-group (their products meet the zeros
+  // that the sample loads past kend return)
+  const int kbeg = piece * p.sub_len;
+  const int kend = min(kbeg + p.sub_len, p.K);
+  const int len4 = 4 * ((kend - kbeg + 15) >> 4);
+  const int total = p.N * len4;
+  const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + kbeg);
+  const int ldb = (int)p.ldb;
+  constexpr int BATCH = 16;   // 16-byte loads per thread in flight at once
+  for (int i0 = 0; i0 < total; i0 += BATCH * SKF_NT) {
+    floatx4 v[BATCH];
+    int at[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int i = i0 + j * SKF_NT + (int)threadIdx.x;
+      const int u = i / len4, c = i - u * len4;
+      at[j] = i < total ? u * pk + 4 * c : -1;
+      v[j] = sk_load(rb, i < total && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
+    }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j)
+      if (at[j] >= 0) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
+  }
+  __syncthreads();
+
+  if (16 * sblk >= p.M) return;
+  switch ((p.N + 15) >> 4) {
+    case 1: fwd_skinny_tile<1>(p, sblk, piece, ws, pk); break;
+    case 2: fwd_skinny_tile<2>(p, sblk, piece, ws, pk); break;
+    case 3: fwd_skinny_tile<3>(p, sblk, piece, ws, pk); break;
+    case 4: fwd_skinny_tile<4>(p, sblk, piece, ws, pk); break;
+    case 5: fwd_skinny_tile<5>(p, sblk, piece, ws, pk); break;
+    case 6: fwd_skinny_tile<6>(p, sblk, piece, ws, pk); break;
+    case 7: fwd_skinny_tile<7>(p, sblk, piece, ws, pk); break;
+    default: fwd_skinny_tile<8>(p, sblk, piece, ws, pk); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_dw_skinny_group(SkinnyGroup g, hipStream_t s) {
@@ -236,6 +360,49 @@ hipError_t launch_dw_skinny_group(SkinnyGroup g, hipStream_t s) {
   for (int q = g.n + 1; q <= GEMM_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
   if (g.start[g.n] <= 0) return hipErrorInvalidValue;
   return launch_k(skinny_dw_kernel, dim3((unsigned)g.start[g.n]), dim3(SK_NT), 0, s, g);
+}
+
+int fwd_skinny_pitch(int sub_len) {
+  // whole k-groups, then a multiple of 4 floats whose quarter is odd: rows
+  // r = 0..15 of a 16-byte fragment read start in 16 distinct groups of 4
+  // banks
+  const int q = 4 * ((sub_len + 15) / 16);
+  return 4 * (q % 2 == 1 ? q : q + 1);
+}
+
+int64_t fwd_skinny_lds_bytes(int N, int sub_len) {
+  return (int64_t)16 * ((N + 15) / 16) * fwd_skinny_pitch(sub_len) * 4;
+}
+
+hipError_t launch_fwd_skinny(const GemmParamsT<float>& p, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0 || p.N > SKINNY_MAX_UNITS || p.K <= 0 || p.nsub <= 0)
+    return hipErrorInvalidValue;
+  // pieces after the first start on whole k-groups; 16-byte row loads
+  if (p.sub_len <= 0 || (p.nsub > 1 && p.sub_len % 16 != 0) || (int64_t)p.nsub * p.sub_len < p.K ||
+      (int64_t)(p.nsub - 1) * p.sub_len >= p.K)
+    return hipErrorInvalidValue;
+  if (p.K % 4 != 0 || p.lda % 4 != 0 || p.ldb % 4 != 0 || p.lda < p.K || p.ldb < p.K ||
+      p.ld0 < p.N)
+    return hipErrorInvalidValue;
+  if ((reinterpret_cast<uintptr_t>(p.A) & 15) != 0 || (reinterpret_cast<uintptr_t>(p.B) & 15) != 0)
+    return hipErrorInvalidValue;
+  // 32-bit offsets: 16 rows of A past the block's first row, every row of B
+  if ((int64_t)16 * p.lda * 4 >= (int64_t)SK_OOB || (int64_t)p.N * p.ldb * 4 >= (int64_t)SK_OOB)
+    return hipErrorInvalidValue;
+  const int64_t lds = fwd_skinny_lds_bytes(p.N, p.sub_len);
+  if (lds > SKINNY_FWD_LDS) return hipErrorInvalidValue;
+  const int64_t groups = ((int64_t)p.M + 127) / 128;
+  if (groups * p.nsub > 0x7fffffff) return hipErrorInvalidValue;
+  static bool attr_set = false;   // the same for every device of the process
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fwd_skinny_kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             SKINNY_FWD_LDS);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  return launch_k(fwd_skinny_kernel, dim3((unsigned)(groups * p.nsub)), dim3(SKF_NT),
+                  (unsigned)lds, s, p, fwd_skinny_pitch(p.sub_len));
 }
 
 }  // namespace nf
