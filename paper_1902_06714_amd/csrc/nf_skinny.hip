@@ -9,19 +9,22 @@
 // into matrix-core operands, with no LDS staging and no barrier in the loop:
 // in a 16x16x4 product lane (r, g) supplies row r of A and column r of B at
 // input index g, so the 4 values of a lane's vector go to 4 different
-// products.  Unit 4 r + e of a group of 64 is row r of unit block e, input
-// 4 r + e' of a tile of 64 is column r of input block e', and input index g
-// is sample 4 j + g of k-step j.  A wave holds the 4 x 4 blocks of each
-// group of 64 units (one or two groups) against one tile of 64 inputs and
-// per k-step of 4 samples issues one 16-byte load per unit group and one for
-// the inputs (each a 4 rows x 256 bytes pattern) for 16 products per unit
-// group.  SKINNY_PD k-steps of loads are in flight.
+// products.  Unit 4 r + e of a segment of 64 units is row r of unit block e;
+// a layer's last units take a segment of 32 (8-byte loads, 2 blocks) and / or
+// of 16 (4-byte loads, 1 block), so a layer of d units costs ceil(d / 16)
+// blocks (7 for 100 units).  The inputs are cut the same way: tiles of 64
+// (4 blocks), the last tile ceil(rest / 16) blocks.  Input index g of the
+// products is sample 4 j + g of k-step j.  A wave holds every (unit block,
+// input block) of its tile and per k-step of 4 samples issues one load per
+// segment of each side (a 4 rows x 256 bytes pattern for a 64-wide
+// segment).  SKINNY_PD k-steps of loads are in flight.
 //
 // A workgroup of 4 waves owns one (piece, input tile): wave w takes the w-th
 // quarter of the piece's k-steps, and the four partial sums are added
-// through LDS in wave order at the end, one unit group at a time.  A tile-0
-// workgroup also sums the delta columns (the bias tendency): each lane over
-// its samples, then over the 4 lanes of a unit, then over the waves.
+// through LDS in wave order at the end, four unit blocks at a time.  A
+// tile-0 workgroup also sums the delta columns (the bias tendency): each
+// lane over its samples, then over the 4 lanes of a unit, then over the
+// waves.
 //
 // Workgroups go round robin over the 8 XCDs (workgroup b runs on XCD b mod
 // 8).  XCD x takes pieces x, x + 8, ... of a layer, each with all of its
@@ -40,9 +43,8 @@ namespace {
 
 constexpr int SK_NT = 256;                 // 4 waves
 constexpr int SK_TN = 64;                  // inputs per tile
-constexpr int SK_TU = 64;                  // units per group
 constexpr unsigned SK_OOB = 0x7ffffff0u;   // buffer length: offsets past it read 0
-static_assert(SKINNY_MAX_UNITS <= 2 * SK_TU, "two unit groups at most");
+static_assert(SKINNY_MAX_UNITS <= 128, "at most 8 unit blocks");
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t sk_rsrc(const float* base) {
   return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)SK_OOB, 0x00020000);
@@ -52,11 +54,66 @@ __device__ __forceinline__ floatx4 sk_load(__amdgpu_buffer_rsrc_t rs, unsigned o
   return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
 }
 
-// One workgroup's (piece, input tile) with NG groups of 64 units (the
-// layer's units rounded up).
-template <int NG>
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ floatx2 sk_load2(__amdgpu_buffer_rsrc_t rs, unsigned off) {
+  return __builtin_bit_cast(floatx2, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+}
+__device__ __forceinline__ float sk_load1(__amdgpu_buffer_rsrc_t rs, unsigned off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+}
+
+// The blocks of one side (units or inputs) of a workgroup's tile: S4
+// segments of 64 rows read with 16-byte loads (row 4 r + e of a segment is
+// row r of its block e), then S2 <= 1 segment of 32 rows read with 8-byte
+// loads (row 2 r + e: block e), then S1 <= 1 segment of 16 rows read with
+// 4-byte loads (row r).  A side of d rows takes ceil(d / 16) blocks.
+template <int S4, int S2, int S1>
+struct SkSide {
+  static constexpr int NB = 4 * S4 + 2 * S2 + S1;
+  static constexpr int B2 = 64 * S4, B1 = 64 * S4 + 32 * S2;   // first rows of the segments
+  // row of block b that lane row r supplies
+  __device__ static int row(int b, int r) {
+    if (b < 4 * S4) return 64 * (b >> 2) + 4 * r + (b & 3);
+    if (b < 4 * S4 + 2 * S2) return B2 + 2 * r + (b - 4 * S4);
+    return B1 + r;
+  }
+  struct Regs {
+    floatx4 v4[S4 > 0 ? S4 : 1];
+    floatx2 v2;
+    float v1;
+  };
+  // one sample row's values of this lane: rows < lim are read at byte
+  // offset base + 4 row; ok false reads zeros
+  __device__ static void load(Regs& g, __amdgpu_buffer_rsrc_t rs, unsigned base, int r, int lim,
+                              bool ok) {
+#pragma unroll
+    for (int i = 0; i < S4; ++i) {
+      const int e = 64 * i + 4 * r;
+      g.v4[i] = sk_load(rs, ok && e < lim ? base + 4u * (unsigned)e : SK_OOB);
+    }
+    if constexpr (S2 > 0) {
+      const int e = B2 + 2 * r;
+      g.v2 = sk_load2(rs, ok && e < lim ? base + 4u * (unsigned)e : SK_OOB);
+    }
+    if constexpr (S1 > 0) {
+      const int e = B1 + r;
+      g.v1 = sk_load1(rs, ok && e < lim ? base + 4u * (unsigned)e : SK_OOB);
+    }
+  }
+  // the value of block b
+  __device__ static float at(const Regs& g, int b) {
+    if (b < 4 * S4) return g.v4[b >> 2][b & 3];
+    if (b < 4 * S4 + 2 * S2) return g.v2[b - 4 * S4];
+    return g.v1;
+  }
+};
+
+// One workgroup's (piece, input tile): unit side U against input side X.
+template <class U, class X>
 __device__ __forceinline__ void skinny_tile(const GemmParamsT<float>& p, int piece, int tile,
                                             floatx4 (*red)[16][64], float (*bred)[SKINNY_MAX_UNITS]) {
+  constexpr int NU = U::NB, NX = X::NB;
   const int M = p.M, N = p.N;
   const int tid = threadIdx.x, lane = tid & 63;
   // the wave index, known to the compiler as uniform: the k-steps and so
@@ -73,61 +130,47 @@ __device__ __forceinline__ void skinny_tile(const GemmParamsT<float>& p, int pie
   const int nks = kend > kbeg ? (kend - kbeg + 3) >> 2 : 0;   // k-steps of 4 samples
   const int qk = (nks + 3) >> 2;
   const int j0 = min(nks, w * qk), j1 = min(nks, j0 + qk);
-
-  // this lane's columns: units 64 c + 4 r .. + 3 of delta (group c), inputs
-  // n0 + 4 r .. + 3
-  bool dok[NG];
-  unsigned doff[NG];
-#pragma unroll
-  for (int c = 0; c < NG; ++c) {
-    dok[c] = SK_TU * c + 4 * r < M;
-    doff[c] = 4u * (unsigned)(gq * (int)p.lda + SK_TU * c + 4 * r);
-  }
-  const bool xok = n0 + 4 * r < N;
   const int lda = (int)p.lda, ldb = (int)p.ldb;
-  const unsigned xoff = 4u * (unsigned)(gq * ldb + n0 + 4 * r);
+  const unsigned dbase = 4u * (unsigned)(gq * lda), xbase = 4u * (unsigned)(gq * ldb + n0);
 
-  floatx4 acc[NG][4][4];
+  floatx4 acc[NU][NX];
 #pragma unroll
-  for (int c = 0; c < NG; ++c)
+  for (int a = 0; a < NU; ++a)
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int b = 0; b < NX; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float bsum[NU];
 #pragma unroll
-      for (int f = 0; f < 4; ++f) acc[c][e][f] = floatx4{0.f, 0.f, 0.f, 0.f};
-  floatx4 bsum[NG];
-#pragma unroll
-  for (int c = 0; c < NG; ++c) bsum[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int a = 0; a < NU; ++a) bsum[a] = 0.f;
 
   struct Step {
-    floatx4 d[NG], x;
+    typename U::Regs d;
+    typename X::Regs x;
   };
   // k-step j: samples kbeg + 4 j + gq; past j1 or kend the loads read zeros
   auto load = [&](Step& st, int j) {
     const int s0 = kbeg + 4 * j;
     const bool ok = j < j1 && s0 + gq < kend;
-    const __amdgpu_buffer_rsrc_t ra = sk_rsrc(p.A + (int64_t)s0 * lda);
-#pragma unroll
-    for (int c = 0; c < NG; ++c) st.d[c] = sk_load(ra, ok && dok[c] ? doff[c] : SK_OOB);
-    st.x = sk_load(sk_rsrc(p.B + (int64_t)s0 * ldb), ok && xok ? xoff : SK_OOB);
+    U::load(st.d, sk_rsrc(p.A + (int64_t)s0 * lda), dbase, r, M, ok);
+    X::load(st.x, sk_rsrc(p.B + (int64_t)s0 * ldb), xbase, r, N - n0, ok);
   };
   auto step = [&](const Step& st) {
 #pragma unroll
-    for (int c = 0; c < NG; ++c)
+    for (int a = 0; a < NU; ++a)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-#pragma unroll
-        for (int f = 0; f < 4; ++f)
-          acc[c][e][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(st.d[c][e], st.x[f], acc[c][e][f], 0, 0, 0);
+      for (int b = 0; b < NX; ++b)
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(U::at(st.d, a), X::at(st.x, b), acc[a][b],
+                                                         0, 0, 0);
     if (do_bias) {
 #pragma unroll
-      for (int c = 0; c < NG; ++c) bsum[c] += st.d[c];
+      for (int a = 0; a < NU; ++a) bsum[a] += U::at(st.d, a);
     }
   };
 
-  // SKINNY_PD k-steps of loads in flight; whole groups load unconditionally
-  // (past the wave's range the loads read zeros), so each wait is for
-  // exactly the k-step needed
-  constexpr int PD = SKINNY_PD;
+  // SKINNY_PD k-steps of loads in flight (one fewer with all 32 blocks,
+  // whose accumulators fill half the registers); whole groups load
+  // unconditionally (past the wave's range the loads read zeros), so each
+  // wait is for exactly the k-step needed
+  constexpr int PD = NU * NX > 28 ? SKINNY_PD - 1 : SKINNY_PD;
   Step st[PD];
 #pragma unroll
   for (int d = 0; d < PD; ++d) load(st[d], j0 + d);
@@ -146,38 +189,56 @@ __device__ __forceinline__ void skinny_tile(const GemmParamsT<float>& p, int pie
   if (do_bias) {
     // lanes r, r + 16, r + 32, r + 48 hold the same units
 #pragma unroll
-    for (int c = 0; c < NG; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float s = bsum[c][e];
-        s += __shfl_xor(s, 16);
-        s += __shfl_xor(s, 32);
-        if (gq == 0) bred[w][SK_TU * c + 4 * r + e] = s;
-      }
+    for (int a = 0; a < NU; ++a) {
+      float t = bsum[a];
+      t += __shfl_xor(t, 16);
+      t += __shfl_xor(t, 32);
+      if (gq == 0) bred[w][U::row(a, r)] = t;
+    }
   }
 
-  // One unit group at a time: the 4 input blocks f of a lane's (unit block
-  // e, accumulator row v) go to LDS as one vector, slot 4 e + v; wave w then
-  // sums slots 4 w .. 4 w + 3 over the waves in wave order and stores rows
-  // 64 c + 16 gq + 4 v + w, inputs n0 + 4 r .. + 3.
+  // Unit blocks 4 c .. 4 c + 3 at a time: the input blocks b of a lane's
+  // (unit block a, accumulator row v) go to LDS as one vector, slot
+  // 4 (a - 4 c) + v; wave w then sums the slots of unit block 4 c + w over
+  // the waves in wave order.  Accumulator row v of lane (r, gq) is row
+  // 4 gq + v of the block (the unit), column r (the input).
   float* out = p.partial + (int64_t)piece * p.pstride;
 #pragma unroll
-  for (int c = 0; c < NG; ++c) {
-    if (c > 0) __syncthreads();   // the previous group's sums are read
+  for (int c = 0; c < (NU + 3) / 4; ++c) {
+    if (c > 0) __syncthreads();   // the previous blocks' sums are read
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        red[w][4 * e + v][lane] =
-            floatx4{acc[c][e][0][v], acc[c][e][1][v], acc[c][e][2][v], acc[c][e][3][v]};
-    __syncthreads();
-    if (xok) {
+    for (int a = 4 * c; a < 4 * c + 4 && a < NU; ++a)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int m = SK_TU * c + 16 * gq + 4 * v + w;
+        floatx4 t = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int b = 0; b < NX; ++b) t[b] = acc[a][b][v];
+        red[w][4 * (a - 4 * c) + v][lane] = t;
+      }
+    __syncthreads();
+    const int a = 4 * c + w;
+    if (a < NU) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
         const int i = 4 * w + v;
         const floatx4 o = ((red[0][i][lane] + red[1][i][lane]) + red[2][i][lane]) + red[3][i][lane];
-        if (m < M) *reinterpret_cast<floatx4*>(out + (int64_t)m * p.ld0 + n0 + 4 * r) = o;
+        int m = 0;
+        // U::row with a wave-uniform block index
+#pragma unroll
+        for (int aa = 4 * c; aa < 4 * c + 4 && aa < NU; ++aa)
+          if (aa == a) m = U::row(aa, 4 * gq + v);
+        if (m >= M) continue;
+        float* orow = out + (int64_t)m * p.ld0 + n0;
+        if constexpr (X::NB == 4 && X::B2 == 64) {
+          // one 16-byte segment: inputs 4 r .. 4 r + 3
+          if (4 * r < N - n0) *reinterpret_cast<floatx4*>(orow + 4 * r) = o;
+        } else {
+#pragma unroll
+          for (int b = 0; b < NX; ++b) {
+            const int n = X::row(b, r);
+            if (n < N - n0) orow[n] = o[b];
+          }
+        }
       }
     }
   }
@@ -186,8 +247,22 @@ __device__ __forceinline__ void skinny_tile(const GemmParamsT<float>& p, int pie
         ((bred[0][tid] + bred[1][tid]) + bred[2][tid]) + bred[3][tid];
 }
 
+// the tile's input side: a whole tile of 64 inputs, or the last tile's
+// ceil(rest / 16) blocks
+template <class U>
+__device__ __forceinline__ void skinny_tile_x(const GemmParamsT<float>& p, int piece, int tile,
+                                              int nx, floatx4 (*red)[16][64],
+                                              float (*bred)[SKINNY_MAX_UNITS]) {
+  switch (nx) {
+    case 1: skinny_tile<U, SkSide<0, 0, 1>>(p, piece, tile, red, bred); break;
+    case 2: skinny_tile<U, SkSide<0, 1, 0>>(p, piece, tile, red, bred); break;
+    case 3: skinny_tile<U, SkSide<0, 1, 1>>(p, piece, tile, red, bred); break;
+    default: skinny_tile<U, SkSide<1, 0, 0>>(p, piece, tile, red, bred); break;
+  }
+}
+
 __global__ void __launch_bounds__(SK_NT, 2) skinny_dw_kernel(const SkinnyGroup g) {
-  // the four waves' accumulators of one unit group, [wave][value][lane],
+  // the four waves' accumulators of four unit blocks, [wave][slot][lane],
   // and the bias sums
   __shared__ floatx4 red[4][16][64];
   __shared__ float bred[4][SKINNY_MAX_UNITS];
@@ -203,10 +278,18 @@ __global__ void __launch_bounds__(SK_NT, 2) skinny_dw_kernel(const SkinnyGroup g
   const int piece = (r0 & 7) + 8 * (slot / ntile);
   const int tile = slot % ntile;
   if (piece >= g.npieces[q]) return;
-  if (p.M > SK_TU)
-    skinny_tile<2>(p, piece, tile, red, bred);
-  else
-    skinny_tile<1>(p, piece, tile, red, bred);
+  const int rest = p.N - tile * SK_TN;
+  const int nx = rest >= SK_TN ? 4 : (rest + 15) >> 4;
+  switch ((p.M + 15) >> 4) {
+    case 1: skinny_tile_x<SkSide<0, 0, 1>>(p, piece, tile, nx, red, bred); break;
+    case 2: skinny_tile_x<SkSide<0, 1, 0>>(p, piece, tile, nx, red, bred); break;
+    case 3: skinny_tile_x<SkSide<0, 1, 1>>(p, piece, tile, nx, red, bred); break;
+    case 4: skinny_tile_x<SkSide<1, 0, 0>>(p, piece, tile, nx, red, bred); break;
+    case 5: skinny_tile_x<SkSide<1, 0, 1>>(p, piece, tile, nx, red, bred); break;
+    case 6: skinny_tile_x<SkSide<1, 1, 0>>(p, piece, tile, nx, red, bred); break;
+    case 7: skinny_tile_x<SkSide<1, 1, 1>>(p, piece, tile, nx, red, bred); break;
+    default: skinny_tile_x<SkSide<2, 0, 0>>(p, piece, tile, nx, red, bred); break;
+  }
 }
 
 // ---------------------------------------------------------------------------
