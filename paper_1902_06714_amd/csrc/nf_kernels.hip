@@ -379,8 +379,9 @@ gemm_group_kernel(const GemmGroupT<T> g) {
 // piece_1) + ...).  The loads of a batch of NB pieces issue together before
 // any is added (past the last piece a batch re-reads the last one and drops
 // it), so a fold of up to NB pieces waits for memory once, not once per
-// piece.  NB is the smallest of 4, 8, 16 that holds every piece, so folds of
-// few pieces (bandwidth-bound on large layers) read no extra bytes.
+// piece.  NB is the smallest of 4, 8, 16, 32 that holds every piece (32
+// past that), so folds of few pieces (bandwidth-bound on large layers) read
+// no extra bytes.
 template <int NB, class T, class Get>
 __device__ __forceinline__ T fold_pieces_nb(int nsub, int P, Get get) {
   T tot = T(0), piece = T(0);
@@ -415,7 +416,8 @@ __device__ __forceinline__ T fold_pieces(int nshards, int nsub, Get get) {
   const int P = nshards * nsub;
   if (P <= 4) return fold_pieces_nb<4, T>(nsub, P, get);
   if (P <= 8) return fold_pieces_nb<8, T>(nsub, P, get);
-  return fold_pieces_nb<16, T>(nsub, P, get);
+  if (P <= 16) return fold_pieces_nb<16, T>(nsub, P, get);
+  return fold_pieces_nb<32, T>(nsub, P, get);
 }
 
 template <class T>

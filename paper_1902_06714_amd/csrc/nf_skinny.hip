@@ -308,9 +308,9 @@ __global__ void __launch_bounds__(SK_NT, 2) skinny_dw_kernel(const SkinnyGroup g
 // ---------------------------------------------------------------------------
 constexpr int SKF_NT = 512;   // 8 waves
 
-template <int NUB>
+template <int NUB, class Stage>
 __device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int sblk, int piece,
-                                                const float* ws, int pk) {
+                                                const float* ws, int pk, Stage&& stage) {
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, gq = lane >> 4;
   const int M = p.M, N = p.N;
@@ -343,10 +343,15 @@ __device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int
       for (int u = 0; u < NUB; ++u)
         acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt], wv[u][tt], acc[u], 0, 0, 0);
   };
+  // the sample rows' first k-groups are requested before the W slice, so
+  // their latency passes while the slice is copied
   constexpr int PD = SKINNY_FWD_PD;
+  const bool has_rows = s0 < M;
   floatx4 xv[PD];
 #pragma unroll
   for (int d = 0; d < PD; ++d) xv[d] = load(d);
+  stage();
+  if (!has_rows) return;
   int t = 0;
   for (; t + PD <= ngr; t += PD) {
 #pragma unroll
@@ -377,42 +382,43 @@ __global__ void __launch_bounds__(SKF_NT) fwd_skinny_kernel(const GemmParamsT<fl
   const int piece = blockIdx.x % p.nsub;
   const int sblk = 8 * (blockIdx.x / p.nsub) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-  // the piece's slice of W: row u, inputs kbeg .. kend - 1 at ws[u * pk + ..],
-  // zeros up to the end of the last k-group (their products meet the zeros
-  // that the sample loads past kend return)
-  const int kbeg = piece * p.sub_len;
-  const int kend = min(kbeg + p.sub_len, p.K);
-  const int len4 = 4 * ((kend - kbeg + 15) >> 4);
-  const int total = p.N * len4;
-  const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + kbeg);
-  const int ldb = (int)p.ldb;
-  constexpr int BATCH = 16;   // 16-byte loads per thread in flight at once
-  for (int i0 = 0; i0 < total; i0 += BATCH * SKF_NT) {
-    floatx4 v[BATCH];
-    int at[BATCH];
+  // copy of the piece's slice of W: row u, inputs kbeg .. kend - 1 at
+  // ws[u * pk + ..], zeros up to the end of the last k-group (their products
+  // meet the zeros that the sample loads past kend return); every wave takes
+  // part, and the barrier ends it
+  auto stage = [&] {
+    const int kbeg = piece * p.sub_len;
+    const int kend = min(kbeg + p.sub_len, p.K);
+    const int len4 = 4 * ((kend - kbeg + 15) >> 4);
+    const int total = p.N * len4;
+    const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + kbeg);
+    const int ldb = (int)p.ldb;
+    constexpr int BATCH = 16;   // 16-byte loads per thread in flight at once
+    for (int i0 = 0; i0 < total; i0 += BATCH * SKF_NT) {
+      floatx4 v[BATCH];
+      int at[BATCH];
 #pragma unroll
-    for (int j = 0; j < BATCH; ++j) {
-      const int i = i0 + j * SKF_NT + (int)threadIdx.x;
-      const int u = i / len4, c = i - u * len4;
-      at[j] = i < total ? u * pk + 4 * c : -1;
-      v[j] = sk_load(rb, i < total && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
+      for (int j = 0; j < BATCH; ++j) {
+        const int i = i0 + j * SKF_NT + (int)threadIdx.x;
+        const int u = i / len4, c = i - u * len4;
+        at[j] = i < total ? u * pk + 4 * c : -1;
+        v[j] = sk_load(rb, i < total && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
+      }
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j)
+        if (at[j] >= 0) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
     }
-#pragma unroll
-    for (int j = 0; j < BATCH; ++j)
-      if (at[j] >= 0) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
-  }
-  __syncthreads();
-
-  if (16 * sblk >= p.M) return;
+    __syncthreads();
+  };
   switch ((p.N + 15) >> 4) {
-    case 1: fwd_skinny_tile<1>(p, sblk, piece, ws, pk); break;
-    case 2: fwd_skinny_tile<2>(p, sblk, piece, ws, pk); break;
-    case 3: fwd_skinny_tile<3>(p, sblk, piece, ws, pk); break;
-    case 4: fwd_skinny_tile<4>(p, sblk, piece, ws, pk); break;
-    case 5: fwd_skinny_tile<5>(p, sblk, piece, ws, pk); break;
-    case 6: fwd_skinny_tile<6>(p, sblk, piece, ws, pk); break;
-    case 7: fwd_skinny_tile<7>(p, sblk, piece, ws, pk); break;
-    default: fwd_skinny_tile<8>(p, sblk, piece, ws, pk); break;
+    case 1: fwd_skinny_tile<1>(p, sblk, piece, ws, pk, stage); break;
+    case 2: fwd_skinny_tile<2>(p, sblk, piece, ws, pk, stage); break;
+    case 3: fwd_skinny_tile<3>(p, sblk, piece, ws, pk, stage); break;
+    case 4: fwd_skinny_tile<4>(p, sblk, piece, ws, pk, stage); break;
+    case 5: fwd_skinny_tile<5>(p, sblk, piece, ws, pk, stage); break;
+    case 6: fwd_skinny_tile<6>(p, sblk, piece, ws, pk, stage); break;
+    case 7: fwd_skinny_tile<7>(p, sblk, piece, ws, pk, stage); break;
+    default: fwd_skinny_tile<8>(p, sblk, piece, ws, pk, stage); break;
   }
 }
 
