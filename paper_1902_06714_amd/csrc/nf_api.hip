@@ -413,9 +413,28 @@ struct DwPiece {
   int64_t pstride, off;                  // weights' pitch per piece, region offset
 };
 
+// Layers that the skinny tendency kernel takes (fp32, at most
+// SKINNY_MAX_UNITS units) share one launch of equal workgroups, one per
+// (piece, 64-input tile); they get one common sub-piece count, doubled only
+// while the doubled launch still fits two workgroups per CU (the kernel's
+// occupancy), so that no CU runs a workgroup after the others are done.
+// Other layers' pieces are sized by the 128 x 128 tiles of the general
+// kernel.
+bool dw_skinny_layer(const nf_net* n, int l) {
+  return n->dtype == nf::DT_F32 && n->layers[l].out <= nf::SKINNY_MAX_UNITS;
+}
+
 int64_t dw_plan(const nf_net* n, int64_t batch, int shards, std::vector<DwPiece>* pieces) {
   const int L = num_layers(n);
   const int64_t shard_len = batch / shards;
+  const int64_t ncu = n->ncu > 0 ? n->ncu : 256;
+  int64_t skinny_wg = 0;
+  for (int l = 1; l <= L; ++l)
+    if (dw_skinny_layer(n, l)) skinny_wg += (n->layers[l].in + 63) / 64 * shards;
+  int skinny_nsub = 1;
+  while (skinny_wg * skinny_nsub * 2 <= 2 * ncu && shard_len / (skinny_nsub * 2) >= 256 &&
+         skinny_nsub < 64 && (int64_t)shards * skinny_nsub * 2 <= 65535)
+    skinny_nsub *= 2;
   int64_t total = 0;
   pieces->clear();
   for (int l = L; l >= 1; --l) {
@@ -423,9 +442,12 @@ int64_t dw_plan(const nf_net* n, int64_t batch, int shards, std::vector<DwPiece>
     const int64_t M = ly.out, N = ly.in;
     int nsub = 1;
     const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    while (tiles * shards * nsub < 256 && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
-           (int64_t)shards * nsub * 2 <= 65535)
-      nsub *= 2;
+    if (dw_skinny_layer(n, l))
+      nsub = skinny_nsub;
+    else
+      while (tiles * shards * nsub < 256 && shard_len / (nsub * 2) >= 256 && nsub < 64 &&
+             (int64_t)shards * nsub * 2 <= 65535)
+        nsub *= 2;
     if (shards * nsub == 1) continue;
     const int64_t pstride = round_up(M * ly.ldw, kAlign);
     const int64_t nsplit = (int64_t)shards * nsub;
