@@ -164,6 +164,51 @@ def test_medium_edges(dims, acts, batch, shards, eta):
     _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 3)
 
 
+# the skinny kernels (fp32 layers of at most 128 units): unit counts that take
+# every combination of 64-, 32- and 16-row segments (1, 10, 16, 33, 49, 64,
+# 97, 100, 113, 127, 128), input tiles with tails of one to four blocks (20,
+# 36, 49, 97, 113, 788), the layer-1 forward over k pieces whose last piece is
+# short (788) or a single piece off a whole k-group (20, 36), shards of a
+# few samples (160 in 16: fewer k-steps than waves in a workgroup), and
+# layers in one launch with both one and several sub-pieces per shard
+SKINNY_EDGES = [
+    ((20, 113, 49, 10), ("tanh", "sigmoid", "sigmoid"), 500, 4, 0.5),
+    ((36, 128, 97, 33), ("sigmoid", "tanh", "gaussian"), 333, 3, 0.5),
+    ((788, 100, 16, 1), ("tanh", "sigmoid", "sigmoid"), 1000, 8, 1.0),
+    ((64, 64, 127, 100), ("tanh",), 2000, 2, 0.5),
+    ((100, 127, 64), ("sigmoid",), 160, 16, 2.0),
+    ((52, 97, 10), ("gaussian", "sigmoid"), 6000, 1, 0.5),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards,eta", SKINNY_EDGES)
+def test_skinny_edges(dims, acts, batch, shards, eta):
+    theta, X, Y = _problem(dims, 5 * sum(dims) + batch, batch * 3)
+    _compare_trajectory(dims, acts, theta, X, Y, batch, eta, shards, 3)
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards,eta", SKINNY_EDGES)
+def test_skinny_edges_take_the_skinny_kernels(dims, acts, batch, shards, eta):
+    """The cases above run where they are meant to: the tendency pieces of
+    every layer go to the skinny kernel, and so does the layer-1 forward of
+    the networks that take the per-sample medium kernel (W_2 .. W_L fit in its
+    LDS; 64-127-100 does not, and runs the general forward)."""
+    medium = dims != (64, 64, 127, 100)
+    theta, X, Y = _problem(dims, 5 * sum(dims) + batch, batch)
+    note(f"skinny routing dims={dims} batch={batch} shards={shards}")
+    with GpuNet(dims, acts, theta) as net:
+        net.nf.nf_profile(net.h, 1)
+        net.train_batch(to_dev(X), to_dev(Y), eta, shards)
+        names = {k["name"]: k["launches"] for k in net.nf.nf_profile_read(net.h)}
+        net.nf.nf_profile(net.h, 0)
+    assert names.get("dw_skinny") == 1, names
+    if medium:
+        assert names.get("fwd_skinny") == 1, names
+        assert not any(n.startswith("gemm") for n in names), names
+    else:
+        assert "fwd_skinny" not in names and "gemm_dw_partial_64x64" not in names, names
+
+
 def _random_cases(n=24, seed=20260):
     """Seeded network shapes across the narrow, medium and contraction paths:
     1 to 4 layers, widths 1 to 200 (narrow nets need every layer after the
