@@ -11,6 +11,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "nf.h"
@@ -413,15 +414,15 @@ struct DwPiece {
   int64_t pstride, off;                  // weights' pitch per piece, region offset
 };
 
-// Layers that the skinny tendency kernel takes (fp32, at most
-// SKINNY_MAX_UNITS units) share one launch of equal workgroups, one per
-// (piece, 64-input tile); they get one common sub-piece count, doubled only
+// Layers that the skinny tendency kernels take (at most SKINNY_MAX_UNITS
+// units) share one launch of equal workgroups, one per (piece, input tile of
+// 64 in fp32, 32 in fp64); they get one common sub-piece count, doubled only
 // while the doubled launch still fits two workgroups per CU (the kernel's
 // occupancy), so that no CU runs a workgroup after the others are done.
 // Other layers' pieces are sized by the 128 x 128 tiles of the general
 // kernel.
 bool dw_skinny_layer(const nf_net* n, int l) {
-  return n->dtype == nf::DT_F32 && n->layers[l].out <= nf::SKINNY_MAX_UNITS;
+  return n->layers[l].out <= nf::SKINNY_MAX_UNITS;
 }
 
 int64_t dw_plan(const nf_net* n, int64_t batch, int shards, std::vector<DwPiece>* pieces) {
@@ -429,8 +430,9 @@ int64_t dw_plan(const nf_net* n, int64_t batch, int shards, std::vector<DwPiece>
   const int64_t shard_len = batch / shards;
   const int64_t ncu = n->ncu > 0 ? n->ncu : 256;
   int64_t skinny_wg = 0;
+  const int64_t tile = n->dtype == nf::DT_F32 ? nf::SKINNY_TILE_F32 : nf::SKINNY_TILE_F64;
   for (int l = 1; l <= L; ++l)
-    if (dw_skinny_layer(n, l)) skinny_wg += (n->layers[l].in + 63) / 64 * shards;
+    if (dw_skinny_layer(n, l)) skinny_wg += (n->layers[l].in + tile - 1) / tile * shards;
   int skinny_nsub = 1;
   while (skinny_wg * skinny_nsub * 2 <= 2 * ncu && shard_len / (skinny_nsub * 2) >= 256 &&
          skinny_nsub < 64 && (int64_t)shards * skinny_nsub * 2 <= 65535)
@@ -639,9 +641,9 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
   if (pieces.empty()) return NF_OK;
 
   // the piece kernels, grouped by tile shape and B-row vector loads (layer
-  // order within a group), up to GEMM_GROUP_MAX layers per launch; fp32
-  // layers of at most SKINNY_MAX_UNITS units with 16-byte operand rows take
-  // the kernel that holds all of a layer's units in one workgroup
+  // order within a group), up to GEMM_GROUP_MAX layers per launch; layers of
+  // at most SKINNY_MAX_UNITS units with 16-byte operand rows take the skinny
+  // tendency kernel of their element type
   const int dtype = dtype_of<T>();
   std::vector<bool> done(pieces.size(), false);
   auto piece_params = [&](const Piece& pc) {
@@ -655,9 +657,9 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
     p.pbias = p.partial + (int64_t)shards * pc.nsub * pc.pstride;
     return p;
   };
-  if constexpr (sizeof(T) == 4) {
+  {
     {
-      nf::SkinnyGroup g{};
+      std::conditional_t<sizeof(T) == 4, nf::SkinnyGroup, nf::SkinnyGroup64> g{};
       double bytes = 0.0, flops = 0.0;
       for (size_t j = 0; j < pieces.size() && g.n < nf::GEMM_GROUP_MAX; ++j) {
         const Piece& pj = pieces[j];
@@ -671,8 +673,13 @@ nf_status run_backward_update(nf_net* n, const T* x, int64_t batch, double eta, 
         done[j] = true;
       }
       if (g.n > 0) {
-        nf_status st = timed(n, "dw_skinny", bytes, flops, s,
-                             [&] { return nf::launch_dw_skinny_group(g, s); });
+        nf_status st;
+        if constexpr (sizeof(T) == 4)
+          st = timed(n, "dw_skinny", bytes, flops, s,
+                     [&] { return nf::launch_dw_skinny_group(g, s); });
+        else
+          st = timed(n, "dw64_skinny", bytes, flops, s,
+                     [&] { return nf::launch_dw_skinny_group64(g, s); });
         if (st != NF_OK) return st;
       }
     }

@@ -147,6 +147,16 @@ struct SkinnyGroup {
   int n;
 };
 hipError_t launch_dw_skinny_group(SkinnyGroup g, hipStream_t s);
+// The same for fp64 layers (input tiles of 32, 16-byte loads of two doubles).
+struct SkinnyGroup64 {
+  GemmParamsT<double> p[GEMM_GROUP_MAX];
+  int start[GEMM_GROUP_MAX + 1];
+  int npieces[GEMM_GROUP_MAX];
+  int n;
+};
+hipError_t launch_dw_skinny_group64(SkinnyGroup64 g, hipStream_t s);
+// inputs per workgroup tile of the fp32 and fp64 tendency kernels
+constexpr int SKINNY_TILE_F32 = 64, SKINNY_TILE_F64 = 32;
 
 // Forward pieces of a fp32 layer of at most SKINNY_MAX_UNITS units (N),
 // operands loaded straight into the matrix cores (csrc/nf_skinny.hip):

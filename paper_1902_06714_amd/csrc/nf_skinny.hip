@@ -293,6 +293,219 @@ __global__ void __launch_bounds__(SK_NT, 2) skinny_dw_kernel(const SkinnyGroup g
 }
 
 // ---------------------------------------------------------------------------
+// fp64 tendency pieces: the same design on v_mfma_f64_16x16x4f64.  A 16-byte
+// load holds two doubles, so the wide segments are 32 rows (row 2 r + e of a
+// segment is row r of its block e) and the last 16 rows take 8-byte loads;
+// input tiles are 32 wide (two blocks).  The accumulator layout differs from
+// fp32: register v of lane (r, g) is row 4 v + g of the block.
+// ---------------------------------------------------------------------------
+typedef double doublex2 __attribute__((ext_vector_type(2)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ doublex2 sk_load_d2(__amdgpu_buffer_rsrc_t rs, unsigned off) {
+  return __builtin_bit_cast(doublex2, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+__device__ __forceinline__ double sk_load_d1(__amdgpu_buffer_rsrc_t rs, unsigned off) {
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+}
+
+// One side of an fp64 tile: S2 segments of 32 rows (16-byte loads), then S1
+// <= 1 segment of 16 rows (8-byte loads).
+template <int S2, int S1>
+struct SkSide64 {
+  static constexpr int NB = 2 * S2 + S1;
+  static constexpr int B1 = 32 * S2;
+  __device__ static int row(int b, int r) {
+    if (b < 2 * S2) return 32 * (b >> 1) + 2 * r + (b & 1);
+    return B1 + r;
+  }
+  struct Regs {
+    doublex2 v2[S2 > 0 ? S2 : 1];
+    double v1;
+  };
+  __device__ static void load(Regs& g, __amdgpu_buffer_rsrc_t rs, unsigned base, int r, int lim,
+                              bool ok) {
+#pragma unroll
+    for (int i = 0; i < S2; ++i) {
+      const int e = 32 * i + 2 * r;
+      g.v2[i] = sk_load_d2(rs, ok && e < lim ? base + 8u * (unsigned)e : SK_OOB);
+    }
+    if constexpr (S1 > 0) {
+      const int e = B1 + r;
+      g.v1 = sk_load_d1(rs, ok && e < lim ? base + 8u * (unsigned)e : SK_OOB);
+    }
+  }
+  __device__ static double at(const Regs& g, int b) {
+    if (b < 2 * S2) return g.v2[b >> 1][b & 1];
+    return g.v1;
+  }
+};
+
+constexpr int SK64_TN = SKINNY_TILE_F64;
+
+template <class U, class X>
+__device__ __forceinline__ void skinny_tile64(const GemmParamsT<double>& p, int piece, int tile,
+                                              doublex2 (*red)[16][64],
+                                              double (*bred)[SKINNY_MAX_UNITS]) {
+  constexpr int NU = U::NB, NX = X::NB;
+  static_assert(NX <= 2, "two input blocks per tile");
+  const int M = p.M, N = p.N;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, gq = lane >> 4;
+  const int n0 = tile * SK64_TN;
+  const bool do_bias = tile == 0;
+
+  const int shard = piece / p.nsub, sub = piece % p.nsub;
+  const int sb = shard * p.shard_len;
+  const int kbeg = sb + sub * p.sub_len;
+  const int kend = min(kbeg + p.sub_len, sb + p.shard_len);
+  const int nks = kend > kbeg ? (kend - kbeg + 3) >> 2 : 0;
+  const int qk = (nks + 3) >> 2;
+  const int j0 = min(nks, w * qk), j1 = min(nks, j0 + qk);
+  const int lda = (int)p.lda, ldb = (int)p.ldb;
+  const unsigned dbase = 8u * (unsigned)(gq * lda), xbase = 8u * (unsigned)(gq * ldb + n0);
+
+  doublex4 acc[NU][NX];
+#pragma unroll
+  for (int a = 0; a < NU; ++a)
+#pragma unroll
+    for (int b = 0; b < NX; ++b) acc[a][b] = doublex4{0.0, 0.0, 0.0, 0.0};
+  double bsum[NU];
+#pragma unroll
+  for (int a = 0; a < NU; ++a) bsum[a] = 0.0;
+
+  struct Step {
+    typename U::Regs d;
+    typename X::Regs x;
+  };
+  auto load = [&](Step& st, int j) {
+    const int s0 = kbeg + 4 * j;
+    const bool ok = j < j1 && s0 + gq < kend;
+    U::load(st.d, sk_rsrc(reinterpret_cast<const float*>(p.A + (int64_t)s0 * lda)), dbase, r, M, ok);
+    X::load(st.x, sk_rsrc(reinterpret_cast<const float*>(p.B + (int64_t)s0 * ldb)), xbase, r,
+            N - n0, ok);
+  };
+  auto step = [&](const Step& st) {
+#pragma unroll
+    for (int a = 0; a < NU; ++a)
+#pragma unroll
+      for (int b = 0; b < NX; ++b)
+        acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(U::at(st.d, a), X::at(st.x, b), acc[a][b],
+                                                         0, 0, 0);
+    if (do_bias) {
+#pragma unroll
+      for (int a = 0; a < NU; ++a) bsum[a] += U::at(st.d, a);
+    }
+  };
+
+  constexpr int PD = SKINNY_PD;
+  Step st[PD];
+#pragma unroll
+  for (int d = 0; d < PD; ++d) load(st[d], j0 + d);
+  int j = j0;
+  for (; j + PD <= j1; j += PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      step(st[d]);
+      load(st[d], j + d + PD);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < PD - 1; ++d)
+    if (j + d < j1) step(st[d]);
+
+  if (do_bias) {
+#pragma unroll
+    for (int a = 0; a < NU; ++a) {
+      double t = bsum[a];
+      t += __shfl_xor(t, 16);
+      t += __shfl_xor(t, 32);
+      if (gq == 0) bred[w][U::row(a, r)] = t;
+    }
+  }
+
+  // Unit blocks 4 c .. 4 c + 3 at a time, as in fp32; accumulator register
+  // v of lane (r, gq) is row 4 v + gq of the block, column r.
+  double* out = p.partial + (int64_t)piece * p.pstride;
+#pragma unroll
+  for (int c = 0; c < (NU + 3) / 4; ++c) {
+    if (c > 0) __syncthreads();
+#pragma unroll
+    for (int a = 4 * c; a < 4 * c + 4 && a < NU; ++a)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        doublex2 t = doublex2{0.0, 0.0};
+#pragma unroll
+        for (int b = 0; b < NX; ++b) t[b] = acc[a][b][v];
+        red[w][4 * (a - 4 * c) + v][lane] = t;
+      }
+    __syncthreads();
+    const int a = 4 * c + w;
+    if (a < NU) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = 4 * w + v;
+        const doublex2 o = ((red[0][i][lane] + red[1][i][lane]) + red[2][i][lane]) + red[3][i][lane];
+        int m = 0;
+#pragma unroll
+        for (int aa = 4 * c; aa < 4 * c + 4 && aa < NU; ++aa)
+          if (aa == a) m = U::row(aa, 4 * v + gq);
+        if (m >= M) continue;
+        double* orow = out + (int64_t)m * p.ld0 + n0;
+#pragma unroll
+        for (int b = 0; b < NX; ++b) {
+          const int n = X::row(b, r);
+          if (n < N - n0) orow[n] = o[b];
+        }
+      }
+    }
+  }
+  if (do_bias && tid < M)
+    p.pbias[(int64_t)piece * M + tid] =
+        ((bred[0][tid] + bred[1][tid]) + bred[2][tid]) + bred[3][tid];
+}
+
+template <class U>
+__device__ __forceinline__ void skinny_tile64_x(const GemmParamsT<double>& p, int piece, int tile,
+                                                int nx, doublex2 (*red)[16][64],
+                                                double (*bred)[SKINNY_MAX_UNITS]) {
+  if (nx == 1)
+    skinny_tile64<U, SkSide64<0, 1>>(p, piece, tile, red, bred);
+  else
+    skinny_tile64<U, SkSide64<1, 0>>(p, piece, tile, red, bred);
+}
+
+__global__ void __launch_bounds__(SK_NT, 2) skinny_dw64_kernel(const SkinnyGroup64 g) {
+  __shared__ doublex2 red[4][16][64];
+  __shared__ double bred[4][SKINNY_MAX_UNITS];
+
+  const int b = blockIdx.x;
+  int q = 0;
+#pragma unroll
+  for (int i = 1; i < GEMM_GROUP_MAX; ++i) q += (i < g.n && b >= g.start[i]);
+  const GemmParamsT<double>& p = g.p[q];
+  const int ntile = (p.N + SK64_TN - 1) / SK64_TN;
+  const int r0 = b - g.start[q];
+  const int slot = r0 >> 3;
+  const int piece = (r0 & 7) + 8 * (slot / ntile);
+  const int tile = slot % ntile;
+  if (piece >= g.npieces[q]) return;
+  const int rest = p.N - tile * SK64_TN;
+  const int nx = rest >= SK64_TN ? 2 : (rest + 15) >> 4;
+  switch ((p.M + 15) >> 4) {
+    case 1: skinny_tile64_x<SkSide64<0, 1>>(p, piece, tile, nx, red, bred); break;
+    case 2: skinny_tile64_x<SkSide64<1, 0>>(p, piece, tile, nx, red, bred); break;
+    case 3: skinny_tile64_x<SkSide64<1, 1>>(p, piece, tile, nx, red, bred); break;
+    case 4: skinny_tile64_x<SkSide64<2, 0>>(p, piece, tile, nx, red, bred); break;
+    case 5: skinny_tile64_x<SkSide64<2, 1>>(p, piece, tile, nx, red, bred); break;
+    case 6: skinny_tile64_x<SkSide64<3, 0>>(p, piece, tile, nx, red, bred); break;
+    case 7: skinny_tile64_x<SkSide64<3, 1>>(p, piece, tile, nx, red, bred); break;
+    default: skinny_tile64_x<SkSide64<4, 0>>(p, piece, tile, nx, red, bred); break;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Forward pieces of a layer of at most SKINNY_MAX_UNITS units (section 3.2:
 // z[s][u] = sum over inputs n of x[s][n] W[u][n], over one piece of the
 // input range).  The k index is contiguous in both operands, so lane (r, g)
@@ -461,6 +674,30 @@ int fwd_skinny_pitch(int sub_len) {
 
 int64_t fwd_skinny_lds_bytes(int N, int sub_len) {
   return (int64_t)16 * ((N + 15) / 16) * fwd_skinny_pitch(sub_len) * 4;
+}
+
+hipError_t launch_dw_skinny_group64(SkinnyGroup64 g, hipStream_t s) {
+  if (g.n < 1 || g.n > GEMM_GROUP_MAX) return hipErrorInvalidValue;
+  g.start[0] = 0;
+  for (int q = 0; q < g.n; ++q) {
+    const GemmParamsT<double>& p = g.p[q];
+    if (p.M <= 0 || p.M > SKINNY_MAX_UNITS || p.N <= 0 || p.K < 0 || g.npieces[q] <= 0)
+      return hipErrorInvalidValue;
+    if (p.nsub <= 0 || g.npieces[q] % p.nsub != 0) return hipErrorInvalidValue;
+    // 16-byte loads of two doubles: even pitches, rows 16-byte aligned
+    if (p.lda % 2 != 0 || p.ldb % 2 != 0 || p.lda < 2 * ((p.M + 1) / 2) ||
+        p.ldb < 2 * ((p.N + 1) / 2) || p.ld0 < p.N)
+      return hipErrorInvalidValue;
+    if ((reinterpret_cast<uintptr_t>(p.A) & 15) != 0 || (reinterpret_cast<uintptr_t>(p.B) & 15) != 0)
+      return hipErrorInvalidValue;
+    const int64_t ld = p.lda > p.ldb ? p.lda : p.ldb;
+    if ((int64_t)4 * ld * 8 >= (int64_t)SK_OOB) return hipErrorInvalidValue;
+    const int ntile = (p.N + SK64_TN - 1) / SK64_TN;
+    g.start[q + 1] = g.start[q] + 8 * ((g.npieces[q] + 7) / 8) * ntile;
+  }
+  for (int q = g.n + 1; q <= GEMM_GROUP_MAX; ++q) g.start[q] = g.start[g.n];
+  if (g.start[g.n] <= 0) return hipErrorInvalidValue;
+  return launch_k(skinny_dw64_kernel, dim3((unsigned)g.start[g.n]), dim3(SK_NT), 0, s, g);
 }
 
 hipError_t launch_fwd_skinny(const GemmParamsT<float>& p, hipStream_t s) {

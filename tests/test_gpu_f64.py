@@ -173,6 +173,42 @@ def test_f64_medium(dims, acts, batch, shards):
     assert not fails, "\n".join(fails[:20])
 
 
+# the fp64 skinny tendency kernel: unit counts over every combination of
+# 32- and 16-row segments (1, 10, 16, 33, 49, 97, 100, 113, 127, 128), input
+# tiles of 32 with one- and two-block tails (20, 36, 49, 97, 113, 788), shards
+# of a few samples, and a check that the launches take that kernel
+SKINNY64 = [
+    ((20, 113, 49, 10), ("tanh", "sigmoid", "sigmoid"), 500, 4),
+    ((36, 128, 97, 33), ("sigmoid", "tanh", "gaussian"), 333, 3),
+    ((788, 100, 16, 1), ("tanh", "sigmoid", "sigmoid"), 1000, 8),
+    ((100, 127, 64), ("sigmoid",), 160, 16),
+]
+
+
+@pytest.mark.parametrize("dims,acts,batch,shards", SKINNY64)
+def test_f64_skinny_tendencies(dims, acts, batch, shards):
+    acts_full = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
+    theta, X, Y = _problem(dims, 7 * sum(dims) + batch, batch * 2)
+    note(f"f64 skinny dims={dims} batch={batch} shards={shards}")
+    ref = theta
+    fails = []
+    with Net64(dims, acts, theta) as net:
+        xd, yd = to_dev64(X), to_dev64(Y)
+        for t in range(2):
+            sl = slice(t * batch, (t + 1) * batch)
+            net.nf.nf_profile(net.h, 1)
+            net.nf.nf_train_batch_f64(net.h, xd[sl], yd[sl], 0.5, shards)
+            names = {k["name"]: k["launches"] for k in net.nf.nf_profile_read(net.h)}
+            net.nf.nf_profile(net.h, 0)
+            assert names.get("dw64_skinny") == 1, names
+            assert not any("dw_partial" in k for k in names), names
+            ref, G = mlp.train_batch(ref, dims, acts_full, X[sl], Y[sl], 0.5, shards,
+                                     precision="f64")
+            fails += [f"step {t}: {m}" for m in _check(net.params(), ref, dims, "params")]
+            fails += [f"step {t}: {m}" for m in _check(net.grads(), G, dims, "grads")]
+    assert not fails, "\n".join(fails[:20])
+
+
 @pytest.mark.parametrize("dims,acts,batch,shards", NARROW64)
 def test_f64_narrow(dims, acts, batch, shards):
     acts_full = list(acts) * (len(dims) - 1) if len(acts) == 1 else list(acts)
