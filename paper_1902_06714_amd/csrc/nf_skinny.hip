@@ -1,7 +1,10 @@
+// Kernels for contractions one side of which is a layer of at most
+// SKINNY_MAX_UNITS units, e.g. the 100-unit layers of a 784-100-100-10
+// network: the tendency pieces in fp32 and fp64, and the layer-1 forward
+// pieces in fp32.
+//
 // Tendency pieces (section 3.3: dC/dW_l = delta_l^T a_{l-1}, dC/db_l = the
-// column sums of delta_l, each over one piece of the batch) of fp32 layers
-// with at most SKINNY_MAX_UNITS units, e.g. the 100-unit layers of a
-// 784-100-100-10 network.
+// column sums of delta_l, each over one piece of the batch), fp32:
 //
 // Both operands are sample-major (delta_l[s][u], a_{l-1}[s][n]) and the sum
 // runs over samples, so a 16-byte load gives a lane 4 consecutive units (or
@@ -42,7 +45,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 namespace {
 
 constexpr int SK_NT = 256;                 // 4 waves
-constexpr int SK_TN = 64;                  // inputs per tile
+constexpr int SK_TN = SKINNY_TILE_F32;     // inputs per tile
 constexpr unsigned SK_OOB = 0x7ffffff0u;   // buffer length: offsets past it read 0
 static_assert(SKINNY_MAX_UNITS <= 128, "at most 8 unit blocks");
 
