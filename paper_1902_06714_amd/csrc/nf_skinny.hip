@@ -36,6 +36,8 @@
 //
 // The per-piece sums land in the same [piece][M][ld0] + [piece][M] layout as
 // the general tendency pieces, and fold_sgd_kernel folds them in piece order.
+#include <atomic>
+
 #include "nf_internal.h"
 
 namespace nf {
@@ -722,13 +724,18 @@ hipError_t launch_fwd_skinny(const GemmParamsT<float>& p, hipStream_t s) {
   if (lds > SKINNY_FWD_LDS) return hipErrorInvalidValue;
   const int64_t groups = ((int64_t)p.M + 127) / 128;
   if (groups * p.nsub > 0x7fffffff) return hipErrorInvalidValue;
-  static bool attr_set = false;   // the same for every device of the process
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fwd_skinny_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             SKINNY_FWD_LDS);
+  // the kernel may use more than the default dynamic LDS: allowed once per
+  // device (any thread may get there first; the call is idempotent)
+  constexpr int kDevices = 64;
+  static std::atomic<bool> attr_set[kDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kDevices || !attr_set[dev].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(fwd_skinny_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, SKINNY_FWD_LDS);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    if (dev >= 0 && dev < kDevices) attr_set[dev].store(true, std::memory_order_release);
   }
   return launch_k(fwd_skinny_kernel, dim3((unsigned)(groups * p.nsub)), dim3(SKF_NT),
                   (unsigned)lds, s, p, fwd_skinny_pitch(p.sub_len));
