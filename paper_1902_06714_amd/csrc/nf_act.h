@@ -62,8 +62,11 @@ __device__ __forceinline__ void act_eval(int act, T z, T& f, T& fp) {
       const T e = act_exp(T(-2) * az);
       const T r = act_rcp12(one + e);
       if constexpr (sizeof(T) == 4) {
+        // both forms for every z and a select: a branch would run both
+        // wherever a wavefront holds pre-activations on both sides of 1/2
+        const T small = act_tanh_small(z);
         const T big = copysignf((one - e) * r, z);
-        f = az < T(0.5) ? act_tanh_small(z) : big;
+        f = az < T(0.5) ? small : big;
       } else {
         f = act_tanh(z);
       }

@@ -114,10 +114,15 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
   constexpr int VW = 16 / sizeof(T);                  // elements per 16-byte load
   constexpr int LPR = MEDIUM_WIDTH / VW;              // lanes per staged weight row
   constexpr int SROWS = M_THREADS / LPR;              // weight rows per load
-  __shared__ __attribute__((aligned(16))) T wl[M::WLDS];  // W_2 .. W_L, padded
-  __shared__ T hs[2][TS][M_HP];                           // activations, deltas
-  __shared__ T bl[L][MEDIUM_WIDTH];                       // b_1 .. b_L
-  __shared__ float4 spare;
+  // one LDS block: the activations and deltas first, so that their reads
+  // take immediate offsets, then W_2 .. W_L (padded), b_1 .. b_L and a spare
+  // 16-byte slot
+  constexpr int HSZ = 2 * TS * M_HP;
+  __shared__ __attribute__((aligned(16))) T sm[HSZ + M::WLDS + L * MEDIUM_WIDTH + 16 / sizeof(T)];
+  T(*const hs)[TS][M_HP] = reinterpret_cast<T(*)[TS][M_HP]>(sm);
+  T* const wl = sm + HSZ;
+  T(*const bl)[MEDIUM_WIDTH] = reinterpret_cast<T(*)[MEDIUM_WIDTH]>(sm + HSZ + M::WLDS);
+  float4* const spare = reinterpret_cast<float4*>(sm + HSZ + M::WLDS + L * MEDIUM_WIDTH);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -176,8 +181,15 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
       }
     }
   };
-  load_z(blockIdx.x);
-  load_y(blockIdx.x);
+  // b_1 of this lane's units, kept in registers for every tile
+  T b1r[NJ];
+#pragma unroll
+  for (int jj = 0; jj < NJ; ++jj) {
+    const int u = unit(jj);
+    const bool ok = has_job(jj, d1) && u < d1;
+    const T b = p.bias[0][ok ? u : 0];
+    b1r[jj] = ok ? b : T(0);
+  }
 
   // b_l for LDS, zero past d_l (128 threads, two whole waves, per layer).  The
   // load issues here, with the others; the value goes to LDS after the weight
@@ -191,6 +203,64 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
   const bool bl_ok = bl_mine && bl_u < p.dims[bl_l];
   const T bl_v = p.bias[bl_l - 1][bl_ok ? bl_u : 0];
 
+  T fp[L - 1][NJ][4];  // f'(z_l), l < L
+
+  // ---- layer 1 of tile t: the pieces of z_1 in piece order, + b_1, f_1;
+  // the next tile's pieces are requested once these are summed
+  auto layer1 = [&](int t) {
+    const int s0 = t * TS, rem = p.B - s0;
+    T zs[NJ][4];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        zs[jj][v] = pz[0][jj][v];
+#pragma unroll
+        for (int q = 1; q < M_PF; ++q)
+          if (q < p.np) zs[jj][v] += pz[q][jj][v];
+      }
+    // pieces past those loaded ahead (small batches cut into many pieces)
+    for (int q = M_PF; q < p.np; ++q) {
+      T tq[NJ][4];
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) {
+        if (!has_job(jj, d1)) break;
+        const int u = unit(jj), rw = row(jj);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool ok = u < d1 && rw + RS * v < rem;
+          tq[jj][v] = M::load(zres, ok ? SZ * (unsigned)(rw * ldz + u) : MEDIUM_OOB,
+                              SZ * (unsigned)((s0 + RS * v) * ldz + q * (int)p.zstride));
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) zs[jj][v] += tq[jj][v];
+    }
+    load_z(t + gridDim.x);
+    const __amdgpu_buffer_rsrc_t ares = rsrc(p.A[0]);
+    const int lda = (int)p.lda[0];
+    with_act(p.acts[0], [&](auto act) {
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) {
+        if (!has_job(jj, d1)) break;
+        const int u = unit(jj), rw = row(jj);
+        const unsigned vb = SZ * (unsigned)(rw * lda + u);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool ok = u < d1 && rw + RS * v < rem;
+          T a, f;
+          act_eval(decltype(act)::value, zs[jj][v] + b1r[jj], a, f);
+          a = ok ? a : T(0);
+          M::store(a, ares, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((s0 + RS * v) * lda));
+          hs[0][rw + RS * v][u] = a;
+          fp[0][jj][v] = f;
+        }
+      }
+    });
+  };
+
   // the weights of layers 2..L into LDS: a row is 128 elements, 16 bytes a lane
   // (32 lanes in fp32, 64 in fp64).
   // Staged row R (over the layers' padded rows in order) is row j of layer l;
@@ -199,7 +269,11 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
   // every product below runs over whole 16-unit blocks (the bank padding at
   // the end of each LDS row is never read).  The LDS pitch is 18 mod 32
   // elements, so fp32 rows are 8-byte aligned: each 16-byte load is stored as
-  // two 8-byte halves.
+  // two 8-byte halves.  The first round of these loads (from the L2) issues
+  // before the first tile's layer-1 pieces and targets (from memory): a CU
+  // keeps a bounded number of loads in flight, so weight loads queued behind
+  // them would arrive at their pace.  The weights are stored to LDS while the
+  // pieces are on their way.
   {
     int rend[L];  // staged rows of layers 2..l
     rend[1] = p.wrows[1];
@@ -207,9 +281,9 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
     for (int l = 3; l <= L; ++l) rend[l - 1] = rend[l - 2] + p.wrows[l - 1];
     const int rtot = rend[L - 1];
     const int c = VW * (tid % LPR);
-    for (int R0 = tid / LPR; R0 < rtot; R0 += SROWS * M_STAGE) {
-      typename M::vec16 v[M_STAGE];
-      int dst[M_STAGE];
+    typename M::vec16 v[M_STAGE];
+    int dst[M_STAGE];
+    auto stage_issue = [&](int R0) {
 #pragma unroll
       for (int i = 0; i < M_STAGE; ++i) {
         const int R = R0 + i * SROWS;
@@ -232,124 +306,104 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
         v[i] = ok ? x : typename M::vec16{};
         dst[i] = in ? pick(p.woff[1], p.woff[2], p.woff[3]) + j * wp + c : -1;
       }
-      // rows past the last layer and columns past the padded width go to a
-      // spare slot, so no load is tied to a branch
+    };
+    // rows past the last layer and columns past the padded width go to a
+    // spare slot, so no load is tied to a branch
+    auto stage_store = [&]() {
 #pragma unroll
       for (int i = 0; i < M_STAGE; ++i) {
         if constexpr (sizeof(T) == 4) {
           float2* d = dst[i] >= 0 ? reinterpret_cast<float2*>(wl + dst[i])
-                                  : reinterpret_cast<float2*>(&spare);
+                                  : reinterpret_cast<float2*>(spare);
           d[0] = make_float2(v[i].x, v[i].y);
           d[1] = make_float2(v[i].z, v[i].w);
         } else {
           *(dst[i] >= 0 ? reinterpret_cast<double2*>(wl + dst[i])
-                        : reinterpret_cast<double2*>(&spare)) = v[i];
+                        : reinterpret_cast<double2*>(spare)) = v[i];
         }
       }
+    };
+    stage_issue(tid / LPR);
+    load_z(blockIdx.x);  // the grid has at most one workgroup per tile
+    load_y(blockIdx.x);
+    stage_store();
+    layer1(blockIdx.x);
+    for (int R0 = tid / LPR + SROWS * M_STAGE; R0 < rtot; R0 += SROWS * M_STAGE) {
+      stage_issue(R0);
+      stage_store();
     }
   }
   if (bl_mine) bl[bl_l - 1][bl_u] = bl_ok ? bl_v : T(0);
-  __syncthreads();  // weights and biases in LDS
+  __syncthreads();  // weights, biases and the first tile's a_1 in LDS
 
-  T fp[L - 1][NJ][4];  // f'(z_l), l < L
+  // the product of job jj over K inputs (a multiple of 4, at most the
+  // 16-padded width, past which both sides are zero): lane (r, g) feeds
+  // unit 16 ub + r and tile row 16 sb + r with input k + g.  TR reads the
+  // staged weights transposed (the delta products W^T delta).
+  int cur = 0;
+  auto product = [&](auto tr, int jj, const T* w, int wp, int K) {
+    constexpr bool TR = decltype(tr)::value;
+    typename M::acc_t acc{};
+    const T* h = &hs[cur][sblk(jj) + r][g];
+    const T* wr = TR ? w + g * wp + unit(jj) : w + unit(jj) * wp + g;
+    const int ws = TR ? wp : 1;  // weight stride per input
+    // 32 inputs at a time: all their operands are read, then the products
+    // run (the other waves of the SIMD cover the read latency); then 16,
+    // then single steps of 4
+    const int K32 = K & ~31, K16 = K & ~15;
+    int k = 0;
+    for (; k < K32; k += 32) {
+      T xa[8], wb[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        wb[i] = wr[(k + 4 * i) * ws];
+        xa[i] = h[k + 4 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc = M::mma(xa[i], wb[i], acc);
+      // keep the reads ahead of the products (the scheduler would otherwise
+      // pair each read with its product and wait on it)
+      __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+    if (k < K16) {
+      T xa[4], wb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        wb[i] = wr[(k + 4 * i) * ws];
+        xa[i] = h[k + 4 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = M::mma(xa[i], wb[i], acc);
+    }
+    for (int k = K16; k < K; k += 4) acc = M::mma(h[k], wr[k * ws], acc);
+    return acc;
+  };
+  using fwd_t = std::integral_constant<bool, false>;
+  using bwd_t = std::integral_constant<bool, true>;
+
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int s0 = t * TS, rem = p.B - s0;
-
-    // ---- layer 1: the pieces of z_1 in piece order, + b_1, f_1
-    {
-      T zs[NJ][4];
-#pragma unroll
-      for (int jj = 0; jj < NJ; ++jj)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          zs[jj][v] = pz[0][jj][v];
-#pragma unroll
-          for (int q = 1; q < M_PF; ++q)
-            if (q < p.np) zs[jj][v] += pz[q][jj][v];
-        }
-      // pieces past those loaded ahead (small batches cut into many pieces)
-      for (int q = M_PF; q < p.np; ++q) {
-        T tq[NJ][4];
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, d1)) break;
-          const int u = unit(jj), rw = row(jj);
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const bool ok = u < d1 && rw + RS * v < rem;
-            tq[jj][v] = M::load(zres, ok ? SZ * (unsigned)(rw * ldz + u) : MEDIUM_OOB,
-                                SZ * (unsigned)((s0 + RS * v) * ldz + q * (int)p.zstride));
-          }
-        }
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) zs[jj][v] += tq[jj][v];
-      }
-      load_z(t + gridDim.x);
-      const __amdgpu_buffer_rsrc_t ares = rsrc(p.A[0]);
-      const int lda = (int)p.lda[0];
-      with_act(p.acts[0], [&](auto act) {
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, d1)) break;
-          const int u = unit(jj), rw = row(jj);
-          const unsigned vb = SZ * (unsigned)(rw * lda + u);
-          const T b = bl[0][u];
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const bool ok = u < d1 && rw + RS * v < rem;
-            T a, f;
-            act_eval(decltype(act)::value, zs[jj][v] + b, a, f);
-            a = ok ? a : T(0);
-            M::store(a, ares, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((s0 + RS * v) * lda));
-            hs[0][rw + RS * v][u] = a;
-            fp[0][jj][v] = f;
-          }
-        }
-      });
+    if (t != (int)blockIdx.x) {
+      layer1(t);
+      __syncthreads();
     }
-    __syncthreads();
 
-    // ---- layers 2..L: z_l = W_l a_{l-1} + b_l; at l = L the output delta
-    int cur = 0;
+    // ---- layers 2..L: z_l = W_l a_{l-1} + b_l; at l = L the output delta.
+    // Each job's activation follows its own product, so one wave's
+    // activation arithmetic overlaps the other waves' matrix work.
 #pragma unroll
     for (int l = 2; l <= L; ++l) {
-      const int N = p.dims[l], Kp = (p.dims[l - 1] + 15) & ~15;
+      const int N = p.dims[l], K = (p.dims[l - 1] + 3) & ~3;
       const int wp = p.wp[l - 1];
       const T* w = wl + p.woff[l - 1];
-      typename M::acc_t acc[NJ];
-#pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) acc[jj] = typename M::acc_t{};
-      // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with input
-      // k0 + 4 i + g; inputs past d_{l-1} are zero on both sides up to the
-      // next multiple of 16
-      for (int k0 = 0; k0 < Kp; k0 += 16) {
-        T xa[NJ][4], wb[NJ][4];
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, N)) break;
-          const int xr = sblk(jj) + r;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            wb[jj][i] = w[unit(jj) * wp + k0 + 4 * i + g];
-            xa[jj][i] = hs[cur][xr][k0 + 4 * i + g];
-          }
-        }
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, N)) break;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc[jj] = M::mma(xa[jj][i], wb[jj][i], acc[jj]);
-        }
-      }
       const __amdgpu_buffer_rsrc_t ores = rsrc(l < L ? p.A[l - 1] : p.D[l - 1]);
       const int lda = (int)p.lda[l - 1];
       with_act(p.acts[l - 1], [&](auto act) {
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
           if (!has_job(jj, N)) break;
+          const typename M::acc_t acc = product(fwd_t{}, jj, w, wp, K);
           const int u = unit(jj), rw = row(jj);
           const unsigned vb = SZ * (unsigned)(rw * lda + u);
           const T b = bl[l - 1][u];
@@ -358,7 +412,7 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
             const bool ok = u < N && rw + RS * v < rem;
             const unsigned so = SZ * (unsigned)((s0 + RS * v) * lda);
             T a, f;
-            act_eval(decltype(act)::value, acc[jj][v] + b, a, f);
+            act_eval(decltype(act)::value, acc[v] + b, a, f);
             if (l < L) {
               a = ok ? a : T(0);
               M::store(a, ores, ok ? vb : MEDIUM_OOB, so);
@@ -383,45 +437,21 @@ __global__ void __launch_bounds__(M_THREADS) medium_kernel(const MediumParamsT<T
     // another barrier.
 #pragma unroll
     for (int l = L - 1; l >= 1; --l) {
-      const int N = p.dims[l], Kp = (p.dims[l + 1] + 15) & ~15;
+      const int N = p.dims[l], K = (p.dims[l + 1] + 3) & ~3;
       const int wp = p.wp[l];
       const T* w = wl + p.woff[l];
-      typename M::acc_t acc[NJ];
-#pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) acc[jj] = typename M::acc_t{};
-      // lane (r, g) feeds unit 16 ub + r and tile row 16 sb + r with unit
-      // k0 + 4 i + g of layer l + 1 (zero on both sides past d_{l+1})
-      for (int k0 = 0; k0 < Kp; k0 += 16) {
-        T xa[NJ][4], wb[NJ][4];
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, N)) break;
-          const int xr = sblk(jj) + r;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            wb[jj][i] = w[(k0 + 4 * i + g) * wp + unit(jj)];
-            xa[jj][i] = hs[cur][xr][k0 + 4 * i + g];
-          }
-        }
-#pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) {
-          if (!has_job(jj, N)) break;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc[jj] = M::mma(xa[jj][i], wb[jj][i], acc[jj]);
-        }
-      }
       const __amdgpu_buffer_rsrc_t dres = rsrc(p.D[l - 1]);
       const int lda = (int)p.lda[l - 1];
 #pragma unroll
       for (int jj = 0; jj < NJ; ++jj) {
         if (!has_job(jj, N)) break;
+        const typename M::acc_t acc = product(bwd_t{}, jj, w, wp, K);
         const int u = unit(jj), rw = row(jj);
         const unsigned vb = SZ * (unsigned)(rw * lda + u);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const bool ok = u < N && rw + RS * v < rem;
-          const T d = ok ? acc[jj][v] * fp[l - 1][jj][v] : T(0);
+          const T d = ok ? acc[v] * fp[l - 1][jj][v] : T(0);
           M::store(d, dres, ok ? vb : MEDIUM_OOB, SZ * (unsigned)((s0 + RS * v) * lda));
           if (l > 1) hs[cur ^ 1][rw + RS * v][u] = d;
         }
