@@ -611,6 +611,13 @@ __global__ void __launch_bounds__(SKF_NT) fwd_skinny_kernel(const GemmParamsT<fl
     const int total = p.N * len4;
     const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + kbeg);
     const int ldb = (int)p.ldb;
+    // 16-byte chunk i is row i / len4, 4-float column i % len4.  The quotient
+    // is a multiply-high by floor(2^32 / len4) + 1, exact while i len4 < 2^32
+    // (the slice fits in LDS, so both stay below 2^14).  Chunks past the
+    // slice go to the spare 16 bytes after its rows, so no store is tied to
+    // a branch.
+    const unsigned mq = len4 > 0 ? 0xffffffffu / (unsigned)len4 + 1u : 0u;
+    const int spare = 16 * ((p.N + 15) >> 4) * pk;
     constexpr int BATCH = 16;   // 16-byte loads per thread in flight at once
     for (int i0 = 0; i0 < total; i0 += BATCH * SKF_NT) {
       floatx4 v[BATCH];
@@ -618,13 +625,13 @@ __global__ void __launch_bounds__(SKF_NT) fwd_skinny_kernel(const GemmParamsT<fl
 #pragma unroll
       for (int j = 0; j < BATCH; ++j) {
         const int i = i0 + j * SKF_NT + (int)threadIdx.x;
-        const int u = i / len4, c = i - u * len4;
-        at[j] = i < total ? u * pk + 4 * c : -1;
-        v[j] = sk_load(rb, i < total && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
+        const int u = (int)__umulhi((unsigned)i, mq), c = i - u * len4;
+        const bool in = i < total;
+        at[j] = in ? u * pk + 4 * c : spare;
+        v[j] = sk_load(rb, in && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
       }
 #pragma unroll
-      for (int j = 0; j < BATCH; ++j)
-        if (at[j] >= 0) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
+      for (int j = 0; j < BATCH; ++j) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
     }
     __syncthreads();
   };
@@ -678,7 +685,8 @@ int fwd_skinny_pitch(int sub_len) {
 }
 
 int64_t fwd_skinny_lds_bytes(int N, int sub_len) {
-  return (int64_t)16 * ((N + 15) / 16) * fwd_skinny_pitch(sub_len) * 4;
+  // the slice's rows, padded to 16 units, and a spare 16-byte slot
+  return (int64_t)16 * ((N + 15) / 16) * fwd_skinny_pitch(sub_len) * 4 + 16;
 }
 
 hipError_t launch_dw_skinny_group64(SkinnyGroup64 g, hipStream_t s) {
