@@ -518,17 +518,26 @@ __global__ void __launch_bounds__(SK_NT, 2) skinny_dw64_kernel(const SkinnyGroup
 // in the 4 products of a k-group of 16 inputs.
 //
 // A workgroup of 8 waves owns one piece and 8 blocks of 16 samples.  It
-// first copies the piece's slice of W (every unit, the piece's inputs) into
-// LDS, at a row pitch of 4 (odd) floats so that the 16 rows of a fragment
-// read fall on distinct banks; after that one barrier each wave runs its
-// own sample block: the sample rows come from global memory, SKINNY_FWD_PD
-// k-groups ahead, the unit rows from LDS.
+// copies the piece's slice of W (every unit, the piece's inputs) into LDS,
+// at a row pitch of 4 (odd) floats so that the 16 rows of a fragment read
+// fall on distinct banks, in two parts: the first SKINNY_FWD_PD k-groups
+// (when the piece has at least twice as many), then the rest, whose loads
+// are in flight while the first part's products run.  After each part's
+// barrier every wave runs its own sample block: the sample rows come from
+// global memory, SKINNY_FWD_PD k-groups ahead, the unit rows from LDS.
 // ---------------------------------------------------------------------------
-constexpr int SKF_NT = 512;   // 8 waves
+constexpr int SKF_NT = 512;    // 8 waves
+constexpr int SKF_BATCH = 8;   // 16-byte copy loads per thread in one round
+
+// the 16-byte chunks of one round of the copy: values and LDS offsets
+struct SkfChunks {
+  floatx4 v[SKF_BATCH];
+  int at[SKF_BATCH];
+};
 
 template <int NUB, class Stage>
 __device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int sblk, int piece,
-                                                const float* ws, int pk, Stage&& stage) {
+                                                const float* ws, int pk, Stage& stage) {
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, gq = lane >> 4;
   const int M = p.M, N = p.N;
@@ -561,16 +570,35 @@ __device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int
       for (int u = 0; u < NUB; ++u)
         acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[tt], wv[u][tt], acc[u], 0, 0, 0);
   };
-  // the sample rows' first k-groups are requested before the W slice, so
-  // their latency passes while the slice is copied
   constexpr int PD = SKINNY_FWD_PD;
   const bool has_rows = s0 < M;
+  // the copy's split: k-groups [0, hs) first, 4 hs chunk columns
+  const int hs = ngr >= 2 * PD ? PD : 0;
+  // the first part's loads (from the L2) issue before the sample rows' (from
+  // memory), so that they are not queued behind them; the second part's
+  // first round follows the sample rows
+  SkfChunks g1, g2;
+  stage.issue(g1, 0, 4 * hs, 0);
   floatx4 xv[PD];
 #pragma unroll
   for (int d = 0; d < PD; ++d) xv[d] = load(d);
-  stage();
-  if (!has_rows) return;
+  stage.issue(g2, 4 * hs, 4 * ngr, 0);
+  stage.store(g1);
+  stage.copy(0, 4 * hs, 1);
+  __syncthreads();
   int t = 0;
+  if (has_rows && hs == PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      step(xv[d], d);
+      xv[d] = load(d + PD);
+    }
+    t = PD;
+  }
+  stage.store(g2);
+  stage.copy(4 * hs, 4 * ngr, 1);
+  __syncthreads();
+  if (!has_rows) return;
   for (; t + PD <= ngr; t += PD) {
 #pragma unroll
     for (int d = 0; d < PD; ++d) {
@@ -593,48 +621,66 @@ __device__ __forceinline__ void fwd_skinny_tile(const GemmParamsT<float>& p, int
     }
 }
 
+// The copy of a piece's slice of W: row u, inputs kbeg .. kend - 1 at
+// ws[u * pk + ..], zeros up to the end of the last k-group (their products
+// meet the zeros that the sample loads past kend return).  A part of it is
+// the chunk columns [c0, c1) (4 floats each) of every row: chunk i of the
+// part is row i / w, column c0 + i % w with w = c1 - c0, the quotient a
+// multiply-high by floor(2^32 / w) + 1, exact while i w < 2^32 (the slice
+// fits in LDS, so both stay below 2^14).  Chunks past the part go to the
+// spare 16 bytes after the slice's rows, so no store is tied to a branch.
+struct SkfStage {
+  const GemmParamsT<float>& p;
+  float* ws;
+  int pk, kbeg, kend, spare, ldb;
+  __amdgpu_buffer_rsrc_t rb;
+
+  __device__ SkfStage(const GemmParamsT<float>& p_, float* ws_, int pk_, int piece) : p(p_), ws(ws_), pk(pk_) {
+    kbeg = piece * p.sub_len;
+    kend = min(kbeg + p.sub_len, p.K);
+    spare = 16 * ((p.N + 15) >> 4) * pk;
+    ldb = (int)p.ldb;
+    rb = sk_rsrc(p.B + kbeg);
+  }
+  __device__ int rounds(int c0, int c1) const {
+    const int total = p.N * (c1 - c0);
+    return total > 0 ? (total + SKF_BATCH * SKF_NT - 1) / (SKF_BATCH * SKF_NT) : 0;
+  }
+  // round q of the part's loads
+  __device__ void issue(SkfChunks& g, int c0, int c1, int q) const {
+    const int w = c1 - c0, total = p.N * w;
+    const unsigned mq = w > 0 ? 0xffffffffu / (unsigned)w + 1u : 0u;
+#pragma unroll
+    for (int j = 0; j < SKF_BATCH; ++j) {
+      const int i = (q * SKF_BATCH + j) * SKF_NT + (int)threadIdx.x;
+      const int u = (int)__umulhi((unsigned)i, mq), c = c0 + i - u * w;
+      const bool in = i < total;
+      g.at[j] = in ? u * pk + 4 * c : spare;
+      g.v[j] = sk_load(rb, in && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
+    }
+  }
+  __device__ void store(const SkfChunks& g) const {
+#pragma unroll
+    for (int j = 0; j < SKF_BATCH; ++j) *reinterpret_cast<floatx4*>(ws + g.at[j]) = g.v[j];
+  }
+  // rounds from q0 on, each loaded and stored in turn
+  __device__ void copy(int c0, int c1, int q0) const {
+    const int nq = rounds(c0, c1);
+    for (int q = q0; q < nq; ++q) {
+      SkfChunks g;
+      issue(g, c0, c1, q);
+      store(g);
+    }
+  }
+};
+
 __global__ void __launch_bounds__(SKF_NT) fwd_skinny_kernel(const GemmParamsT<float> p, int pk) {
   extern __shared__ floatx4 ws4[];
   float* ws = reinterpret_cast<float*>(ws4);
   // workgroup b: piece b % nsub, sample blocks 8 (b / nsub) .. + 7
   const int piece = blockIdx.x % p.nsub;
   const int sblk = 8 * (blockIdx.x / p.nsub) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-
-  // copy of the piece's slice of W: row u, inputs kbeg .. kend - 1 at
-  // ws[u * pk + ..], zeros up to the end of the last k-group (their products
-  // meet the zeros that the sample loads past kend return); every wave takes
-  // part, and the barrier ends it
-  auto stage = [&] {
-    const int kbeg = piece * p.sub_len;
-    const int kend = min(kbeg + p.sub_len, p.K);
-    const int len4 = 4 * ((kend - kbeg + 15) >> 4);
-    const int total = p.N * len4;
-    const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + kbeg);
-    const int ldb = (int)p.ldb;
-    // 16-byte chunk i is row i / len4, 4-float column i % len4.  The quotient
-    // is a multiply-high by floor(2^32 / len4) + 1, exact while i len4 < 2^32
-    // (the slice fits in LDS, so both stay below 2^14).  Chunks past the
-    // slice go to the spare 16 bytes after its rows, so no store is tied to
-    // a branch.
-    const unsigned mq = len4 > 0 ? 0xffffffffu / (unsigned)len4 + 1u : 0u;
-    const int spare = 16 * ((p.N + 15) >> 4) * pk;
-    constexpr int BATCH = 16;   // 16-byte loads per thread in flight at once
-    for (int i0 = 0; i0 < total; i0 += BATCH * SKF_NT) {
-      floatx4 v[BATCH];
-      int at[BATCH];
-#pragma unroll
-      for (int j = 0; j < BATCH; ++j) {
-        const int i = i0 + j * SKF_NT + (int)threadIdx.x;
-        const int u = (int)__umulhi((unsigned)i, mq), c = i - u * len4;
-        const bool in = i < total;
-        at[j] = in ? u * pk + 4 * c : spare;
-        v[j] = sk_load(rb, in && kbeg + 4 * c < kend ? 4u * (unsigned)(u * ldb + 4 * c) : SK_OOB);
-      }
-#pragma unroll
-      for (int j = 0; j < BATCH; ++j) *reinterpret_cast<floatx4*>(ws + at[j]) = v[j];
-    }
-    __syncthreads();
-  };
+  SkfStage stage(p, ws, pk, piece);
   switch ((p.N + 15) >> 4) {
     case 1: fwd_skinny_tile<1>(p, sblk, piece, ws, pk, stage); break;
     case 2: fwd_skinny_tile<2>(p, sblk, piece, ws, pk, stage); break;
