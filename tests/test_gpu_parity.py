@@ -169,8 +169,11 @@ def test_medium_edges(dims, acts, batch, shards, eta):
 # 97, 100, 113, 127, 128), input tiles with tails of one to four blocks (20,
 # 36, 49, 97, 113, 788), the layer-1 forward over k pieces whose last piece is
 # short (788) or a single piece off a whole k-group (20, 36), shards of a
-# few samples (160 in 16: fewer k-steps than waves in a workgroup), and
-# layers in one launch with both one and several sub-pieces per shard
+# few samples (160 in 16: fewer k-steps than waves in a workgroup), layers
+# in one launch with both one and several sub-pieces per shard, and 784
+# inputs into 128 units at 10000 samples: three pieces, whose W slices the
+# forward copies in two parts (the second in two rounds of loads) for the
+# 17-group pieces and in one part for the 15-group last one
 SKINNY_EDGES = [
     ((20, 113, 49, 10), ("tanh", "sigmoid", "sigmoid"), 500, 4, 0.5),
     ((36, 128, 97, 33), ("sigmoid", "tanh", "gaussian"), 333, 3, 0.5),
@@ -178,6 +181,7 @@ SKINNY_EDGES = [
     ((64, 64, 127, 100), ("tanh",), 2000, 2, 0.5),
     ((100, 127, 64), ("sigmoid",), 160, 16, 2.0),
     ((52, 97, 10), ("gaussian", "sigmoid"), 6000, 1, 0.5),
+    ((784, 128, 10), ("tanh", "sigmoid"), 10000, 1, 0.5),
 ]
 
 
